@@ -1,0 +1,173 @@
+"""Seeded synthetic inputs for the BART sweep: predictors, binning, response and
+prior hyperparameters.
+
+This module holds no part of the MCMC arithmetic.  It produces the binned
+predictor matrix, the centred response and the hyperparameters that both the
+HIP path and the CPU oracle take as inputs, so the two sides start from
+identical data.
+
+* Predictors are replaced by their index in the splitting grid, 1 byte each
+  (sec. 3.2 "Predictors"): ``x_b = #{k : c_k <= x}`` in ``[0, K_a]``, so that
+  "go right iff ``x_b >= s``" means ``x >= c_s`` (Algorithm 1).
+* Grids (sec. 2.1 "Hyperparameters"): ``K`` evenly spaced cuts strictly inside
+  the data range, or ``K`` empirical quantiles.
+* Hyperparameter defaults (sec. 2.1): ``mu_mu = 0`` for centred data, ``sigma_mu``
+  from the data range, ``nu = 3``, ``lambda`` from the data variance.  The paper
+  only says "some measure of location and scale"; the readings used here are
+  listed with the design notes.
+
+Each predictor column is drawn from its own counter-seeded numpy generator
+(``default_rng([2410, 23244, config, column])``), so columns can be generated
+and binned one at a time and the 10^7-row workload never holds its fp32
+matrix whole.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+SEED_BASE = (2410, 23244)
+
+# The five synthetic workloads: (n, p, n_tree, depth D, sweeps, cut grid,
+# number of cuts, response generator, noise sd, index-cache bytes).
+WORKLOADS = {
+    1: dict(n=1_000, p=10, m=50, D=6, sweeps=100, grid="uniform", K=100, gen="sin5",
+            noise=0.5, idx_bytes=1),
+    2: dict(n=100_000, p=100, m=200, D=6, sweeps=1000, grid="quantile", K=255, gen="sin10x",
+            noise=1.0, idx_bytes=1),
+    3: dict(n=1_000_000, p=100, m=200, D=6, sweeps=1000, grid="quantile", K=255,
+            gen="sin10x", noise=1.0, idx_bytes=1),
+    4: dict(n=10_000_000, p=100, m=200, D=6, sweeps=200, grid="quantile", K=255,
+            gen="sin10x", noise=1.0, idx_bytes=2),
+    5: dict(n=1_000_000, p=1000, m=1000, D=8, sweeps=200, grid="quantile", K=255,
+            gen="sin10x", noise=1.0, idx_bytes=1),
+}
+
+
+@dataclass
+class Hyper:
+    alpha: float = 0.95
+    beta: float = 2.0
+    mu_mu: float = 0.0
+    sigma_mu: float = 1.0
+    nu: float = 3.0
+    lam: float = 1.0
+    sigma2_init: float = 1.0
+    p_grow: float = 0.5
+
+
+@dataclass
+class Inputs:
+    config: int
+    n: int
+    p: int
+    m: int
+    D: int
+    idx_bytes: int
+    sweeps: int
+    X_b: np.ndarray            # uint8 [p][n]
+    n_cuts: np.ndarray         # int32 [p]
+    y_c: np.ndarray            # float32 [n], centred response
+    offset: float              # mean of y (fp64), added back by predict
+    hyper: Hyper = field(default_factory=Hyper)
+    seed: int = 0
+
+    @property
+    def workload(self) -> str:
+        return (f"bart_sweep_n{self.n}_p{self.p}_ntree{self.m}_D{self.D}"
+                f"_idx{8 * self.idx_bytes}")
+
+
+def column(config: int, a: int, n: int) -> np.ndarray:
+    """Predictor column a, U[0,1) in fp32."""
+    return np.random.default_rng([*SEED_BASE, config, a]).random(n, dtype=np.float32)
+
+
+def cutpoints(x: np.ndarray, K: int, grid: str) -> np.ndarray:
+    x = np.asarray(x, dtype=np.float64)
+    if grid == "uniform":
+        lo, hi = float(x.min()), float(x.max())
+        return lo + np.arange(1, K + 1, dtype=np.float64) * (hi - lo) / (K + 1)
+    if grid == "quantile":
+        return np.quantile(x, np.arange(1, K + 1, dtype=np.float64) / (K + 1))
+    raise ValueError(grid)
+
+
+def bin_column(x: np.ndarray, cuts: np.ndarray) -> np.ndarray:
+    """x_b = #{k : c_k <= x}."""
+    xb = np.searchsorted(cuts, np.asarray(x, dtype=np.float64), side="right")
+    assert xb.max(initial=0) <= 255
+    return xb.astype(np.uint8)
+
+
+def _response(gen: str, cols: dict, n: int) -> np.ndarray:
+    if gen == "sin5":
+        return sum(np.sin(2.0 * np.pi * cols[j].astype(np.float64)) for j in range(5))
+    if gen == "sin10x":
+        f = sum(np.sin(2.0 * np.pi * cols[j].astype(np.float64)) for j in range(10))
+        return f + 0.5 * cols[10].astype(np.float64) * cols[11].astype(np.float64)
+    raise ValueError(gen)
+
+
+def default_hyper(y: np.ndarray, m: int, nu: float = 3.0, alpha: float = 0.95,
+                  beta: float = 2.0) -> Hyper:
+    """Defaults for centred y: sigma_mu puts the range of y at +-2 prior sd of
+    the sum of m leaves; lambda puts the data variance at the 0.9 quantile of
+    the sigma^2 prior; sigma^2 starts at the data variance."""
+    from scipy.stats import chi2
+
+    y = np.asarray(y, dtype=np.float64)
+    s2 = float(np.var(y))
+    rng = float(y.max() - y.min()) if y.size else 1.0
+    sigma_mu = rng / (2.0 * 2.0 * math.sqrt(m)) if rng > 0 else 1.0
+    lam = s2 * float(chi2.ppf(0.1, nu)) / nu if s2 > 0 else 1.0
+    return Hyper(alpha=alpha, beta=beta, mu_mu=0.0, sigma_mu=sigma_mu, nu=nu, lam=lam,
+                 sigma2_init=s2 if s2 > 0 else 1.0)
+
+
+def make_inputs(config: int, n: int | None = None, p: int | None = None,
+                m: int | None = None, D: int | None = None,
+                idx_bytes: int | None = None) -> Inputs:
+    """Inputs of one workload; n, p, m, D may be overridden to get a smaller
+    case of the same generator (the seeds of the columns do not change)."""
+    w = dict(WORKLOADS[config])
+    n = int(n if n is not None else w["n"])
+    p = int(p if p is not None else w["p"])
+    m = int(m if m is not None else w["m"])
+    D = int(D if D is not None else w["D"])
+    idx_bytes = int(idx_bytes if idx_bytes is not None else w["idx_bytes"])
+    needed = 5 if w["gen"] == "sin5" else 12
+    X_b = np.empty((p, n), np.uint8)
+    n_cuts = np.empty(p, np.int32)
+    cols = {}
+    for a in range(p):
+        x = column(config, a, n)
+        if a < needed:
+            cols[a] = x
+        cuts = cutpoints(x, w["K"], w["grid"])
+        X_b[a] = bin_column(x, cuts)
+        n_cuts[a] = w["K"]
+    for a in range(p, needed):  # informative columns beyond p (tiny test shapes)
+        cols[a] = column(config, a, n)
+    f = _response(w["gen"], cols, n)
+    noise = np.random.default_rng([*SEED_BASE, config, 10**6]).standard_normal(n) * w["noise"]
+    y = f + noise
+    offset = float(y.mean()) if n else 0.0
+    y_c = (y - offset).astype(np.float32)
+    hyper = default_hyper(y - offset, m)
+    return Inputs(config=config, n=n, p=p, m=m, D=D, idx_bytes=idx_bytes, sweeps=w["sweeps"],
+                  X_b=X_b, n_cuts=n_cuts, y_c=y_c, offset=offset, hyper=hyper, seed=config)
+
+
+def timing_dgp(n: int, p: int) -> tuple[np.ndarray, np.ndarray]:
+    """The paper's own timing data (sec. 4.1, "Data generating process"):
+    y_i = cos(2 n pi/32 (i-1)/(n-1)), X_ij = (i + (p+1) j) mod 256 with 1-based
+    i, j; X is already an index in a 255-cut grid."""
+    i = np.arange(1, n + 1, dtype=np.int64)
+    X_b = np.empty((p, n), np.uint8)
+    for j in range(1, p + 1):
+        X_b[j - 1] = ((i + (p + 1) * j) % 256).astype(np.uint8)
+    y = np.cos(2.0 * n * np.pi / 32.0 * (i - 1) / max(n - 1, 1))
+    return X_b, y
