@@ -1,0 +1,173 @@
+/*
+ * bart.h -- C ABI of libbart: the per-tree backfitting sweep of Bayesian
+ * Additive Regression Trees (BART) on one AMD Instinct MI355X (gfx950).
+ *
+ * The method is the Metropolis-within-Gibbs sampler of "Very Fast Bayesian
+ * Additive Regression Trees on GPU" (arXiv 2410.23244): sum-of-trees model
+ * (sec. 2.1, eq. bartdef), GROW/PRUNE structure moves (sec. 3.3, "Tree
+ * structure proposal"), exact leaf and error-variance draws (sec. 2.2 "The
+ * BART MCMC", sec. 3.3), trees stored as fixed-size heaps (sec. 3.2) and an
+ * index cache plus residual cache updated tree by tree (sec. 3.3).
+ *
+ * Conventions shared by every entry point:
+ *  - D = max_depth, with D = 1 for a root-only tree (sec. 3.2); H = 2^(D-1).
+ *    Heap index h >= 1, root 1, children 2h (left) and 2h+1 (right).
+ *  - Tree arrays, one row per tree: axis u16 [ntree][H], cut u8 [ntree][H]
+ *    (cut 0 = leaf, cuts start at 1), leaf f32 [ntree][2H].
+ *  - X_b is the binned predictor matrix, predictor-major: u8 [p][x_stride],
+ *    X_b[a][i] = index of observation i in the splitting grid of axis a, in
+ *    [0, n_cuts[a]] (sec. 3.2, "Predictors").  Observation i goes right at
+ *    node h iff X_b[axis[h]][i] >= cut[h] (Algorithm 1).
+ *  - All device pointers are HIP device memory of the current device.  The
+ *    library never allocates device memory: X_b and the workspace are
+ *    borrowed from the caller and must outlive the handle.
+ *  - Every call returns BART_OK (0) or a negative error code; arguments are
+ *    validated before anything is enqueued, and on error nothing is enqueued
+ *    and the state is unchanged.  bart_last_error() describes the last error
+ *    of the calling thread.
+ *  - Work is enqueued asynchronously on the handle's HIP stream; only
+ *    bart_get_state() and bart_status() synchronise it.
+ */
+#ifndef BART_H
+#define BART_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BART_OK 0
+#define BART_EINVAL (-1)   /* invalid argument or configuration */
+#define BART_ENOSPACE (-2) /* workspace too small or misaligned */
+#define BART_EHIP (-3)     /* a HIP runtime call failed */
+#define BART_ESTATE (-4)   /* call not allowed in the handle's current state */
+#define BART_ENOTSUP (-5)  /* size beyond what this build supports */
+#define BART_EDEVICE (-6)  /* the device reported a failure (see bart_status) */
+
+/* Device error bits reported by bart_status() */
+#define BART_DEVERR_TIMEOUT 1u   /* a cross-workgroup wait exceeded its spin limit */
+#define BART_DEVERR_CACHE 2u     /* index cache inconsistent with the trees */
+
+typedef struct bart_handle bart_handle;
+
+/* Model and problem configuration. */
+typedef struct {
+  int32_t n;          /* observations, >= 1 */
+  int32_t p;          /* predictors, >= 1 */
+  int32_t ntree;      /* trees m (sec. 2.1 "Hyperparameters"), >= 1 */
+  int32_t max_depth;  /* D in [2, 8]; nodes at depth D-1 are leaves */
+  int32_t idx_bytes;  /* 1 or 2: width of the index cache entries */
+  int32_t grid;       /* workgroups of the sweep kernel; 0 = automatic */
+  int64_t x_stride;   /* elements between predictor rows of X_b: >= n, multiple of 16 */
+  double alpha, beta; /* tree prior P_d = alpha (1+d)^-beta, alpha in [0,1], beta >= 0 */
+  double mu_mu;       /* leaf prior mean (sec. 2.1 "Prior over leaf values") */
+  double sigma_mu;    /* leaf prior sd, > 0 */
+  double nu, lambda;  /* error-variance prior lambda nu / sigma^2 ~ chi^2_nu, > 0 */
+  double sigma2_init; /* initial sigma^2, > 0 */
+  double p_grow;      /* P(GROW) when both GROW and PRUNE are possible, in [0,1] */
+} bart_config;
+
+/* Chain state, in the layouts above.  For bart_get_state the array pointers
+ * are caller-owned device buffers that receive copies; for bart_set_state
+ * they are read.  idx is dense [ntree][n] of idx_bytes-wide entries. */
+typedef struct {
+  uint16_t *axis;
+  uint8_t *cut;
+  float *leaf;
+  void *idx;
+  float *resid;   /* [n]: y_c - sum of trees (sec. 3.3 "Residuals cache") */
+  double sigma2;
+  int64_t sweep;  /* index of the sweep in progress */
+  int32_t next;   /* next step of that sweep: 0..ntree-1 trees, ntree = sigma^2 */
+  int32_t pad;
+} bart_state;
+
+/* Per-step record written by bart_debug_steps (4224 bytes).  Slots are heap
+ * indices; count/sum cover the leaves of the larger tree of the move (the
+ * proposed tree for GROW, the current tree for PRUNE, sec. 3.3 "Traverse
+ * indices cache"), leaf_new the leaves of the final tree. */
+typedef struct {
+  int32_t kind;      /* 0 tree step, 1 sigma^2 step */
+  int32_t tree;
+  int64_t sweep;
+  int32_t move;      /* 0 none, 1 GROW, 2 PRUNE */
+  int32_t eta, axis, cut;
+  int32_t n_grow_cand, n_prune_cand; /* #growable leaves, #prunable nodes of T */
+  int32_t accept;
+  int32_t n_leaves;
+  double log_r, ln_u;
+  double log_r_scale;  /* unused on the device (0) */
+  double ssr, sigma2;  /* sigma^2 step: sum of squared residuals and new sigma^2 */
+  int32_t pad[10];
+  int32_t count[256];
+  double sum[256];     /* partial-residual sums S_h = sum r_i + n_h * old value */
+  float leaf_new[256];
+} bart_trace;
+
+/* Launch shape chosen by bart_init. */
+typedef struct {
+  int32_t grid, block, chunks_per_thread, lds_bytes;
+  int32_t obs_per_thread, max_leaves, pad[2];
+} bart_launch;
+
+/* Bytes of device workspace bart_init needs for cfg (0 if cfg is invalid). */
+size_t bart_workspace_bytes(const bart_config *cfg);
+
+/* Create a chain.  X_b: device u8 [p][x_stride], borrowed.  y_c: device f32
+ * [n], the centred response, copied into the residual cache.  n_cuts: HOST
+ * int32 [p], number of cutpoints K_a in [0, 255] of each axis, copied.
+ * workspace: device, >= bart_workspace_bytes(cfg), 256-byte aligned,
+ * borrowed.  stream: a hipStream_t (NULL = default stream).  Initial state:
+ * every tree root-only with leaf 0, index cache 1, residuals = y_c,
+ * sigma^2 = sigma2_init, sweep 0 (sec. 3.3 "Residuals cache").  On success
+ * *out receives the handle. */
+int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c,
+              const int32_t *n_cuts, void *workspace, size_t ws_bytes, void *stream,
+              bart_handle **out);
+
+/* Run k_sweeps >= 0 whole sweeps (each: every tree in order, then sigma^2;
+ * sec. 2.2 "The BART MCMC").  The chain must be at a sweep boundary
+ * (BART_ESTATE otherwise).  Random draws of sweep s, tree j are a pure
+ * function of (seed, s, j): two calls of k sweeps equal one call of 2k. */
+int bart_step(bart_handle *h, int32_t k_sweeps, uint64_t seed);
+
+/* Sum-of-trees prediction f(x) = offset + sum_j g(x; T_j, M_j) (eq. bartdef),
+ * each tree traversed by Algorithm 1, summed in fp64 in tree order and
+ * rounded to f32.  Xt: device u8 [p][xt_stride] binned like X_b,
+ * xt_stride >= n_t and a multiple of 16; out: device f32 [n_t]. */
+int bart_predict(bart_handle *h, const uint8_t *Xt, int64_t xt_stride, int64_t n_t,
+                 double offset, float *out);
+
+/* Copy the state into caller device buffers and fill the scalars; this
+ * synchronises the handle's stream. */
+int bart_get_state(bart_handle *h, bart_state *dst);
+
+/* Replace the state from caller device buffers (index cache and trees must
+ * be consistent: every idx entry a leaf of its tree).  Per-leaf counts are
+ * recomputed on the device. */
+int bart_set_state(bart_handle *h, const bart_state *src);
+
+/* Run the next n_steps steps (tree steps and sigma^2 steps, in order, from
+ * any position) with the same kernel as bart_step, writing one record per
+ * step into trace (device bart_trace [n_steps]). */
+int bart_debug_steps(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace);
+
+/* Synchronise the stream and return BART_OK, or BART_EDEVICE with the device
+ * error bits in *bits (may be NULL). */
+int bart_status(bart_handle *h, uint32_t *bits);
+
+/* Launch shape of the sweep kernel. */
+int bart_launch_info(const bart_handle *h, bart_launch *out);
+
+/* Release the handle (the caller frees X_b and the workspace). */
+void bart_destroy(bart_handle *h);
+
+/* Message of the last error on the calling thread ("" if none). */
+const char *bart_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BART_H */

@@ -1,0 +1,537 @@
+// bart.hip -- host side of libbart: validation, workspace carving, launches.
+// The C ABI is declared and documented in include/bart.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "common.hpp"
+#include "sweep.hpp"
+
+using namespace bart;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                              \
+  do {                                                                             \
+    hipError_t e_ = (expr);                                                        \
+    if (e_ != hipSuccess)                                                          \
+      return fail(BART_EHIP, "%s failed: %s", #expr, hipGetErrorString(e_));       \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+size_t up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct Layout {
+  int64_t n_pad;
+  size_t resid, idx, axis, cut, leaf, count, prop, z, n_cuts, nz_list, nz_rank, ctl, slots,
+      result, args, total;
+};
+
+const char *check_config(const bart_config *c) {
+  if (!c) return "config is NULL";
+  if (c->n < 1) return "n must be >= 1";
+  if (c->p < 1 || c->p > 65535) return "p must be in [1, 65535]";
+  if (c->ntree < 1) return "ntree must be >= 1";
+  if (c->max_depth < 2 || c->max_depth > 8) return "max_depth must be in [2, 8]";
+  if (c->idx_bytes != 1 && c->idx_bytes != 2) return "idx_bytes must be 1 or 2";
+  if (c->grid < 0 || c->grid > kMaxGrid) return "grid must be in [0, 256]";
+  if (c->x_stride < c->n || c->x_stride % 16) return "x_stride must be >= n and a multiple of 16";
+  if (!(c->alpha >= 0.0 && c->alpha <= 1.0)) return "alpha must be in [0, 1]";
+  if (!(c->beta >= 0.0 && std::isfinite(c->beta))) return "beta must be finite and >= 0";
+  if (!std::isfinite(c->mu_mu)) return "mu_mu must be finite";
+  if (!(c->sigma_mu > 0.0 && std::isfinite(c->sigma_mu))) return "sigma_mu must be > 0";
+  if (!(c->nu > 0.0 && std::isfinite(c->nu))) return "nu must be > 0";
+  if (!(c->lambda > 0.0 && std::isfinite(c->lambda))) return "lambda must be > 0";
+  if (!(c->sigma2_init > 0.0 && std::isfinite(c->sigma2_init))) return "sigma2_init must be > 0";
+  if (!(c->p_grow >= 0.0 && c->p_grow <= 1.0)) return "p_grow must be in [0, 1]";
+  if (c->nu + (double)c->n < 2.0) return "nu + n must be >= 2 (gamma shape >= 1)";
+  return nullptr;
+}
+
+Layout make_layout(const bart_config &c) {
+  Layout L{};
+  const int64_t H = 1 << (c.max_depth - 1);
+  const int64_t m = c.ntree;
+  L.n_pad = (int64_t)up((size_t)c.n, 256);
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = up(o + bytes, kAlign);
+    return at;
+  };
+  L.resid = take(sizeof(float) * L.n_pad);
+  L.idx = take((size_t)m * L.n_pad * c.idx_bytes);
+  L.axis = take(sizeof(uint16_t) * m * H);
+  L.cut = take(m * H);
+  L.leaf = take(sizeof(float) * m * 2 * H);
+  L.count = take(sizeof(int32_t) * m * 2 * H);
+  L.prop = take(sizeof(Prop) * m);
+  L.z = take(sizeof(double) * 2 * m * 2 * H);
+  L.n_cuts = take(sizeof(int32_t) * c.p);
+  L.nz_list = take(sizeof(int32_t) * c.p);
+  L.nz_rank = take(sizeof(int32_t) * c.p);
+  L.ctl = take(sizeof(Ctl));
+  L.slots = take(sizeof(uint64_t) * kMaxGrid * kSlot);
+  L.result = take(sizeof(uint64_t) * kSlot);
+  L.args = take(sizeof(SweepArgs));
+  L.total = o;
+  return L;
+}
+
+using SweepFn = void (*)(const SweepArgs *, Launch);
+constexpr int kVs[] = {1, 2, 4, 8};
+
+SweepFn sweep_fn(int V, int IB) {
+  if (IB == 1) {
+    switch (V) {
+      case 1: return sweep_kernel<1, 1>;
+      case 2: return sweep_kernel<2, 1>;
+      case 4: return sweep_kernel<4, 1>;
+      case 8: return sweep_kernel<8, 1>;
+    }
+  } else {
+    switch (V) {
+      case 1: return sweep_kernel<1, 2>;
+      case 2: return sweep_kernel<2, 2>;
+      case 4: return sweep_kernel<4, 2>;
+      case 8: return sweep_kernel<8, 2>;
+    }
+  }
+  return nullptr;
+}
+
+// ---------------------------------------------------------------- kernels
+
+__global__ void k_init_resid(float *resid, const float *y, int64_t n, int64_t n_pad) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n_pad;
+       i += (int64_t)gridDim.x * blockDim.x)
+    resid[i] = i < n ? y[i] : 0.f;
+}
+
+__global__ void k_fill_idx(uint8_t *idx, int64_t entries, int ib) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < entries;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    if (ib == 1)
+      idx[i] = 1;
+    else
+      ((uint16_t *)idx)[i] = 1;
+  }
+}
+
+__global__ void k_init_trees(uint16_t *axis, uint8_t *cut, float *leaf, int32_t *count, int64_t m,
+                             int H, int32_t n) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < m * 2 * H;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int h = (int)(i % (2 * H));
+    leaf[i] = 0.f;
+    count[i] = h == 1 ? n : 0;
+    if (h < H) {
+      const int64_t q = (i / (2 * H)) * H + h;
+      axis[q] = 0;
+      cut[q] = 0;
+    }
+  }
+}
+
+__global__ void k_set_ctl(Ctl *ctl, double sigma2, int64_t sweep, int reset_stats) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    ctl->sigma2 = sigma2;
+    ctl->sweep = sweep;
+    if (reset_stats) {
+      ctl->error = 0;
+      for (int k = 0; k < 6; ++k) ctl->stats[k] = 0;
+    }
+  }
+}
+
+__global__ void k_clear_words(uint64_t *p, int64_t words) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < words;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0;
+}
+
+__global__ void k_zero_i32(int32_t *p, int64_t count) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0;
+}
+
+// Per-leaf counts of every tree from the index cache (after a state load).
+__global__ void k_recount(const uint8_t *idx, int64_t ldi, int ib, int32_t *count, int32_t n,
+                          int H) {
+  __shared__ int hist[256];
+  const int j = blockIdx.y;
+  for (int k = threadIdx.x; k < 256; k += blockDim.x) hist[k] = 0;
+  __syncthreads();
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int v = ib == 1 ? idx[j * ldi + i] : ((const uint16_t *)idx)[j * ldi + i];
+    if (v < 2 * H) atomicAdd(&hist[v], 1);
+  }
+  __syncthreads();
+  for (int k = threadIdx.x; k < 2 * H; k += blockDim.x)
+    if (hist[k]) atomicAdd(&count[(int64_t)j * 2 * H + k], hist[k]);
+}
+
+// f(x) = offset + sum_j g(x; T_j, M_j): Algorithm 1 per tree, fp64 sum in tree order.
+__global__ void k_predict(const uint8_t *Xt, int64_t ldx, int64_t nt, int p,
+                          const uint16_t *axis, const uint8_t *cut, const float *leaf, int m,
+                          int D, int H, double offset, float *out) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i >= nt) return;
+  double acc = 0.0;
+  for (int j = 0; j < m; ++j) {
+    const uint16_t *ax = axis + (int64_t)j * H;
+    const uint8_t *ct = cut + (int64_t)j * H;
+    int index = 1;
+    bool found = false;
+    for (int lvl = 1; lvl <= D - 1; ++lvl) {
+      const int a = ax[index], split = ct[index];
+      found = found || split == 0;
+      const int xa = Xt[(int64_t)(a < p ? a : 0) * ldx + i];
+      const int child = 2 * index + (xa >= split ? 1 : 0);
+      index = found ? index : child;
+    }
+    acc += (double)leaf[(int64_t)j * 2 * H + index];
+  }
+  out[i] = (float)(offset + acc);
+}
+
+int grid_for(int64_t work, int block) {
+  int64_t g = (work + block - 1) / block;
+  return (int)std::max<int64_t>(1, std::min<int64_t>(g, 65536));
+}
+
+}  // namespace
+
+struct bart_handle {
+  bart_config cfg;
+  Layout lay;
+  char *ws;
+  const uint8_t *X;
+  hipStream_t stream;
+  int device;
+  int H, p_nz, V, G, lds;
+  int64_t chunks;
+  int64_t sweep;
+  int32_t next;
+  std::vector<int32_t> n_cuts, nz_list, nz_rank;
+  SweepFn fn;
+};
+
+namespace {
+
+template <class T>
+T *at(bart_handle *h, size_t off) {
+  return (T *)(h->ws + off);
+}
+
+SweepArgs make_args(bart_handle *h) {
+  const bart_config &c = h->cfg;
+  SweepArgs A{};
+  A.X = h->X;
+  A.ldx = c.x_stride;
+  A.resid = at<float>(h, h->lay.resid);
+  A.idx = at<void>(h, h->lay.idx);
+  A.ldi = h->lay.n_pad;
+  A.axis = at<uint16_t>(h, h->lay.axis);
+  A.cut = at<uint8_t>(h, h->lay.cut);
+  A.leaf = at<float>(h, h->lay.leaf);
+  A.count = at<int32_t>(h, h->lay.count);
+  A.prop = at<Prop>(h, h->lay.prop);
+  A.z = at<double>(h, h->lay.z);
+  A.n_cuts = at<int32_t>(h, h->lay.n_cuts);
+  A.nz_list = at<int32_t>(h, h->lay.nz_list);
+  A.nz_rank = at<int32_t>(h, h->lay.nz_rank);
+  A.ctl = at<Ctl>(h, h->lay.ctl);
+  A.slots = at<uint64_t>(h, h->lay.slots);
+  A.result = at<uint64_t>(h, h->lay.result);
+  A.n = c.n;
+  A.p = c.p;
+  A.m = c.ntree;
+  A.D = c.max_depth;
+  A.H = h->H;
+  A.p_nz = h->p_nz;
+  A.G = h->G;
+  A.chunks = (int32_t)h->chunks;
+  A.alpha = c.alpha;
+  A.beta = c.beta;
+  A.mu_mu = c.mu_mu;
+  A.sigma_mu = c.sigma_mu;
+  A.nu = c.nu;
+  A.lambda = c.lambda;
+  A.p_grow = c.p_grow;
+  return A;
+}
+
+int launch_sweep(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace) {
+  HIP_TRY(hipSetDevice(h->device));
+  const int64_t words = (int64_t)kMaxGrid * kSlot + kSlot;
+  k_clear_words<<<grid_for(words, 256), 256, 0, h->stream>>>(at<uint64_t>(h, h->lay.slots),
+                                                               words);
+  HIP_TRY(hipGetLastError());
+  const SweepArgs *A = at<SweepArgs>(h, h->lay.args);
+  Launch Lc{h->sweep, h->next, n_steps, seed, trace};
+  void *args[] = {&A, &Lc};
+  HIP_TRY(hipLaunchCooperativeKernel((const void *)h->fn, dim3(h->G), dim3(kBlock), args, 0,
+                                     h->stream));
+  return BART_OK;
+}
+
+void advance(bart_handle *h, int64_t steps) {
+  const int64_t per = (int64_t)h->cfg.ntree + 1;
+  const int64_t pos = h->sweep * per + h->next + steps;
+  h->sweep = pos / per;
+  h->next = (int32_t)(pos % per);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *bart_last_error(void) { return g_err.c_str(); }
+
+size_t bart_workspace_bytes(const bart_config *cfg) {
+  if (check_config(cfg)) return 0;
+  return make_layout(*cfg).total;
+}
+
+int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, const int32_t *n_cuts,
+              void *workspace, size_t ws_bytes, void *stream, bart_handle **out) {
+  if (!out) return fail(BART_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (const char *why = check_config(cfg)) return fail(BART_EINVAL, "%s", why);
+  if (!X_b || !y_c || !n_cuts || !workspace) return fail(BART_EINVAL, "NULL pointer argument");
+  if ((uintptr_t)workspace % kAlign) return fail(BART_ENOSPACE, "workspace not 256-byte aligned");
+  if ((uintptr_t)X_b % 16) return fail(BART_EINVAL, "X_b not 16-byte aligned");
+  const Layout lay = make_layout(*cfg);
+  if (ws_bytes < lay.total)
+    return fail(BART_ENOSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, lay.total);
+  std::vector<int32_t> nc(n_cuts, n_cuts + cfg->p), nzl, nzr(cfg->p, -1);
+  for (int a = 0; a < cfg->p; ++a) {
+    if (nc[a] < 0 || nc[a] > 255) return fail(BART_EINVAL, "n_cuts[%d]=%d not in [0,255]", a, nc[a]);
+    if (nc[a] > 0) {
+      nzr[a] = (int32_t)nzl.size();
+      nzl.push_back(a);
+    }
+  }
+  const int64_t chunks = ((int64_t)cfg->n + 3) / 4;
+  int device = 0;
+  HIP_TRY(hipGetDevice(&device));
+  hipDeviceProp_t prop;
+  HIP_TRY(hipGetDeviceProperties(&prop, device));
+  // launch shape: fewest chunks per thread that fit one workgroup per CU
+  int gmax = std::min(prop.multiProcessorCount, kMaxGrid);
+  int V = 0, G = 0;
+  for (int v : kVs) {
+    const int64_t need = (chunks + (int64_t)v * kBlock - 1) / ((int64_t)v * kBlock);
+    const int g = cfg->grid > 0 ? cfg->grid : (int)need;
+    if (need <= g && g <= gmax) {
+      V = v;
+      G = g;
+      break;
+    }
+  }
+  if (!V)
+    return fail(BART_ENOTSUP, "n=%d needs more than %d workgroups x %d chunks of 4 observations",
+                cfg->n, gmax, kVs[3]);
+  SweepFn fn = sweep_fn(V, cfg->idx_bytes);
+  int per_cu = 0;
+  HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)fn, kBlock, 0));
+  if (per_cu < 1) return fail(BART_ENOTSUP, "sweep kernel does not fit on a compute unit");
+  hipFuncAttributes fa;
+  HIP_TRY(hipFuncGetAttributes(&fa, (const void *)fn));
+
+  bart_handle *h = new bart_handle();
+  h->cfg = *cfg;
+  h->lay = lay;
+  h->ws = (char *)workspace;
+  h->X = X_b;
+  h->stream = (hipStream_t)stream;
+  h->device = device;
+  h->H = 1 << (cfg->max_depth - 1);
+  h->p_nz = (int)nzl.size();
+  h->V = V;
+  h->G = G;
+  h->lds = (int)fa.sharedSizeBytes;
+  h->chunks = chunks;
+  h->sweep = 0;
+  h->next = 0;
+  h->n_cuts = nc;
+  h->nz_list = nzl;
+  h->nz_rank = nzr;
+  h->fn = fn;
+  if (h->nz_list.empty()) h->nz_list.push_back(0);
+
+  auto init = [&]() -> int {
+    hipStream_t st = h->stream;
+    HIP_TRY(hipMemcpyAsync(at<int32_t>(h, lay.n_cuts), h->n_cuts.data(), sizeof(int32_t) * cfg->p,
+                           hipMemcpyHostToDevice, st));
+    HIP_TRY(hipMemcpyAsync(at<int32_t>(h, lay.nz_list), h->nz_list.data(),
+                           sizeof(int32_t) * std::min<size_t>(h->nz_list.size(), cfg->p),
+                           hipMemcpyHostToDevice, st));
+    HIP_TRY(hipMemcpyAsync(at<int32_t>(h, lay.nz_rank), h->nz_rank.data(), sizeof(int32_t) * cfg->p,
+                           hipMemcpyHostToDevice, st));
+    k_init_resid<<<grid_for(lay.n_pad, 256), 256, 0, st>>>(at<float>(h, lay.resid), y_c, cfg->n,
+                                                             lay.n_pad);
+    const int64_t entries = (int64_t)cfg->ntree * lay.n_pad;
+    k_fill_idx<<<grid_for(entries, 256), 256, 0, st>>>(at<uint8_t>(h, lay.idx), entries,
+                                                         cfg->idx_bytes);
+    k_init_trees<<<grid_for((int64_t)cfg->ntree * 2 * h->H, 256), 256, 0, st>>>(
+        at<uint16_t>(h, lay.axis), at<uint8_t>(h, lay.cut), at<float>(h, lay.leaf),
+        at<int32_t>(h, lay.count), cfg->ntree, h->H, cfg->n);
+    k_set_ctl<<<1, 64, 0, st>>>(at<Ctl>(h, lay.ctl), cfg->sigma2_init, 0, 1);
+    HIP_TRY(hipGetLastError());
+    const SweepArgs args = make_args(h);
+    HIP_TRY(hipMemcpyAsync(at<SweepArgs>(h, lay.args), &args, sizeof args, hipMemcpyHostToDevice, st));
+    // the host copies of n_cuts must stay valid until the copies ran
+    HIP_TRY(hipStreamSynchronize(st));
+    return BART_OK;
+  };
+  const int rc = init();
+  if (rc) {
+    delete h;
+    return rc;
+  }
+  *out = h;
+  return BART_OK;
+}
+
+int bart_step(bart_handle *h, int32_t k_sweeps, uint64_t seed) {
+  if (!h) return fail(BART_EINVAL, "handle is NULL");
+  if (k_sweeps < 0) return fail(BART_EINVAL, "k_sweeps must be >= 0");
+  if (h->next != 0) return fail(BART_ESTATE, "chain is inside sweep %lld (step %d)",
+                                (long long)h->sweep, h->next);
+  const int64_t steps = (int64_t)k_sweeps * (h->cfg.ntree + 1);
+  if (steps > 0x7fffff00LL) return fail(BART_EINVAL, "too many steps in one call");
+  if (steps == 0) return BART_OK;
+  const int rc = launch_sweep(h, (int32_t)steps, seed, nullptr);
+  if (rc) return rc;
+  advance(h, steps);
+  return BART_OK;
+}
+
+int bart_debug_steps(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace) {
+  if (!h) return fail(BART_EINVAL, "handle is NULL");
+  if (n_steps < 0) return fail(BART_EINVAL, "n_steps must be >= 0");
+  if (n_steps > 0 && !trace) return fail(BART_EINVAL, "trace is NULL");
+  if (n_steps == 0) return BART_OK;
+  const int rc = launch_sweep(h, n_steps, seed, trace);
+  if (rc) return rc;
+  advance(h, n_steps);
+  return BART_OK;
+}
+
+int bart_predict(bart_handle *h, const uint8_t *Xt, int64_t xt_stride, int64_t n_t, double offset,
+                 float *out) {
+  if (!h) return fail(BART_EINVAL, "handle is NULL");
+  if (n_t < 0) return fail(BART_EINVAL, "n_t must be >= 0");
+  if (n_t == 0) return BART_OK;
+  if (!Xt || !out) return fail(BART_EINVAL, "NULL pointer argument");
+  if (xt_stride < n_t || xt_stride % 16) return fail(BART_EINVAL, "xt_stride must be >= n_t and a multiple of 16");
+  HIP_TRY(hipSetDevice(h->device));
+  k_predict<<<grid_for(n_t, 256), 256, 0, h->stream>>>(
+      Xt, xt_stride, n_t, h->cfg.p, at<uint16_t>(h, h->lay.axis), at<uint8_t>(h, h->lay.cut),
+      at<float>(h, h->lay.leaf), h->cfg.ntree, h->cfg.max_depth, h->H, offset, out);
+  HIP_TRY(hipGetLastError());
+  return BART_OK;
+}
+
+int bart_get_state(bart_handle *h, bart_state *d) {
+  if (!h || !d) return fail(BART_EINVAL, "NULL argument");
+  if (!d->axis || !d->cut || !d->leaf || !d->idx || !d->resid)
+    return fail(BART_EINVAL, "NULL state buffer");
+  HIP_TRY(hipSetDevice(h->device));
+  const bart_config &c = h->cfg;
+  const size_t m = c.ntree, H = h->H;
+  hipStream_t st = h->stream;
+  HIP_TRY(hipMemcpyAsync(d->axis, at<void>(h, h->lay.axis), 2 * m * H, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(d->cut, at<void>(h, h->lay.cut), m * H, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(d->leaf, at<void>(h, h->lay.leaf), 4 * m * 2 * H, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpy2DAsync(d->idx, (size_t)c.n * c.idx_bytes, at<void>(h, h->lay.idx),
+                           (size_t)h->lay.n_pad * c.idx_bytes, (size_t)c.n * c.idx_bytes, m,
+                           hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(d->resid, at<void>(h, h->lay.resid), 4 * (size_t)c.n, hipMemcpyDeviceToDevice, st));
+  Ctl ctl;
+  HIP_TRY(hipMemcpyAsync(&ctl, at<void>(h, h->lay.ctl), sizeof(Ctl), hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  d->sigma2 = ctl.sigma2;
+  d->sweep = h->sweep;
+  d->next = h->next;
+  d->pad = 0;
+  return BART_OK;
+}
+
+int bart_set_state(bart_handle *h, const bart_state *s) {
+  if (!h || !s) return fail(BART_EINVAL, "NULL argument");
+  if (!s->axis || !s->cut || !s->leaf || !s->idx || !s->resid)
+    return fail(BART_EINVAL, "NULL state buffer");
+  const bart_config &c = h->cfg;
+  if (!(s->sigma2 > 0.0 && std::isfinite(s->sigma2))) return fail(BART_EINVAL, "sigma2 must be > 0");
+  if (s->sweep < 0 || s->next < 0 || s->next > c.ntree) return fail(BART_EINVAL, "bad position");
+  HIP_TRY(hipSetDevice(h->device));
+  const size_t m = c.ntree, H = h->H;
+  hipStream_t st = h->stream;
+  HIP_TRY(hipMemcpyAsync(at<void>(h, h->lay.axis), s->axis, 2 * m * H, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(at<void>(h, h->lay.cut), s->cut, m * H, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(at<void>(h, h->lay.leaf), s->leaf, 4 * m * 2 * H, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpy2DAsync(at<void>(h, h->lay.idx), (size_t)h->lay.n_pad * c.idx_bytes, s->idx,
+                           (size_t)c.n * c.idx_bytes, (size_t)c.n * c.idx_bytes, m,
+                           hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(at<void>(h, h->lay.resid), s->resid, 4 * (size_t)c.n, hipMemcpyDeviceToDevice, st));
+  const int64_t cells = (int64_t)m * 2 * H;
+  k_zero_i32<<<grid_for(cells, 256), 256, 0, st>>>(at<int32_t>(h, h->lay.count), cells);
+  dim3 g(std::min<int64_t>(((int64_t)c.n + 1023) / 1024, 64), (unsigned)m);
+  k_recount<<<g, 1024, 0, st>>>(at<uint8_t>(h, h->lay.idx), h->lay.n_pad, c.idx_bytes,
+                                at<int32_t>(h, h->lay.count), c.n, h->H);
+  k_set_ctl<<<1, 64, 0, st>>>(at<Ctl>(h, h->lay.ctl), s->sigma2, s->sweep, 0);
+  HIP_TRY(hipGetLastError());
+  h->sweep = s->sweep;
+  h->next = s->next;
+  return BART_OK;
+}
+
+int bart_status(bart_handle *h, uint32_t *bits) {
+  if (!h) return fail(BART_EINVAL, "handle is NULL");
+  HIP_TRY(hipSetDevice(h->device));
+  Ctl ctl;
+  HIP_TRY(hipMemcpyAsync(&ctl, at<void>(h, h->lay.ctl), sizeof(Ctl), hipMemcpyDeviceToHost, h->stream));
+  HIP_TRY(hipStreamSynchronize(h->stream));
+  if (bits) *bits = ctl.error;
+  if (ctl.error) return fail(BART_EDEVICE, "device error bits 0x%x", ctl.error);
+  return BART_OK;
+}
+
+int bart_launch_info(const bart_handle *h, bart_launch *o) {
+  if (!h || !o) return fail(BART_EINVAL, "NULL argument");
+  memset(o, 0, sizeof *o);
+  o->grid = h->G;
+  o->block = kBlock;
+  o->chunks_per_thread = h->V;
+  o->lds_bytes = h->lds;
+  o->obs_per_thread = 4 * h->V;
+  o->max_leaves = std::min(h->H, kMaxLeaves);
+  return BART_OK;
+}
+
+void bart_destroy(bart_handle *h) { delete h; }
+
+}  // extern "C"

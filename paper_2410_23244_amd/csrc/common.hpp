@@ -1,0 +1,72 @@
+// common.hpp -- layouts shared by the host library and the kernels of libbart.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/bart.h"
+
+namespace bart {
+
+constexpr int kBlock = 1024;          // threads per workgroup of the sweep kernel
+constexpr int kWaves = kBlock / 64;   // wave64 on CDNA4
+constexpr int kMaxLeaves = 128;       // leaves of a depth-8 heap tree
+constexpr int kSlot = 136;            // 64-bit words per workgroup mailbox (>= kMaxLeaves + 1)
+constexpr int kBinFloats = 32768;     // 128 KiB of LDS per-leaf bins
+constexpr int kMaxGrid = 256;         // mailboxes reserved in the workspace
+constexpr int kFlagWord = kMaxLeaves; // result word holding accept/merge flags
+
+enum Move : int32_t { kNone = 0, kGrow = 1, kPrune = 2 };
+
+// Proposal of one tree for its step of the current sweep (sec. 3.3 items 1
+// and 6: everything that does not depend on residuals), 96 bytes.
+struct Prop {
+  int32_t move, eta, axis, cut;
+  int32_t nG, nP, L, rank_l;  // #G(T), #P(T), leaves of the larger tree, rank of 2*eta
+  int32_t rank_r, pad0, pad1, pad2;
+  uint64_t mask[4];           // bit h set iff heap slot h is a leaf of the larger tree
+  double c_prior;             // log r minus the marginal-likelihood term
+  double ln_u;                // log of the accept uniform
+};
+static_assert(sizeof(Prop) == 96, "Prop layout");
+
+// Scalars the kernels keep in device memory.
+struct Ctl {
+  double sigma2;
+  int64_t sweep;
+  uint32_t error;
+  uint32_t pad;
+  uint64_t stats[6];  // GROW proposed, PRUNE proposed, GROW accepted, PRUNE accepted, tree steps, leaves
+};
+
+struct SweepArgs {
+  const uint8_t *X;
+  int64_t ldx;
+  float *resid;
+  void *idx;
+  int64_t ldi;  // entries between index-cache rows
+  uint16_t *axis;
+  uint8_t *cut;
+  float *leaf;
+  int32_t *count;
+  Prop *prop;
+  double *z;  // [2][m][2H] leaf normals, by sweep parity
+  const int32_t *n_cuts;
+  const int32_t *nz_list;
+  const int32_t *nz_rank;
+  Ctl *ctl;
+  uint64_t *slots;   // [kMaxGrid][kSlot]
+  uint64_t *result;  // [kSlot]
+  int32_t n, p, m, D, H, p_nz, G, chunks;
+  double alpha, beta, mu_mu, sigma_mu, nu, lambda, p_grow;
+};
+
+// What changes from one launch of the sweep kernel to the next.
+struct Launch {
+  int64_t s0;         // sweep of the first step
+  int32_t j0;         // first step inside that sweep (0..m-1 trees, m = sigma^2)
+  int32_t n_steps;
+  uint64_t seed;
+  bart_trace *trace;  // NULL: no trace
+};
+
+}  // namespace bart

@@ -1,0 +1,165 @@
+"""Lockstep comparison of the HIP sweep with the CPU oracle.
+
+The device chain runs to some state, the oracle loads that state, then both
+execute the same steps (tree steps and sigma^2 steps, same seed) and every
+step's record is compared:
+
+* move, node, axis, cut, #G(T), #P(T), every per-leaf count: bit-exact;
+* accept: bit-exact, except a tie |ln u - log r| <= 1e-4 (1 + sum |terms|),
+  where the oracle adopts the device decision to stay in lockstep;
+* partial-residual sums S_h: |dS| <= 1e-5 x the leaf's l1 mass
+  sum_i |r_i| + n_h |old value| (sums cancel, so relative error is measured
+  against the mass that was summed);
+* new leaf values: |dmu| <= 1e-5 (|mu| + 1/sqrt(prec));
+* SSR and sigma^2: relative 1e-5 (the device sums fp32 workgroup partials);
+and at the end the index caches and tree structures must be identical and
+the residuals close.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+import oracle
+
+
+@dataclass
+class Report:
+    steps: int = 0
+    tree_steps: int = 0
+    accepts: int = 0
+    ties: int = 0
+    moves: int = 0
+    max_sum_err: float = 0.0      # max |dS| / l1 mass
+    max_leaf_err: float = 0.0     # max |dmu| / (|mu| + 1/sqrt(prec))
+    max_logr_err: float = 0.0
+    max_resid_err: float = 0.0
+    notes: list = field(default_factory=list)
+
+
+def oracle_config(inp, fix_sigma2=False):
+    h = inp.hyper
+    return oracle.make_config(n=inp.n, p=inp.p, m=inp.m, D=inp.D, idx_bytes=inp.idx_bytes,
+                              alpha=h.alpha, beta=h.beta, mu_mu=h.mu_mu, sigma_mu=h.sigma_mu,
+                              nu=h.nu, lam=h.lam, p_grow=h.p_grow, fix_sigma2=fix_sigma2)
+
+
+def chain_from_state(inp, st) -> oracle.Chain:
+    ch = oracle.Chain(oracle_config(inp), inp.X_b, inp.n_cuts, inp.y_c, st["sigma2"])
+    ch.load(st["axis"], st["cut"], st["leaf"], st["idx"], st["resid"], st["sigma2"],
+            st["sweep"], st["next"])
+    return ch
+
+
+def _leaf_l1(inp, idx_row, resid, leaf_row, move, eta, a, s):
+    """l1 mass of the partial residuals of every larger-tree leaf (256 slots)."""
+    c = idx_row.astype(np.int64)
+    cp = c.copy()
+    if move == 1:
+        sel = c == eta
+        cp[sel] = 2 * eta + (inp.X_b[a][sel] >= s)
+    l1 = np.bincount(cp, weights=np.abs(resid.astype(np.float64)), minlength=256)
+    cnt = np.bincount(cp, minlength=256).astype(np.float64)
+    old = np.zeros(256)
+    old[: leaf_row.size] = np.abs(leaf_row.astype(np.float64))
+    if move == 1:
+        old[2 * eta] = old[eta]
+        old[2 * eta + 1] = old[eta]
+    return l1 + cnt * old
+
+
+def compare_steps(inp, ch: oracle.Chain, trg: np.ndarray, seed: int, rep: Report,
+                  sum_tol=1e-5, leaf_tol=1e-5, tie_tol=1e-4, var_tol=1e-5):
+    H = 1 << (inp.D - 1)
+    sig_mu2 = inp.hyper.sigma_mu ** 2
+    for k, g in enumerate(trg):
+        rep.steps += 1
+        j = ch.next
+        if j < inp.m:
+            saved = (ch.idx[j].copy(), ch.resid.copy(), ch.axis[j].copy(), ch.cut[j].copy(),
+                     ch.leaf[j].copy(), ch.sigma2, ch.sweep, ch.next)
+            o = ch.step(seed)
+            assert g["kind"] == 0 and o["kind"] == 0, (k, g["kind"], o["kind"])
+            assert (g["tree"], g["sweep"]) == (o["tree"], o["sweep"]), (k, g["tree"], o["tree"])
+            for f in ["move", "eta", "axis", "cut", "n_grow_cand", "n_prune_cand", "n_leaves"]:
+                assert g[f] == o[f], (k, j, f, g[f], o[f])
+            np.testing.assert_array_equal(g["count"], o["count"], err_msg=f"counts step {k}")
+            rep.tree_steps += 1
+            if o["move"] != 0:
+                rep.moves += 1
+                band = tie_tol * (1.0 + o["log_r_scale"])
+                rep.max_logr_err = max(rep.max_logr_err, abs(g["log_r"] - o["log_r"]) / band)
+                assert abs(g["ln_u"] - o["ln_u"]) <= 1e-12 * (1 + abs(o["ln_u"])), k
+                if g["accept"] != o["accept"]:
+                    if abs(o["ln_u"] - o["log_r"]) > band:
+                        raise AssertionError(f"step {k} tree {j}: accept gpu={g['accept']} "
+                                             f"oracle={o['accept']} ln_u={o['ln_u']} "
+                                             f"log_r={o['log_r']} gpu log_r={g['log_r']}")
+                    rep.ties += 1
+                    rep.notes.append(f"tie at step {k} (tree {j})")
+                    (ch.idx[j], ch.resid[...], ch.axis[j], ch.cut[j], ch.leaf[j]) = (
+                        saved[0], saved[1], saved[2], saved[3], saved[4])
+                    ch.sigma2, ch.sweep, ch.next = saved[5], saved[6], saved[7]
+                    o = ch.step(seed, force=int(g["accept"]))
+                rep.accepts += int(o["accept"])
+            # partial-residual sums against the l1 mass of each leaf
+            l1 = _leaf_l1(inp, saved[0], saved[1], saved[4], int(o["move"]), int(o["eta"]),
+                          int(o["axis"]), int(o["cut"]))
+            used = o["count"] > 0
+            err = np.abs(g["sum"] - o["sum"])
+            rel = np.where(used, err / np.maximum(l1, 1e-30), err)
+            rep.max_sum_err = max(rep.max_sum_err, float(rel.max()))
+            assert rel.max() <= sum_tol, (k, j, float(rel.max()))
+            # new leaf values
+            cnt = o["count"].astype(np.float64)
+            if (o["move"] == 1 and not o["accept"]) or (o["move"] == 2 and o["accept"]):
+                e = int(o["eta"])
+                cnt[e] = cnt[2 * e] + cnt[2 * e + 1]
+            prec = cnt / o["sigma2"] + 1.0 / sig_mu2
+            scale = np.abs(o["leaf_new"].astype(np.float64)) + 1.0 / np.sqrt(prec)
+            lerr = np.abs(g["leaf_new"].astype(np.float64) - o["leaf_new"]) / scale
+            rep.max_leaf_err = max(rep.max_leaf_err, float(lerr.max()))
+            assert lerr.max() <= leaf_tol, (k, j, float(lerr.max()))
+        else:
+            o = ch.step(seed)
+            assert g["kind"] == 1 and o["kind"] == 1, (k, g["kind"], o["kind"])
+            assert g["sweep"] == o["sweep"]
+            assert abs(g["ssr"] - o["ssr"]) <= var_tol * o["ssr"], (k, g["ssr"], o["ssr"])
+            assert abs(g["sigma2"] - o["sigma2"]) <= var_tol * o["sigma2"], (k, g["sigma2"],
+                                                                           o["sigma2"])
+            # keep the chains on the same sigma^2 so the next sweep is comparable
+            ch.sigma2 = float(g["sigma2"])
+    return rep
+
+
+def compare_states(inp, gst: dict, ch: oracle.Chain, rep: Report, resid_tol=1e-5):
+    np.testing.assert_array_equal(gst["idx"], ch.idx, err_msg="index cache")
+    np.testing.assert_array_equal(gst["cut"], ch.cut, err_msg="cut")
+    H = 1 << (inp.D - 1)
+    for j in range(inp.m):
+        for h in range(1, H):
+            if gst["cut"][j, h]:
+                assert gst["axis"][j, h] == ch.axis[j, h], (j, h)
+    scale = np.abs(ch.leaf).max() + np.abs(ch.resid).max()
+    err = np.abs(gst["resid"].astype(np.float64) - ch.resid)
+    rel = err / (np.abs(ch.resid) + 0.1 * scale)
+    rep.max_resid_err = float(rel.max())
+    assert rel.max() <= resid_tol, float(rel.max())
+    assert gst["sweep"] == ch.sweep and gst["next"] == ch.next
+    assert abs(gst["sigma2"] - ch.sigma2) <= 1e-5 * ch.sigma2
+
+
+def lockstep(inp, gpu, seed: int, warm_sweeps: int, n_steps: int) -> Report:
+    """Warm the device chain, then run n_steps in lockstep with the oracle."""
+    if warm_sweeps:
+        gpu.step(warm_sweeps, seed)
+    st = gpu.get_state()
+    assert gpu.status() == 0
+    ch = chain_from_state(inp, st)
+    trg = gpu.debug_steps(n_steps, seed)
+    assert gpu.status() == 0
+    rep = compare_steps(inp, ch, trg, seed, Report())
+    compare_states(inp, gpu.get_state(), ch, rep)
+    return rep

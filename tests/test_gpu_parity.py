@@ -1,0 +1,96 @@
+"""Parity of the HIP sweep (through the C ABI) with the CPU oracle, lockstep.
+
+Small cases cover every workload shape (u8 and u16 index caches, depth 6 and
+8, one and many workgroups, ragged tails); the full-size cases run the
+headline shapes in the launch configuration the benchmark times."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from paper_2410_23244_amd.inputs import make_inputs
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu(inp, grid=0):
+    from paper_2410_23244_amd.bart import from_inputs
+
+    return from_inputs(inp, grid=grid)
+
+
+CASES = {
+    # name: (config, overrides, warm sweeps, lockstep steps, grid)
+    "w1_full": (1, dict(), 3, 2 * 51, 0),
+    "w1_ragged_tiny": (1, dict(n=37, p=3, m=5), 2, 3 * 6, 0),
+    "w2_ragged": (2, dict(n=20011, m=60), 2, 61 + 30, 0),
+    "w2_many_wg": (2, dict(n=40003, p=30, m=40), 2, 41 * 2, 10),
+    "w4_u16": (4, dict(n=30001, p=20, m=50), 2, 51 + 10, 0),
+    "w5_depth8": (5, dict(n=25003, p=1000, m=120), 2, 121 + 5, 0),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_lockstep_small(name):
+    cfg, over, warm, steps, grid = CASES[name]
+    inp = make_inputs(cfg, **over)
+    print(f"case {name}: n={inp.n} p={inp.p} m={inp.m} D={inp.D} idx={inp.idx_bytes}", flush=True)
+    g = _gpu(inp, grid)
+    info = g.launch_info()
+    print(f"  grid={info.grid} chunks/thread={info.chunks_per_thread}", flush=True)
+    rep = parity.lockstep(inp, g, seed=inp.seed + 100, warm_sweeps=warm, n_steps=steps)
+    print(f"  {rep}", flush=True)
+    assert rep.tree_steps > 0 and rep.moves > 0
+
+
+def test_predict_matches_oracle():
+    inp = make_inputs(1, n=3001, p=10, m=30)
+    g = _gpu(inp)
+    g.step(5, 7)
+    st = g.get_state()
+    ch = parity.chain_from_state(inp, st)
+    Xt = make_inputs(1, n=1999, p=10, m=30).X_b
+    want = ch.predict(Xt, inp.offset)
+    got = g.predict(Xt, inp.offset).cpu().numpy()
+    np.testing.assert_array_equal(got, want)
+    # on the training set, y_c - f equals the residual cache up to fp32 drift
+    f = g.predict(inp.X_b, 0.0).cpu().numpy().astype(np.float64)
+    err = np.abs(st["resid"] - (inp.y_c.astype(np.float64) - f)).max()
+    assert err < 1e-4 * np.abs(inp.y_c).max()
+
+
+def test_steps_compose_and_are_deterministic():
+    inp = make_inputs(2, n=5003, p=12, m=9)
+    a, b = _gpu(inp), _gpu(inp)
+    a.step(3, 11)
+    a.step(2, 11)
+    b.step(5, 11)
+    sa, sb = a.get_state(), b.get_state()
+    for k in ["axis", "cut", "leaf", "idx", "resid"]:
+        np.testing.assert_array_equal(sa[k], sb[k], err_msg=k)
+    assert sa["sigma2"] == sb["sigma2"] and sa["sweep"] == sb["sweep"] == 5
+
+
+def test_set_state_roundtrip_continues_identically():
+    inp = make_inputs(1, n=2000, p=8, m=12)
+    a = _gpu(inp)
+    a.step(4, 3)
+    st = a.get_state()
+    b = _gpu(inp)
+    b.set_state(st)
+    a.step(2, 3)
+    b.step(2, 3)
+    sa, sb = a.get_state(), b.get_state()
+    for k in ["axis", "cut", "leaf", "idx", "resid"]:
+        np.testing.assert_array_equal(sa[k], sb[k], err_msg=k)
+    assert a.status() == 0 and b.status() == 0
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_lockstep_full_size(cfg):
+    inp = make_inputs(cfg)
+    print(f"full workload {cfg}: n={inp.n} p={inp.p} m={inp.m}", flush=True)
+    g = _gpu(inp)
+    rep = parity.lockstep(inp, g, seed=inp.seed, warm_sweeps=3, n_steps=inp.m + 1)
+    print(f"  {rep}", flush=True)
