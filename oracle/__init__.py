@@ -82,7 +82,7 @@ def lib():
         L.oc_log_ratio.restype = f64
         L.oc_route.argtypes = [i32, vp, vp, vp, i64, i64]
         L.oc_route.restype = i32
-        L.oc_step.argtypes = [P(Config), vp, vp, i64, P(_State), u64, i32, vp]
+        L.oc_step.argtypes = [P(Config), vp, vp, i64, P(_State), u64, i32, vp, vp]
         L.oc_step.restype = C.c_int
         L.oc_run.argtypes = [P(Config), vp, vp, i64, P(_State), u64, i64, vp]
         L.oc_run.restype = C.c_int
@@ -232,12 +232,17 @@ class Chain:
         self.sweep = st.sweep
         self.next = st.next
 
-    def step(self, seed: int, force: int = -1, trace: bool = True):
-        """One step: tree step `next` of the current sweep, or the sigma^2 step."""
+    def step(self, seed: int, force: int = -1, trace: bool = True, adopt=None):
+        """One step: tree step `next` of the current sweep, or the sigma^2 step.
+        force (0/1) and adopt (256 leaf values) are lockstep hooks: the state
+        continues from that decision / those draws; the trace still reports
+        the oracle's own."""
         st = self._state()
         tr = np.zeros(1, TRACE_DTYPE) if trace else None
+        ad = None if adopt is None else np.ascontiguousarray(adopt, dtype=np.float32)
         rc = lib().oc_step(C.byref(self.cfg), _ptr(self.n_cuts), _ptr(self.X), self.X.shape[1],
-                           C.byref(st), seed, force, _ptr(tr) if trace else None)
+                           C.byref(st), seed, force, None if ad is None else _ptr(ad),
+                           _ptr(tr) if trace else None)
         if rc:
             raise RuntimeError(f"oracle step failed ({rc})")
         self._pull(st)

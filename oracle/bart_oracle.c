@@ -467,7 +467,8 @@ int32_t oc_route(int32_t D, const uint16_t *axis, const uint8_t *cut, const uint
 /* One step of the sweep (sec. 2.2 "The BART MCMC", sec. 3.3).          */
 
 static void tree_step(const oc_config *c, const int32_t *n_cuts, const uint8_t *X, int64_t ldx,
-                      oc_state *st, uint64_t seed, int32_t force, oc_trace *tr) {
+                      oc_state *st, uint64_t seed, int32_t force, const float *adopt,
+                      oc_trace *tr) {
   const int32_t H = 1 << (c->D - 1);
   const int32_t j = st->next;
   const uint64_t s = (uint64_t)st->sweep;
@@ -564,8 +565,10 @@ static void tree_step(const oc_config *c, const int32_t *n_cuts, const uint8_t *
     oc_leaf_posterior((double)cnt[h], S[h], st->sigma2, c->mu_mu, c->sigma_mu, &mean, &prec);
     double z = oc_normal(seed, s, (uint64_t)j, (uint64_t)h);
     fresh[h] = (float)(mean + z / sqrt(prec));
-    leaf[h] = fresh[h];
     if (tr) tr->leaf_new[h] = fresh[h];
+    /* lockstep hook: carry on from another implementation's draws */
+    if (adopt) fresh[h] = adopt[h];
+    leaf[h] = fresh[h];
   }
 
   /* 8: residual cache and index cache (sec. 3.3 items 11, "Residuals cache") */
@@ -601,10 +604,10 @@ static void sigma_step(const oc_config *c, oc_state *st, uint64_t seed, oc_trace
 }
 
 int oc_step(const oc_config *c, const int32_t *n_cuts, const uint8_t *X, int64_t ldx,
-            oc_state *st, uint64_t seed, int32_t force, oc_trace *trace) {
+            oc_state *st, uint64_t seed, int32_t force, const float *adopt, oc_trace *trace) {
   if (c->D < 2 || c->D > 8 || st->next < 0 || st->next > c->m) return -1;
   if (st->next < c->m) {
-    tree_step(c, n_cuts, X, ldx, st, seed, force, trace);
+    tree_step(c, n_cuts, X, ldx, st, seed, force, adopt, trace);
     st->next += 1;
   } else {
     sigma_step(c, st, seed, trace);
@@ -617,7 +620,7 @@ int oc_step(const oc_config *c, const int32_t *n_cuts, const uint8_t *X, int64_t
 int oc_run(const oc_config *c, const int32_t *n_cuts, const uint8_t *X, int64_t ldx,
            oc_state *st, uint64_t seed, int64_t n_steps, oc_trace *traces) {
   for (int64_t k = 0; k < n_steps; k++) {
-    int rc = oc_step(c, n_cuts, X, ldx, st, seed, -1, traces ? traces + k : NULL);
+    int rc = oc_step(c, n_cuts, X, ldx, st, seed, -1, NULL, traces ? traces + k : NULL);
     if (rc) return rc;
   }
   return 0;

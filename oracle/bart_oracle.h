@@ -91,8 +91,13 @@ double oc_log_ratio(const oc_config *c, const int32_t *n_cuts, const uint8_t *X,
                     int32_t eta, int32_t a, int32_t s, double *scale);
 int32_t oc_route(int32_t D, const uint16_t *axis, const uint8_t *cut, const uint8_t *X,
                  int64_t ldx, int64_t i);
+/* One step (tree step `next`, or the sigma^2 step).  Lockstep hooks for
+ * comparing another implementation step by step: force >= 0 replaces the
+ * accept decision of a tree step; adopt (256 floats, or NULL) replaces the
+ * new leaf values used to update the state after they were drawn and
+ * recorded in the trace.  Neither changes what the trace reports. */
 int oc_step(const oc_config *c, const int32_t *n_cuts, const uint8_t *X, int64_t ldx,
-            oc_state *st, uint64_t seed, int32_t force, oc_trace *trace);
+            oc_state *st, uint64_t seed, int32_t force, const float *adopt, oc_trace *trace);
 int oc_run(const oc_config *c, const int32_t *n_cuts, const uint8_t *X, int64_t ldx,
            oc_state *st, uint64_t seed, int64_t n_steps, oc_trace *traces);
 void oc_predict(const oc_config *c, const uint16_t *axis, const uint8_t *cut,

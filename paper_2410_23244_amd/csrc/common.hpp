@@ -10,7 +10,7 @@ namespace bart {
 constexpr int kBlock = 1024;          // threads per workgroup of the sweep kernel
 constexpr int kWaves = kBlock / 64;   // wave64 on CDNA4
 constexpr int kMaxLeaves = 128;       // leaves of a depth-8 heap tree
-constexpr int kSlot = 136;            // 64-bit words per workgroup mailbox (>= kMaxLeaves + 1)
+constexpr int kSlot = 264;            // 64-bit words per workgroup mailbox (>= 2 kMaxLeaves + 1)
 constexpr int kBinFloats = 32768;     // 128 KiB of LDS per-leaf bins
 constexpr int kMaxGrid = 256;         // mailboxes reserved in the workspace
 constexpr int kFlagWord = kMaxLeaves; // result word holding accept/merge flags

@@ -93,7 +93,7 @@ struct Shared {
   Ctx ctx[2];
   double red[kMaxLeaves + 1];
   double part[kBlock];
-  double tot[kMaxLeaves + 1];
+  double tot[2 * kMaxLeaves + 1];
   double S[kMaxLeaves];
   double cntd[kMaxLeaves];
   float mu_old[kMaxLeaves];
@@ -239,6 +239,8 @@ __device__ __forceinline__ void run(const SweepArgs *__restrict__ A, const Launc
     rawx[v] = 0;
   }
   for (int k = t; k < kBinFloats; k += kBlock) sh.bins[k] = 0.f;
+  if (tracing)
+    for (int q = t; q < (int)(sizeof(bart_trace) / 4); q += kBlock) ((uint32_t *)&sh.rec)[q] = 0u;
   if (t == 0) {
     sh.abort_flag = 0;
     sh.dev_err = 0;
@@ -354,21 +356,27 @@ __device__ __forceinline__ void run(const SweepArgs *__restrict__ A, const Launc
       if (lane == 0) atomicAdd(&sh.red_nr, nr);
       // 3. fixed-order workgroup reduction, bins zeroed for the next step
       for (int k = wave; k < L; k += kWaves) {
-        float acc = 0.f;
+        double acc = 0.0;
         if (lane <= setmask) {
 #pragma unroll
           for (int u = 0; u < kWaves; ++u) {
             const int q = ((k * kWaves + u) << setbits) | lane;
-            acc += sh.bins[q];
+            acc += (double)sh.bins[q];
             sh.bins[q] = 0.f;
           }
         }
-        const double tot = wave_sum((double)acc);
+        const double tot = wave_sum(acc);
         if (lane == 0) sh.red[k] = tot;
       }
       __syncthreads();
-      if (t < L) st_dev(&A->slots[(int64_t)w * kSlot + t], word(seq, __float_as_uint((float)sh.red[t])));
-      if (t == L) st_dev(&A->slots[(int64_t)w * kSlot + L], word(seq, (uint32_t)sh.red_nr));
+      // each partial as an fp32 (hi, lo) pair: hi + lo carries ~48 bits of the fp64 sum
+      if (t < 2 * L) {
+        const double x = sh.red[t >> 1];
+        const float hi = (float)x;
+        const float part = (t & 1) ? (float)(x - (double)hi) : hi;
+        st_dev(&A->slots[(int64_t)w * kSlot + t], word(seq, __float_as_uint(part)));
+      }
+      if (t == 2 * L) st_dev(&A->slots[(int64_t)w * kSlot + t], word(seq, (uint32_t)sh.red_nr));
 
       // prefetch the next tree while the master decides
       if (next_tree) issue(j + 1, nxt, cb ^ 1);
@@ -376,7 +384,7 @@ __device__ __forceinline__ void run(const SweepArgs *__restrict__ A, const Launc
       if (MASTER) {
         const double s2 = sh.sigma2, v2 = A->sigma_mu * A->sigma_mu;
         // 4b. gather the mailboxes: thread (seg, k) sums the workgroups of its segment in order
-        const int K1 = L + 1;
+        const int K1 = 2 * L + 1;
         const int nseg = kBlock / K1;
         if (t < nseg * K1) {
           const int k = t % K1, seg = t / K1;
@@ -406,7 +414,8 @@ __device__ __forceinline__ void run(const SweepArgs *__restrict__ A, const Launc
 #pragma unroll
             for (int u = 0; u < 8; ++u)
               if (gb + u < g1)
-                acc += (k < L) ? (double)__uint_as_float((uint32_t)wv[u]) : (double)(uint32_t)wv[u];
+                acc += (k < 2 * L) ? (double)__uint_as_float((uint32_t)wv[u])
+                                   : (double)(uint32_t)wv[u];
           }
           sh.part[t] = acc;
         }
@@ -418,7 +427,7 @@ __device__ __forceinline__ void run(const SweepArgs *__restrict__ A, const Launc
         }
         __syncthreads();
         // 4c. partial sums S_h = R_h + n_h * (old value) (sec. 3.3 item 8)
-        const double nR = sh.tot[L];
+        const double nR = sh.tot[2 * L];
         if (t < L) {
           const int h = my_h;
           const bool child = (move == kGrow) && ((h >> 1) == eta);
@@ -426,7 +435,7 @@ __device__ __forceinline__ void run(const SweepArgs *__restrict__ A, const Launc
           const float mo = child ? eta_leaf : my_leaf;
           sh.cntd[t] = nk;
           sh.mu_old[t] = mo;
-          sh.S[t] = sh.tot[t] + nk * (double)mo;
+          sh.S[t] = (sh.tot[2 * t] + sh.tot[2 * t + 1]) + nk * (double)mo;
         }
         __syncthreads();
         // 4d. accept / reject (item 9)

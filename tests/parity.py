@@ -13,7 +13,10 @@ step's record is compared:
 * new leaf values: |dmu| <= 1e-5 (|mu| + 1/sqrt(prec));
 * SSR and sigma^2: relative 1e-5 (the device sums fp32 workgroup partials);
 and at the end the index caches and tree structures must be identical and
-the residuals close.
+the residuals close.  After each tree step the oracle carries on from the
+device's new leaf values (and, on a tie, its decision), so that every step
+compares the two implementations on identical trees, residuals and random
+streams rather than on two chains that drift apart by fp32 rounding.
 """
 from __future__ import annotations
 
@@ -71,7 +74,7 @@ def _leaf_l1(inp, idx_row, resid, leaf_row, move, eta, a, s):
 
 
 def compare_steps(inp, ch: oracle.Chain, trg: np.ndarray, seed: int, rep: Report,
-                  sum_tol=1e-5, leaf_tol=1e-5, tie_tol=1e-4, var_tol=1e-5):
+                  sum_tol=1e-5, leaf_tol=1e-5, tie_tol=1e-4, var_tol=1e-5, adopt_leaves=True):
     H = 1 << (inp.D - 1)
     sig_mu2 = inp.hyper.sigma_mu ** 2
     for k, g in enumerate(trg):
@@ -80,7 +83,10 @@ def compare_steps(inp, ch: oracle.Chain, trg: np.ndarray, seed: int, rep: Report
         if j < inp.m:
             saved = (ch.idx[j].copy(), ch.resid.copy(), ch.axis[j].copy(), ch.cut[j].copy(),
                      ch.leaf[j].copy(), ch.sigma2, ch.sweep, ch.next)
-            o = ch.step(seed)
+            # the oracle continues from the device's leaf draws (compared below), so every
+            # step starts from identical trees, residuals and random streams
+            adopt = g["leaf_new"] if adopt_leaves else None
+            o = ch.step(seed, adopt=adopt)
             assert g["kind"] == 0 and o["kind"] == 0, (k, g["kind"], o["kind"])
             assert (g["tree"], g["sweep"]) == (o["tree"], o["sweep"]), (k, g["tree"], o["tree"])
             for f in ["move", "eta", "axis", "cut", "n_grow_cand", "n_prune_cand", "n_leaves"]:
@@ -102,7 +108,7 @@ def compare_steps(inp, ch: oracle.Chain, trg: np.ndarray, seed: int, rep: Report
                     (ch.idx[j], ch.resid[...], ch.axis[j], ch.cut[j], ch.leaf[j]) = (
                         saved[0], saved[1], saved[2], saved[3], saved[4])
                     ch.sigma2, ch.sweep, ch.next = saved[5], saved[6], saved[7]
-                    o = ch.step(seed, force=int(g["accept"]))
+                    o = ch.step(seed, force=int(g["accept"]), adopt=adopt)
                 rep.accepts += int(o["accept"])
             # partial-residual sums against the l1 mass of each leaf
             l1 = _leaf_l1(inp, saved[0], saved[1], saved[4], int(o["move"]), int(o["eta"]),
@@ -134,7 +140,7 @@ def compare_steps(inp, ch: oracle.Chain, trg: np.ndarray, seed: int, rep: Report
     return rep
 
 
-def compare_states(inp, gst: dict, ch: oracle.Chain, rep: Report, resid_tol=1e-5):
+def compare_states(inp, gst: dict, ch: oracle.Chain, rep: Report):
     np.testing.assert_array_equal(gst["idx"], ch.idx, err_msg="index cache")
     np.testing.assert_array_equal(gst["cut"], ch.cut, err_msg="cut")
     H = 1 << (inp.D - 1)
@@ -142,11 +148,11 @@ def compare_states(inp, gst: dict, ch: oracle.Chain, rep: Report, resid_tol=1e-5
         for h in range(1, H):
             if gst["cut"][j, h]:
                 assert gst["axis"][j, h] == ch.axis[j, h], (j, h)
-    scale = np.abs(ch.leaf).max() + np.abs(ch.resid).max()
-    err = np.abs(gst["resid"].astype(np.float64) - ch.resid)
-    rel = err / (np.abs(ch.resid) + 0.1 * scale)
-    rep.max_resid_err = float(rel.max())
-    assert rel.max() <= resid_tol, float(rel.max())
+    # the oracle adopted the device's leaf draws, so the fp32 residual updates
+    # r + (old - new) were the same operations on the same values on both sides
+    rep.max_resid_err = float(np.abs(gst["resid"].astype(np.float64) - ch.resid).max())
+    np.testing.assert_array_equal(gst["resid"], ch.resid, err_msg="residual cache")
+    np.testing.assert_array_equal(gst["leaf"], ch.leaf, err_msg="leaf values")
     assert gst["sweep"] == ch.sweep and gst["next"] == ch.next
     assert abs(gst["sigma2"] - ch.sigma2) <= 1e-5 * ch.sigma2
 
