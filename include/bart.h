@@ -59,7 +59,8 @@ typedef struct {
   int32_t ntree;      /* trees m (sec. 2.1 "Hyperparameters"), >= 1 */
   int32_t max_depth;  /* D in [2, 8]; nodes at depth D-1 are leaves */
   int32_t idx_bytes;  /* 1 or 2: width of the index cache entries */
-  int32_t grid;       /* workgroups of the sweep kernel; 0 = automatic */
+  int32_t grid;       /* workgroups of the sweep kernel (one decides, the rest own
+                         the observations): 0 = automatic, else in [2, 256] */
   int64_t x_stride;   /* elements between predictor rows of X_b: >= n, multiple of 16 */
   double alpha, beta; /* tree prior P_d = alpha (1+d)^-beta, alpha in [0,1], beta >= 0 */
   double mu_mu;       /* leaf prior mean (sec. 2.1 "Prior over leaf values") */

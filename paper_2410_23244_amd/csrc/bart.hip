@@ -52,7 +52,7 @@ const char *check_config(const bart_config *c) {
   if (c->ntree < 1) return "ntree must be >= 1";
   if (c->max_depth < 2 || c->max_depth > 8) return "max_depth must be in [2, 8]";
   if (c->idx_bytes != 1 && c->idx_bytes != 2) return "idx_bytes must be 1 or 2";
-  if (c->grid < 0 || c->grid > kMaxGrid) return "grid must be in [0, 256]";
+  if (c->grid < 0 || c->grid == 1 || c->grid > kMaxGrid) return "grid must be 0 or in [2, 256]";
   if (c->x_stride < c->n || c->x_stride % 16) return "x_stride must be >= n and a multiple of 16";
   if (!(c->alpha >= 0.0 && c->alpha <= 1.0)) return "alpha must be in [0, 1]";
   if (!(c->beta >= 0.0 && std::isfinite(c->beta))) return "beta must be finite and >= 0";
@@ -90,7 +90,7 @@ Layout make_layout(const bart_config &c) {
   L.nz_rank = take(sizeof(int32_t) * c.p);
   L.ctl = take(sizeof(Ctl));
   L.slots = take(sizeof(uint64_t) * kMaxGrid * kSlot);
-  L.result = take(sizeof(uint64_t) * kSlot);
+  L.result = take(sizeof(uint64_t) * kMaxGrid * kSlot);
   L.args = take(sizeof(SweepArgs));
   L.total = o;
   return L;
@@ -263,7 +263,7 @@ SweepArgs make_args(bart_handle *h) {
   A.nz_rank = at<int32_t>(h, h->lay.nz_rank);
   A.ctl = at<Ctl>(h, h->lay.ctl);
   A.slots = at<uint64_t>(h, h->lay.slots);
-  A.result = at<uint64_t>(h, h->lay.result);
+  A.boxes = at<uint64_t>(h, h->lay.result);
   A.n = c.n;
   A.p = c.p;
   A.m = c.ntree;
@@ -284,7 +284,7 @@ SweepArgs make_args(bart_handle *h) {
 
 int launch_sweep(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace) {
   HIP_TRY(hipSetDevice(h->device));
-  const int64_t words = (int64_t)kMaxGrid * kSlot + kSlot;
+  const int64_t words = 2 * (int64_t)kMaxGrid * kSlot;  // mailboxes and result boxes
   k_clear_words<<<grid_for(words, 256), 256, 0, h->stream>>>(at<uint64_t>(h, h->lay.slots),
                                                                words);
   HIP_TRY(hipGetLastError());
@@ -338,11 +338,12 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
   HIP_TRY(hipGetDevice(&device));
   hipDeviceProp_t prop;
   HIP_TRY(hipGetDeviceProperties(&prop, device));
-  // launch shape: fewest chunks per thread that fit one workgroup per CU
+  // launch shape: workgroup 0 decides, workgroups 1..G-1 own the observations;
+  // fewest chunks of 4 observations per thread with one workgroup per CU
   int gmax = std::min(prop.multiProcessorCount, kMaxGrid);
   int V = 0, G = 0;
   for (int v : kVs) {
-    const int64_t need = (chunks + (int64_t)v * kBlock - 1) / ((int64_t)v * kBlock);
+    const int64_t need = 1 + (chunks + (int64_t)v * kBlock - 1) / ((int64_t)v * kBlock);
     const int g = cfg->grid > 0 ? cfg->grid : (int)need;
     if (need <= g && g <= gmax) {
       V = v;
@@ -351,8 +352,9 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
     }
   }
   if (!V)
-    return fail(BART_ENOTSUP, "n=%d needs more than %d workgroups x %d chunks of 4 observations",
-                cfg->n, gmax, kVs[3]);
+    return fail(BART_ENOTSUP,
+                "n=%d needs more than %d worker workgroups x %d chunks of 4 observations",
+                cfg->n, gmax - 1, kVs[3]);
   SweepFn fn = sweep_fn(V, cfg->idx_bytes);
   int per_cu = 0;
   HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)fn, kBlock, 0));

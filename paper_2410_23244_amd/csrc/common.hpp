@@ -13,9 +13,19 @@ constexpr int kMaxLeaves = 128;       // leaves of a depth-8 heap tree
 constexpr int kSlot = 264;            // 64-bit words per workgroup mailbox (>= 2 kMaxLeaves + 1)
 constexpr int kBinFloats = 32768;     // 128 KiB of LDS per-leaf bins
 constexpr int kMaxGrid = 256;         // mailboxes reserved in the workspace
-constexpr int kFlagWord = kMaxLeaves; // result word holding accept/merge flags
 
 enum Move : int32_t { kNone = 0, kGrow = 1, kPrune = 2 };
+
+// Global-address-space view of a device pointer.  Pointers read out of the
+// argument block are generic ("flat") to the compiler; flat loads count
+// against the LDS wait counter too, so an LDS read would stall behind every
+// outstanding HBM load.  Kernels access device memory through gbl(p).
+template <class T>
+using gptr = __attribute__((address_space(1))) T *;
+template <class T>
+__device__ __forceinline__ gptr<T> gbl(T *p) {
+  return (gptr<T>)p;
+}
 
 // Proposal of one tree for its step of the current sweep (sec. 3.3 items 1
 // and 6: everything that does not depend on residuals), 96 bytes.
@@ -55,7 +65,7 @@ struct SweepArgs {
   const int32_t *nz_rank;
   Ctl *ctl;
   uint64_t *slots;   // [kMaxGrid][kSlot]
-  uint64_t *result;  // [kSlot]
+  uint64_t *boxes;   // [kMaxGrid][kSlot] master -> worker: word 0 flags, 1..L residual deltas
   int32_t n, p, m, D, H, p_nz, G, chunks;
   double alpha, beta, mu_mu, sigma_mu, nu, lambda, p_grow;
 };
