@@ -2,21 +2,25 @@
 
 A step is one full MCMC sweep (every tree updated in order, then sigma^2)
 over the synthetic workload n=1e6, p=100, ntree=200, depth 6, uint8 index
-cache.  Inputs are generated and uploaded before the timed region; the timed
-region is one bart_step(K) launch, bracketed by device synchronisations and
-timed with HIP events on the chain's stream.  Prints one JSON line.
+cache.  Inputs are generated and uploaded before the timed region.  Warm-up
+and timed sweeps run as bart_step calls of --sweeps-per-launch sweeps each
+(one kernel launch per call); each timed launch is bracketed by HIP events on
+the chain's stream, and the whole timed region by device synchronisations.
+Prints one JSON line.
 
 Roofline: the algorithmic bytes of a tree step are (9 + 2 s_idx) per
 observation (read the index row and the predictor row, read and write the
 residual, write the index row) plus 4 bytes per observation per sweep for
-sigma^2; achieved = algorithmic bytes / launch duration, against 8 TB/s.
+sigma^2; achieved = algorithmic bytes per launch / average launch duration,
+against 8 TB/s.  traffic = HBM bytes per launch measured by the FETCH_SIZE
+and WRITE_SIZE counters (calibrated on a plain copy) for the current kernel
+sources, else null.
 """
 from __future__ import annotations
 
 import argparse
 import json
 import os
-import platform
 import sys
 import time
 
@@ -56,56 +60,118 @@ def cpu_baseline(inp, state, seed: int, sweeps: int) -> dict:
                       f"(host has {os.cpu_count()} logical CPUs)"}
 
 
+def copy_probe(mib: int) -> int:
+    """A plain elementwise copy (dst = -src) of known size for counter calibration."""
+    import torch
+
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": 4 * n, "copy_probe_bytes_written": 4 * n,
+                      "launches": 3}), flush=True)
+    return 0
+
+
+def kernel_source_digest() -> str:
+    """sha256 over the HIP sources of the sweep (to tell whether stored counters are stale)."""
+    import hashlib
+
+    d = os.path.join(ROOT, "paper_2410_23244_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(d)):
+        if name.endswith((".hip", ".hpp")):
+            with open(os.path.join(d, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def stored_traffic(workload: str, sweeps_per_launch: int):
+    """HBM bytes per launch from the committed counter summary, or None when it was
+    taken on other sources or another workload."""
+    path = os.path.join(ROOT, "profiles", "sweep_kernel_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_src_sha256") != kernel_source_digest() or rec.get("workload") != workload:
+        return None
+    return (rec["fetch_bytes_per_sweep"] + rec["write_bytes_per_sweep"]) * sweeps_per_launch
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000, help="timed sweeps")
-    ap.add_argument("--warmup", type=int, default=10, help="untimed sweeps")
+    ap.add_argument("--warmup", type=int, default=100, help="untimed sweeps before timing")
+    ap.add_argument("--sweeps-per-launch", type=int, default=100,
+                    help="sweeps per bart_step call (one kernel launch each)")
+    ap.add_argument("--launch", choices=["ordinary", "cooperative"], default="ordinary",
+                    help="how the sweep kernel is launched (kernel tracers cannot record "
+                         "cooperative launches)")
     ap.add_argument("--config", type=int, default=3, help="workload number (3 = headline)")
-    ap.add_argument("--cpu-sweeps", type=int, default=5, help="oracle sweeps (0 = skip)")
+    ap.add_argument("--cpu-sweeps", type=int, default=20, help="oracle sweeps (0 = skip)")
     ap.add_argument("--seed", type=int, default=3)
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (read MIB, write MIB) three "
+                         "times, to calibrate HBM byte counters, and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(the sweep is built and measured on a single MI355X)", file=sys.stderr)
         return 2
+    S = args.sweeps_per_launch
+    if S < 1 or args.steps < S or args.steps % S or args.warmup % S:
+        print("--steps must be a positive multiple of --sweeps-per-launch, --warmup a multiple",
+              file=sys.stderr)
+        return 2
 
     import torch
 
-    from paper_2410_23244_amd.bart import from_inputs
+    from paper_2410_23244_amd.bart import (BART_LAUNCH_COOPERATIVE, BART_LAUNCH_ORDINARY,
+                                           from_inputs)
     from paper_2410_23244_amd.inputs import make_inputs
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        return copy_probe(args.copy_probe)
     t0 = time.perf_counter()
     inp = make_inputs(args.config)
     print(f"[bench] inputs {inp.workload} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
           flush=True)
-    g = from_inputs(inp)
+    mode = BART_LAUNCH_ORDINARY if args.launch == "ordinary" else BART_LAUNCH_COOPERATIVE
+    g = from_inputs(inp, launch=mode)
     info = g.launch_info()
     stream = g.stream
-    if args.warmup:
-        g.step(args.warmup, args.seed)
+    for _ in range(args.warmup // S):
+        g.step(S, args.seed)
     torch.cuda.synchronize()
     assert g.status() == 0, "device error during warm-up"
     print(f"[bench] warm-up {args.warmup} sweeps done", file=sys.stderr, flush=True)
 
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    L = args.steps // S
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * L)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    e0.record(stream)
-    g.step(args.steps, args.seed)
-    e1.record(stream)
+    for i in range(L):
+        ev[2 * i].record(stream)
+        g.step(S, args.seed)
+        ev[2 * i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    ms = e0.elapsed_time(e1)
     assert g.status() == 0, "device error during the timed sweeps"
-    sec = ms / 1e3
-    sweeps_per_s = args.steps / sec
+    ms = ev[0].elapsed_time(ev[-1])
+    launch_ms = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(L)]
+    avg_launch = sum(launch_ms) / L
+    sweeps_per_s = args.steps / (ms / 1e3)
     per_sweep = model_bytes_per_sweep(inp.n, inp.m, inp.idx_bytes)
-    achieved = per_sweep * args.steps / sec / 1e9
-    print(f"[bench] {args.steps} sweeps: events {ms:.1f} ms, wall {wall * 1e3:.1f} ms",
+    achieved = per_sweep * S / (avg_launch / 1e3) / 1e9
+    print(f"[bench] {args.steps} sweeps in {L} launches: events {ms:.1f} ms, wall "
+          f"{wall * 1e3:.1f} ms, per launch {min(launch_ms):.2f}..{max(launch_ms):.2f} ms",
           file=sys.stderr, flush=True)
 
     cpu = None
@@ -128,15 +194,19 @@ def main() -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": inp.workload, "n": inp.n, "p": inp.p, "ntree": inp.m,
-                   "max_depth": inp.D, "idx_bytes": inp.idx_bytes,
-                   "sweeps_per_launch": args.steps, "grid": info.grid,
+                   "max_depth": inp.D, "idx_bytes": inp.idx_bytes, "sweeps_per_launch": S,
+                   "launch": args.launch, "grid": info.grid,
                    "chunks_per_thread": info.chunks_per_thread, "parallelism": "1 GPU"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": stored_traffic(inp.workload, S),
+                     "kernel": "bart::sweep_kernel<1, 1>", "avg_launch_ms": avg_launch,
+                     "algorithmic_bytes_per_launch": per_sweep * S},
         "cpu_baseline": cpu,
-        "host": platform.node(),
     }
     print(json.dumps(line), flush=True)
+    g.close()
+    torch.cuda.synchronize()
     return 0
 
 

@@ -50,6 +50,19 @@ extern "C" {
 #define BART_DEVERR_TIMEOUT 1u   /* a cross-workgroup wait exceeded its spin limit */
 #define BART_DEVERR_CACHE 2u     /* index cache inconsistent with the trees */
 
+/* How bart_step and bart_debug_steps launch the sweep kernel.  Its workgroups
+ * wait on each other, so all of them must be resident at once.
+ *  COOPERATIVE: hipLaunchCooperativeKernel, which guarantees co-residency.
+ *  ORDINARY: hipLaunchKernel.  The grid never exceeds one workgroup per
+ *    compute unit, so on a device with no other long-running work every
+ *    workgroup becomes resident; kernels running concurrently on other
+ *    streams only delay that, and a wait that outlasts its spin limit ends the
+ *    launch with BART_DEVERR_TIMEOUT instead of hanging.  Use it where
+ *    cooperative launches are unavailable (stream capture into a HIP graph,
+ *    kernel tracers that cannot record them). */
+#define BART_LAUNCH_COOPERATIVE 0
+#define BART_LAUNCH_ORDINARY 1
+
 typedef struct bart_handle bart_handle;
 
 /* Model and problem configuration. */
@@ -61,6 +74,8 @@ typedef struct {
   int32_t idx_bytes;  /* 1 or 2: width of the index cache entries */
   int32_t grid;       /* workgroups of the sweep kernel (one decides, the rest own
                          the observations): 0 = automatic, else in [2, 256] */
+  int32_t launch;     /* BART_LAUNCH_COOPERATIVE or BART_LAUNCH_ORDINARY */
+  int32_t reserved;   /* must be 0 */
   int64_t x_stride;   /* elements between predictor rows of X_b: >= n, multiple of 16 */
   double alpha, beta; /* tree prior P_d = alpha (1+d)^-beta, alpha in [0,1], beta >= 0 */
   double mu_mu;       /* leaf prior mean (sec. 2.1 "Prior over leaf values") */
@@ -110,7 +125,7 @@ typedef struct {
 /* Launch shape chosen by bart_init. */
 typedef struct {
   int32_t grid, block, chunks_per_thread, lds_bytes;
-  int32_t obs_per_thread, max_leaves, pad[2];
+  int32_t obs_per_thread, max_leaves, launch, pad;
 } bart_launch;
 
 /* Bytes of device workspace bart_init needs for cfg (0 if cfg is invalid). */

@@ -53,6 +53,9 @@ const char *check_config(const bart_config *c) {
   if (c->max_depth < 2 || c->max_depth > 8) return "max_depth must be in [2, 8]";
   if (c->idx_bytes != 1 && c->idx_bytes != 2) return "idx_bytes must be 1 or 2";
   if (c->grid < 0 || c->grid == 1 || c->grid > kMaxGrid) return "grid must be 0 or in [2, 256]";
+  if (c->launch != BART_LAUNCH_COOPERATIVE && c->launch != BART_LAUNCH_ORDINARY)
+    return "launch must be BART_LAUNCH_COOPERATIVE or BART_LAUNCH_ORDINARY";
+  if (c->reserved != 0) return "reserved must be 0";
   if (c->x_stride < c->n || c->x_stride % 16) return "x_stride must be >= n and a multiple of 16";
   if (!(c->alpha >= 0.0 && c->alpha <= 1.0)) return "alpha must be in [0, 1]";
   if (!(c->beta >= 0.0 && std::isfinite(c->beta))) return "beta must be finite and >= 0";
@@ -291,8 +294,12 @@ int launch_sweep(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *tra
   const SweepArgs *A = at<SweepArgs>(h, h->lay.args);
   Launch Lc{h->sweep, h->next, n_steps, seed, trace};
   void *args[] = {&A, &Lc};
-  HIP_TRY(hipLaunchCooperativeKernel((const void *)h->fn, dim3(h->G), dim3(kBlock), args, 0,
-                                     h->stream));
+  // the grid holds at most one workgroup per compute unit (checked at init)
+  if (h->cfg.launch == BART_LAUNCH_COOPERATIVE)
+    HIP_TRY(hipLaunchCooperativeKernel((const void *)h->fn, dim3(h->G), dim3(kBlock), args, 0,
+                                       h->stream));
+  else
+    HIP_TRY(hipLaunchKernel((const void *)h->fn, dim3(h->G), dim3(kBlock), args, 0, h->stream));
   return BART_OK;
 }
 
@@ -531,6 +538,7 @@ int bart_launch_info(const bart_handle *h, bart_launch *o) {
   o->lds_bytes = h->lds;
   o->obs_per_thread = 4 * h->V;
   o->max_leaves = std::min(h->H, kMaxLeaves);
+  o->launch = h->cfg.launch;
   return BART_OK;
 }
 

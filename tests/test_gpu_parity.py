@@ -14,29 +14,32 @@ from tests import parity
 pytestmark = pytest.mark.gpu
 
 
-def _gpu(inp, grid=0):
+COOP, ORDINARY = 0, 1  # BART_LAUNCH_COOPERATIVE, BART_LAUNCH_ORDINARY
+
+
+def _gpu(inp, grid=0, launch=COOP):
     from paper_2410_23244_amd.bart import from_inputs
 
-    return from_inputs(inp, grid=grid)
+    return from_inputs(inp, grid=grid, launch=launch)
 
 
 CASES = {
-    # name: (config, overrides, warm sweeps, lockstep steps, grid)
-    "w1_full": (1, dict(), 3, 2 * 51, 0),
-    "w1_ragged_tiny": (1, dict(n=37, p=3, m=5), 2, 3 * 6, 0),
-    "w2_ragged": (2, dict(n=20011, m=60), 2, 61 + 30, 0),
-    "w2_many_wg": (2, dict(n=40003, p=30, m=40), 2, 41 * 2, 10),
-    "w4_u16": (4, dict(n=30001, p=20, m=50), 2, 51 + 10, 0),
-    "w5_depth8": (5, dict(n=25003, p=1000, m=120), 2, 121 + 5, 0),
+    # name: (config, overrides, warm sweeps, lockstep steps, grid, launch)
+    "w1_full": (1, dict(), 3, 2 * 51, 0, COOP),
+    "w1_ragged_tiny": (1, dict(n=37, p=3, m=5), 2, 3 * 6, 0, COOP),
+    "w2_ragged": (2, dict(n=20011, m=60), 2, 61 + 30, 0, COOP),
+    "w2_many_wg": (2, dict(n=40003, p=30, m=40), 2, 41 * 2, 10, ORDINARY),
+    "w4_u16": (4, dict(n=30001, p=20, m=50), 2, 51 + 10, 0, COOP),
+    "w5_depth8": (5, dict(n=25003, p=1000, m=120), 2, 121 + 5, 0, COOP),
 }
 
 
 @pytest.mark.parametrize("name", list(CASES))
 def test_lockstep_small(name):
-    cfg, over, warm, steps, grid = CASES[name]
+    cfg, over, warm, steps, grid, launch = CASES[name]
     inp = make_inputs(cfg, **over)
     print(f"case {name}: n={inp.n} p={inp.p} m={inp.m} D={inp.D} idx={inp.idx_bytes}", flush=True)
-    g = _gpu(inp, grid)
+    g = _gpu(inp, grid, launch)
     info = g.launch_info()
     print(f"  grid={info.grid} chunks/thread={info.chunks_per_thread}", flush=True)
     rep = parity.lockstep(inp, g, seed=inp.seed + 100, warm_sweeps=warm, n_steps=steps)
@@ -87,10 +90,24 @@ def test_set_state_roundtrip_continues_identically():
     assert a.status() == 0 and b.status() == 0
 
 
+def test_launch_modes_agree():
+    inp = make_inputs(2, n=30011, p=16, m=20)
+    a, b = _gpu(inp, launch=COOP), _gpu(inp, launch=ORDINARY)
+    assert a.launch_info().launch == COOP and b.launch_info().launch == ORDINARY
+    a.step(6, 5)
+    b.step(6, 5)
+    sa, sb = a.get_state(), b.get_state()
+    for k in ["axis", "cut", "leaf", "idx", "resid"]:
+        np.testing.assert_array_equal(sa[k], sb[k], err_msg=k)
+    assert sa["sigma2"] == sb["sigma2"]
+
+
 @pytest.mark.parametrize("cfg", [2, 3])
 def test_lockstep_full_size(cfg):
+    """Full size, in the launch mode the benchmark times, after the benchmark's
+    warm-up length (trees near their stationary size)."""
     inp = make_inputs(cfg)
     print(f"full workload {cfg}: n={inp.n} p={inp.p} m={inp.m}", flush=True)
-    g = _gpu(inp)
-    rep = parity.lockstep(inp, g, seed=inp.seed, warm_sweeps=3, n_steps=inp.m + 1)
+    g = _gpu(inp, launch=ORDINARY)
+    rep = parity.lockstep(inp, g, seed=inp.seed, warm_sweeps=100, n_steps=inp.m + 1)
     print(f"  {rep}", flush=True)
