@@ -41,8 +41,8 @@ size_t up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Layout {
   int64_t n_pad;
-  size_t resid, idx, axis, cut, leaf, count, prop, z, n_cuts, nz_list, nz_rank, ctl, slots,
-      result, args, total;
+  size_t resid, idx, axis, cut, leaf, count, prop, z, n_cuts, nz_list, nz_rank, ctl, pub,
+      args, total;
 };
 
 const char *check_config(const bart_config *c) {
@@ -52,7 +52,7 @@ const char *check_config(const bart_config *c) {
   if (c->ntree < 1) return "ntree must be >= 1";
   if (c->max_depth < 2 || c->max_depth > 8) return "max_depth must be in [2, 8]";
   if (c->idx_bytes != 1 && c->idx_bytes != 2) return "idx_bytes must be 1 or 2";
-  if (c->grid < 0 || c->grid == 1 || c->grid > kMaxGrid) return "grid must be 0 or in [2, 256]";
+  if (c->grid < 0 || c->grid > kMaxGrid) return "grid must be 0 or in [1, 256]";
   if (c->launch != BART_LAUNCH_COOPERATIVE && c->launch != BART_LAUNCH_ORDINARY)
     return "launch must be BART_LAUNCH_COOPERATIVE or BART_LAUNCH_ORDINARY";
   if (c->reserved != 0) return "reserved must be 0";
@@ -92,8 +92,7 @@ Layout make_layout(const bart_config &c) {
   L.nz_list = take(sizeof(int32_t) * c.p);
   L.nz_rank = take(sizeof(int32_t) * c.p);
   L.ctl = take(sizeof(Ctl));
-  L.slots = take(sizeof(uint64_t) * kMaxGrid * kSlot);
-  L.result = take(sizeof(uint64_t) * kMaxGrid * kSlot);
+  L.pub = take(sizeof(uint64_t) * 2 * kMaxGrid * kStride);
   L.args = take(sizeof(SweepArgs));
   L.total = o;
   return L;
@@ -265,8 +264,7 @@ SweepArgs make_args(bart_handle *h) {
   A.nz_list = at<int32_t>(h, h->lay.nz_list);
   A.nz_rank = at<int32_t>(h, h->lay.nz_rank);
   A.ctl = at<Ctl>(h, h->lay.ctl);
-  A.slots = at<uint64_t>(h, h->lay.slots);
-  A.boxes = at<uint64_t>(h, h->lay.result);
+  A.pub = at<uint64_t>(h, h->lay.pub);
   A.n = c.n;
   A.p = c.p;
   A.m = c.ntree;
@@ -287,8 +285,9 @@ SweepArgs make_args(bart_handle *h) {
 
 int launch_sweep(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace) {
   HIP_TRY(hipSetDevice(h->device));
-  const int64_t words = 2 * (int64_t)kMaxGrid * kSlot;  // mailboxes and result boxes
-  k_clear_words<<<grid_for(words, 256), 256, 0, h->stream>>>(at<uint64_t>(h, h->lay.slots),
+  // mailbox words carry launch-relative step numbers: clear both buffers
+  const int64_t words = 2 * (int64_t)kMaxGrid * kStride;
+  k_clear_words<<<grid_for(words, 256), 256, 0, h->stream>>>(at<uint64_t>(h, h->lay.pub),
                                                                words);
   HIP_TRY(hipGetLastError());
   const SweepArgs *A = at<SweepArgs>(h, h->lay.args);
@@ -308,6 +307,20 @@ void advance(bart_handle *h, int64_t steps) {
   const int64_t pos = h->sweep * per + h->next + steps;
   h->sweep = pos / per;
   h->next = (int32_t)(pos % per);
+}
+
+// Steps in launches of at most kMaxLaunchSteps (the mailbox step numbers
+// are 20 bits wide and restart with every launch).
+int run_steps(bart_handle *h, int64_t steps, uint64_t seed, bart_trace *trace) {
+  int64_t done = 0;
+  while (done < steps) {
+    const int32_t k = (int32_t)std::min<int64_t>(steps - done, kMaxLaunchSteps);
+    const int rc = launch_sweep(h, k, seed, trace ? trace + done : nullptr);
+    if (rc) return rc;
+    advance(h, k);
+    done += k;
+  }
+  return BART_OK;
 }
 
 }  // namespace
@@ -350,7 +363,7 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
   int gmax = std::min(prop.multiProcessorCount, kMaxGrid);
   int V = 0, G = 0;
   for (int v : kVs) {
-    const int64_t need = 1 + (chunks + (int64_t)v * kBlock - 1) / ((int64_t)v * kBlock);
+    const int64_t need = (chunks + (int64_t)v * kBlock - 1) / ((int64_t)v * kBlock);
     const int g = cfg->grid > 0 ? cfg->grid : (int)need;
     if (need <= g && g <= gmax) {
       V = v;
@@ -360,8 +373,8 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
   }
   if (!V)
     return fail(BART_ENOTSUP,
-                "n=%d needs more than %d worker workgroups x %d chunks of 4 observations",
-                cfg->n, gmax - 1, kVs[3]);
+                "n=%d needs more than %d workgroups x %d chunks of 4 observations",
+                cfg->n, gmax, kVs[3]);
   SweepFn fn = sweep_fn(V, cfg->idx_bytes);
   int per_cu = 0;
   HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)fn, kBlock, 0));
@@ -430,23 +443,14 @@ int bart_step(bart_handle *h, int32_t k_sweeps, uint64_t seed) {
   if (h->next != 0) return fail(BART_ESTATE, "chain is inside sweep %lld (step %d)",
                                 (long long)h->sweep, h->next);
   const int64_t steps = (int64_t)k_sweeps * (h->cfg.ntree + 1);
-  if (steps > 0x7fffff00LL) return fail(BART_EINVAL, "too many steps in one call");
-  if (steps == 0) return BART_OK;
-  const int rc = launch_sweep(h, (int32_t)steps, seed, nullptr);
-  if (rc) return rc;
-  advance(h, steps);
-  return BART_OK;
+  return run_steps(h, steps, seed, nullptr);
 }
 
 int bart_debug_steps(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace) {
   if (!h) return fail(BART_EINVAL, "handle is NULL");
   if (n_steps < 0) return fail(BART_EINVAL, "n_steps must be >= 0");
   if (n_steps > 0 && !trace) return fail(BART_EINVAL, "trace is NULL");
-  if (n_steps == 0) return BART_OK;
-  const int rc = launch_sweep(h, n_steps, seed, trace);
-  if (rc) return rc;
-  advance(h, n_steps);
-  return BART_OK;
+  return run_steps(h, n_steps, seed, trace);
 }
 
 int bart_predict(bart_handle *h, const uint8_t *Xt, int64_t xt_stride, int64_t n_t, double offset,

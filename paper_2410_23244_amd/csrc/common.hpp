@@ -7,12 +7,13 @@
 
 namespace bart {
 
-constexpr int kBlock = 1024;          // threads per workgroup of the sweep kernel
+constexpr int kBlock = 512;           // threads per workgroup of the sweep kernel (256 VGPRs each)
 constexpr int kWaves = kBlock / 64;   // wave64 on CDNA4
 constexpr int kMaxLeaves = 128;       // leaves of a depth-8 heap tree
-constexpr int kSlot = 264;            // 64-bit words per workgroup mailbox (>= 2 kMaxLeaves + 1)
+constexpr int kStride = 144;          // 64-bit words per mailbox (>= kMaxLeaves + 1, 128-byte lines)
 constexpr int kBinFloats = 32768;     // 128 KiB of LDS per-leaf bins
-constexpr int kMaxGrid = 256;         // mailboxes reserved in the workspace
+constexpr int kMaxGrid = 256;         // mailboxes per buffer reserved in the workspace
+constexpr int kMaxLaunchSteps = (1 << 20) - 8;  // steps per launch (20-bit sequence numbers)
 
 enum Move : int32_t { kNone = 0, kGrow = 1, kPrune = 2 };
 
@@ -64,8 +65,7 @@ struct SweepArgs {
   const int32_t *nz_list;
   const int32_t *nz_rank;
   Ctl *ctl;
-  uint64_t *slots;   // [kMaxGrid][kSlot]
-  uint64_t *boxes;   // [kMaxGrid][kSlot] master -> worker: word 0 flags, 1..L residual deltas
+  uint64_t *pub;     // [2][kMaxGrid][kStride] mailboxes, by step parity
   int32_t n, p, m, D, H, p_nz, G, chunks;
   double alpha, beta, mu_mu, sigma_mu, nu, lambda, p_grow;
 };

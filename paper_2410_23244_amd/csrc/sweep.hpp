@@ -1,32 +1,34 @@
 // sweep.hpp -- persistent HIP kernel running whole BART sweeps on gfx950.
 //
-// One cooperative launch runs a range of steps; a step is the update of one
-// tree (sec. 3.3, "Computations sequential along trees", items 7-11) or the
+// One launch runs a range of steps; a step is the update of one tree (sec.
+// 3.3, "Computations sequential along trees", items 7-11) or the
 // error-variance draw that ends a sweep (sec. 3.3, "Sampling the error
-// variance").  Each workgroup owns a fixed slice of the observations and
+// variance").  Every workgroup owns a fixed slice of the observations and
 // keeps its residuals in registers for the whole launch (the residual cache
 // of sec. 3.3 never leaves the chip); the index cache row of the tree being
 // updated and the predictor row of its proposed axis are streamed from HBM
 // (predictor-major u8, coalesced 4-byte chunks).
 //
-// Per tree step:
-//   1. route (sec. 3.3 item 2): idx' = 2 eta + [x_a >= s] for points in the
-//      grown leaf, the index otherwise; converted to the rank of the leaf in
-//      the larger tree;
-//   2. indexed reduce (item 7, "the bottleneck"): per-lane private LDS bins
-//      of fp32 residual sums, then a fixed-order workgroup reduction in fp64;
-//   3. every worker workgroup posts its per-leaf partials in its own mailbox
-//      as (sequence << 32 | fp32 payload) words; no atomics, no fences;
-//   4. workgroup 0 (the "master", which owns no observations) gathers the
-//      mailboxes in fixed order (so the sums are deterministic), finishes the
-//      MH ratio (items 8-9), draws the leaves (item 10) and posts the flags
-//      and per-leaf residual deltas in one contiguous result block;
-//   5. each worker polls that block with one coalesced wave load, applies
-//      r += old - new (item 11) and rewrites the index row where the tree
-//      changed.
-// While waiting in step j every workgroup already loads the index row and
-// predictor row of tree j+1: proposals do not depend on earlier trees
-// (sec. 3.3, "Computations parallel across trees").
+// There is no coordinating workgroup.  Per tree step j, every workgroup
+//   1. posts its per-leaf partial residual sums of tree j (and, for a GROW,
+//      the count of its points going right) in its own mailbox, as 64-bit
+//      words carrying a 20-bit step number over a 44-bit payload, so a
+//      reader needs no fence and no separate flag;
+//   2. routes its points through tree j+1 (the route depends only on the
+//      index cache and the proposal, sec. 3.3 "Computations parallel across
+//      trees") while the other mailboxes fill;
+//   3. reads all mailboxes in one fixed order and sums them in fp64, so every
+//      workgroup holds bit-identical totals; from them it computes the MH
+//      decision (item 9) and the leaf draws (item 10) itself: the same code
+//      on the same inputs gives the same result everywhere;
+//   4. applies r += old - new to its residuals and rewrites its part of the
+//      index row where the tree changed (item 11);
+//   5. accumulates tree j+1's partial sums from the updated residuals in
+//      per-lane private LDS bins and reduces them in a fixed order.
+// One cross-workgroup hop per tree.  Tree j's structure, leaf values and
+// counts are written by its owner workgroup (j mod G) and read by all in
+// the next sweep; the sigma^2 step publishes them with release/acquire
+// fences.
 #pragma once
 #include "common.hpp"
 #include "propose.hpp"
@@ -35,31 +37,34 @@
 namespace bart {
 
 constexpr uint32_t kSpinLimit = 1u << 21;
+constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
 
-__device__ __forceinline__ uint64_t ld_dev(uint64_t *p) {
-  return __hip_atomic_load(gbl(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ uint64_t ld_dev(const uint64_t *p) {
+  return __hip_atomic_load(gbl(const_cast<uint64_t *>(p)), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void st_dev(uint64_t *p, uint64_t v) {
   __hip_atomic_store(gbl(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ uint64_t word(uint32_t seq, uint32_t payload) {
-  return ((uint64_t)seq << 32) | payload;
-}
 
-// Bounded wait until *p carries sequence seq; false on timeout.
-__device__ __forceinline__ bool wait_word(uint64_t *p, uint32_t seq, uint64_t &v) {
-  v = ld_dev(p);
-  uint32_t spins = 0;
-  while ((uint32_t)(v >> 32) != seq) {
-    __builtin_amdgcn_s_sleep(1);
-    if (++spins > kSpinLimit) return false;
-    v = ld_dev(p);
-  }
-  return true;
+// Mailbox word: step number (20 bits) over a 44-bit payload.  An fp64 value
+// is carried as its top 44 bits (sign, exponent, 32 mantissa bits), a count
+// as an integer.
+constexpr int kPayloadBits = 44;
+constexpr uint64_t kPayloadMask = (1ull << kPayloadBits) - 1ull;
+__device__ __forceinline__ uint64_t mk_word(uint32_t seq, uint64_t payload) {
+  return ((uint64_t)seq << kPayloadBits) | payload;
+}
+__device__ __forceinline__ uint32_t seq_of(uint64_t w) { return (uint32_t)(w >> kPayloadBits); }
+__device__ __forceinline__ uint64_t pack_f64(double x) {
+  return (uint64_t)__double_as_longlong(x) >> (64 - kPayloadBits);
+}
+__device__ __forceinline__ double unpack_f64(uint64_t w) {
+  return __longlong_as_double((long long)((w & kPayloadMask) << (64 - kPayloadBits)));
 }
 
 // Workgroup barrier that orders LDS accesses only: outstanding global loads
-// (prefetches of the next tree) stay in flight across it.
+// (prefetches of later trees) stay in flight across it.
 __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
@@ -88,17 +93,6 @@ __device__ __forceinline__ double wave_total63(double v) {
   return v;
 }
 
-__device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-__device__ __forceinline__ int wave_sum(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-
 // Log marginal-likelihood ratio of splitting a leaf into (L, R): the
 // partial residuals of a leaf with n points, its N(mu_mu, sigma_mu^2) value
 // integrated out (sec. 2.1), are N(mu_mu 1, sigma^2 I + sigma_mu^2 1 1^T).
@@ -113,31 +107,43 @@ __device__ inline double split_llr(double s2, double mu_mu, double v, double nL,
   return det + v / (2.0 * s2) * (qL + qR - qP);
 }
 
-// Per-workgroup view of the tree being stepped.
+// Per-workgroup view of one tree's proposal.
 struct Ctx {
   Prop pr;
   uint8_t rank_of[256];          // heap slot -> rank among larger-tree leaves (0xFF: none)
   uint16_t heap_of[kMaxLeaves];  // rank -> heap slot
 };
 
+// What the decision of one tree needs besides the sums: per rank of the
+// larger tree its stored count, current value and leaf normal, and the same
+// for the node eta of the move (sec. 3.3 items 4-5, 8).
+struct TreeData {
+  int32_t cnt[kMaxLeaves];
+  float mu[kMaxLeaves];
+  double z[kMaxLeaves];
+  int32_t eta_cnt;
+  float eta_mu;
+  double eta_z;
+};
+
 struct Shared {
   float bins[kBinFloats];
-  Ctx ctx[2];
-  double red[kMaxLeaves + 1];
+  Ctx ctx[kRing];
+  TreeData td[2];
+  double red[kMaxLeaves + 1];  // this workgroup's partial sums of the tree to post next
   double part[kBlock];
-  double tot[2 * kMaxLeaves + 1];
+  double tot[kMaxLeaves + 1];
   double S[kMaxLeaves];
   double cntd[kMaxLeaves];
   float mu_old[kMaxLeaves];
   float delta[kMaxLeaves];
+  float newv[kMaxLeaves];
   uint16_t fin[kMaxLeaves];
   double wave_part[kWaves];
-  uint32_t res[kMaxLeaves + 1];  // master: payloads of the result boxes
-  float newv[kMaxLeaves];
-  bart_trace rec;
   double sigma2;
   double dec_logr, dec_S_eta, dec_n_eta;
-  int red_nr;
+  uint64_t stats[6];  // workgroup 0: move statistics of this launch
+  int nr[2];  // GROW right-counts of the trees being routed, by tree parity
   int flags;  // bit0 accept, bit1 merged
   int abort_flag;
   int dev_err;
@@ -158,10 +164,10 @@ struct IdxChunk<2> {
   static __device__ __forceinline__ T put(T c, int b, int v) { return c | ((T)v << (16 * b)); }
 };
 
-// Proposal of tree j: thread t < 24 loads 32-bit word t of its record
-// (a lane-varying load, so nothing waits for it until it is stored to LDS).
 constexpr int kPropWords = (int)(sizeof(Prop) / 4);
 
+// Word t (< 24) of tree j's proposal record: a lane-varying load, so nothing
+// waits for it until it is stored to LDS.
 __device__ __forceinline__ uint32_t load_prop_word(const SweepArgs *__restrict__ A, int j) {
   const int t = threadIdx.x;
   return t < kPropWords ? (gbl((const uint32_t *)(A->prop + j)))[t] : 0u;
@@ -184,6 +190,44 @@ __device__ __forceinline__ void build_ranks(const SweepArgs *__restrict__ A, Ctx
   }
 }
 
+// Per-thread registers of one tree's decision data in flight (thread t holds
+// rank t; thread kBlock-1 the node eta).
+struct TdRegs {
+  int32_t cnt;
+  float mu;
+  double z;
+};
+
+__device__ __forceinline__ TdRegs load_tree_data(const SweepArgs *__restrict__ A, const Ctx &c,
+                                                 int j, int64_t s) {
+  const int t = threadIdx.x, H = A->H;
+  TdRegs r{0, 0.f, 0.0};
+  int h = -1;
+  if (t < c.pr.L) h = c.heap_of[t];
+  if (t == kBlock - 1 && c.pr.move != kNone) h = c.pr.eta;
+  if (h >= 0) {
+    const int64_t o = (int64_t)j * 2 * H + h;
+    r.cnt = gbl((const int32_t *)A->count)[o];
+    r.mu = gbl((const float *)A->leaf)[o];
+    r.z = gbl((const double *)A->z)[(int64_t)(s & 1) * A->m * 2 * H + o];
+  }
+  return r;
+}
+
+__device__ __forceinline__ void store_tree_data(TreeData &td, const Ctx &c, const TdRegs &r) {
+  const int t = threadIdx.x;
+  if (t < c.pr.L) {
+    td.cnt[t] = r.cnt;
+    td.mu[t] = r.mu;
+    td.z[t] = r.z;
+  }
+  if (t == kBlock - 1) {
+    td.eta_cnt = r.cnt;
+    td.eta_mu = r.mu;
+    td.eta_z = r.z;
+  }
+}
+
 // Leaf normals of sweep s for trees >= j0, grid-stride over (tree, pair of
 // heap slots); each Philox block gives the normals of slots 2u and 2u+1.
 __device__ __noinline__ void gen_normals(const SweepArgs *__restrict__ A, uint64_t seed, int64_t s,
@@ -200,25 +244,16 @@ __device__ __noinline__ void gen_normals(const SweepArgs *__restrict__ A, uint64
   }
 }
 
-// Master: proposals of trees [j0, m) of sweep s, one thread per tree.
+// Proposals of sweep s for the trees >= j0 this workgroup owns (tree j is
+// owned by workgroup j mod G), one thread per tree.
 __device__ __noinline__ void gen_proposals(const SweepArgs *__restrict__ A, uint64_t seed, int64_t s,
                                            int j0) {
-  for (int tr = j0 + (int)threadIdx.x; tr < A->m; tr += kBlock)
-    propose_tree(A, seed, tr, s, A->prop[tr]);
+  for (int tr = (int)blockIdx.x + A->G * (int)threadIdx.x; tr < A->m; tr += A->G * kBlock)
+    if (tr >= j0) propose_tree(A, seed, tr, s, A->prop[tr]);
 }
 
-// Master: copy the staged trace record of a step out and clear the stage.
-__device__ __noinline__ void flush_trace(bart_trace *dst, bart_trace *stage) {
-  uint32_t *d = (uint32_t *)dst;
-  uint32_t *src = (uint32_t *)stage;
-  for (int q = threadIdx.x; q < (int)(sizeof(bart_trace) / 4); q += kBlock) {
-    d[q] = src[q];
-    src[q] = 0u;
-  }
-}
-
-// Master: sigma^2 | rest ~ InvGamma((nu+n)/2, (nu lambda + SSR)/2), the
-// conjugate update of the prior lambda nu / sigma^2 ~ chi^2_nu (eq. bartdef).
+// sigma^2 | rest ~ InvGamma((nu+n)/2, (nu lambda + SSR)/2), the conjugate
+// update of the prior lambda nu / sigma^2 ~ chi^2_nu (eq. bartdef).
 __device__ __noinline__ double draw_sigma2(const SweepArgs *__restrict__ A, uint64_t seed, int64_t s,
                                            double ssr) {
   const double shape = 0.5 * (A->nu + (double)A->n);
@@ -226,188 +261,308 @@ __device__ __noinline__ double draw_sigma2(const SweepArgs *__restrict__ A, uint
   return scale / gamma_mt(seed, (uint64_t)s, shape);
 }
 
-// Grid-wide rendezvous at sequence seq (prologue): every workgroup posts
-// word 0 of its mailbox, the master waits for all of them and answers in
-// result word 0.  Callers release their writes before, acquire after.
-__device__ __forceinline__ void rendezvous(const SweepArgs *__restrict__ A, Shared &sh,
-                                           uint32_t seq, bool master) {
-  const int t = threadIdx.x;
-  if (t == 0) st_dev(&A->slots[(int64_t)blockIdx.x * kSlot], word(seq, 0));
-  if (master) {
+// Post words 0..K-1 (this workgroup's mailbox in buffer par).
+__device__ __forceinline__ uint64_t *mailbox(const SweepArgs *__restrict__ A, int par, int g) {
+  return A->pub + ((int64_t)par * kMaxGrid + g) * kStride;
+}
+
+// Read word k < K of every mailbox of buffer par once all carry step number
+// seq, and sum them in a fixed order into sh.tot[k] (fp64; words k < nsum
+// are fp64 values, the others counts).  Thread (seg, k) sums the workgroups
+// of its segment in increasing order, polling up to 4 mailboxes at a time;
+// thread k then sums the segments in increasing order.  Every workgroup runs
+// the same partition, so every workgroup gets the same bits.  Ends with an
+// LDS barrier.
+__device__ __forceinline__ void gather(const SweepArgs *__restrict__ A, Shared &sh, int par,
+                                       uint32_t seq, int K, int nsum) {
+  const int t = threadIdx.x, G = A->G;
+  int nseg = kBlock / K;
+  if (nseg > G) nseg = G;
+  if (t < nseg * K) {
+    const int k = t % K, seg = t / K;
+    const int g0 = (seg * G) / nseg, g1 = ((seg + 1) * G) / nseg;
+    const uint64_t *base = A->pub + (int64_t)par * kMaxGrid * kStride + k;
+    double acc = 0.0;
 #pragma unroll 1
-    for (int g = 1 + t; g < A->G; g += kBlock) {
-      uint64_t v;
-      if (!wait_word(&A->slots[(int64_t)g * kSlot], seq, v)) sh.abort_flag = 1;
+    for (int gb = g0; gb < g1; gb += 4) {
+      uint64_t wv[4];
+      uint32_t pending = (g1 - gb >= 4) ? 0xFu : ((1u << (g1 - gb)) - 1u);
+      uint32_t spins = 0;
+      const uint64_t *pb = base + (int64_t)gb * kStride;
+      while (pending) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if ((pending >> u) & 1u) wv[u] = ld_dev(pb + u * kStride);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (((pending >> u) & 1u) && seq_of(wv[u]) == seq) pending &= ~(1u << u);
+        if (pending) {
+          __builtin_amdgcn_s_sleep(1);
+          if (++spins > kSpinLimit) {
+            sh.abort_flag = 1;
+            break;
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (gb + u < g1)
+          acc += k < nsum ? unpack_f64(wv[u]) : (double)(wv[u] & kPayloadMask);
     }
-    __syncthreads();
-    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "agent");
-    __syncthreads();
-    for (int g = 1 + t; g < A->G; g += kBlock) st_dev(&A->boxes[(int64_t)g * kSlot], word(seq, 0));
-  } else {
-    if (t == 0) {
-      uint64_t v;
-      if (!wait_word(&A->boxes[(int64_t)blockIdx.x * kSlot], seq, v)) sh.abort_flag = 1;
-    }
-    __syncthreads();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    sh.part[t] = acc;
   }
-}
-
-// Worker: wait until words 0..nw-1 (nw <= 64) of its own result box all
-// carry seq, polling them with one coalesced load of the calling wave per
-// round (the box is written by the master alone and read by this workgroup
-// alone, so polls never queue behind other workgroups'); lane k returns word k.
-__device__ __forceinline__ uint64_t poll_result(const SweepArgs *__restrict__ A, Shared &sh,
-                                                uint32_t seq, int nw) {
-  const int lane = threadIdx.x & 63;
-  uint64_t v = 0;
-  uint32_t spins = 0;
-  while (true) {
-    if (lane < nw) v = ld_dev(&A->boxes[(int64_t)blockIdx.x * kSlot + lane]);
-    const bool ready = lane >= nw || (uint32_t)(v >> 32) == seq;
-    if (__all(ready)) break;
-    __builtin_amdgcn_s_sleep(1);
-    if (++spins > kSpinLimit) {
-      sh.abort_flag = 1;
-      break;
-    }
-  }
-  return v;
-}
-
-// ------------------------------------------------------------------ master
-// Per-rank data of the tree about to be decided, loaded ahead of its step.
-struct MasterPre {
-  int h, cnt, eta_cnt;
-  float leaf, eta_leaf;
-  double z, eta_z;
-};
-
-// Master: proposal of tree j into ctx c, then its per-rank tree data (heap
-// slot, stored count, current value, leaf normal) into registers.  Called
-// right after the previous step was posted, so these loads overlap the
-// workers' data pass.
-__device__ __forceinline__ MasterPre master_prepare(const SweepArgs *__restrict__ A, Shared &sh,
-                                                    Ctx &c, int j, int64_t s) {
-  const int t = threadIdx.x, H = A->H;
-  const uint32_t wd = load_prop_word(A, j);
-  if (t < kPropWords) ((uint32_t *)&c.pr)[t] = wd;
   lds_barrier();
-  build_ranks(A, c);
-  lds_barrier();
-  MasterPre m{0, 0, 0, 0.f, 0.f, 0.0, 0.0};
-  const int L = c.pr.L, move = c.pr.move, eta = c.pr.eta;
-  if (t < L) {
-    const gptr<const float> lf = gbl((const float *)A->leaf) + (int64_t)j * 2 * H;
-    const gptr<const int32_t> cn = gbl((const int32_t *)A->count) + (int64_t)j * 2 * H;
-    const gptr<const double> zj =
-        gbl((const double *)A->z) + ((int64_t)(s & 1) * A->m + j) * 2 * H;
-    m.h = c.heap_of[t];
-    m.cnt = cn[m.h];
-    m.leaf = lf[m.h];
-    m.z = zj[m.h];
-    if (move != kNone) {
-      m.eta_cnt = cn[eta];
-      m.eta_leaf = lf[eta];
-      m.eta_z = zj[eta];
-    }
+  if (t < K) {
+    double acc = 0.0;
+    for (int seg = 0; seg < nseg; ++seg) acc += sh.part[seg * K + t];
+    sh.tot[t] = acc;
   }
-  return m;
+  lds_barrier();
 }
 
-__device__ __forceinline__ void master_loop(const SweepArgs *__restrict__ A, const Launch &Lc,
-                                            Shared &sh) {
+// Trace record of tree step j (written by the tree's owner): counts and
+// partial sums per slot of the larger tree, new values of the final tree.
+__device__ __noinline__ void trace_tree_step(bart_trace *R, Shared &sh, const Ctx &c, int j,
+                                             int64_t s, int H) {
   const int t = threadIdx.x;
-  const int H = A->H;
-  const bool tracing = Lc.trace != nullptr;
+  const int eta = c.pr.eta, kl = c.pr.rank_l;
+  const int acc = sh.flags & 1, merged = (sh.flags >> 1) & 1;
+  if (t < 256) {
+    const int rnk = c.rank_of[t];
+    const bool in = rnk != 0xFF && t < 2 * H;
+    R->count[t] = in ? (int32_t)sh.cntd[rnk] : 0;
+    R->sum[t] = in ? sh.S[rnk] : 0.0;
+    float lv = 0.f;
+    if (in && !(merged && (t >> 1) == eta)) lv = sh.newv[rnk];
+    if (merged && t == eta) lv = sh.newv[kl];
+    R->leaf_new[t] = lv;
+  }
+  if (t == 0) {
+    R->kind = 0;
+    R->tree = j;
+    R->sweep = s;
+    R->move = c.pr.move;
+    R->eta = eta;
+    R->axis = c.pr.axis;
+    R->cut = c.pr.cut;
+    R->n_grow_cand = c.pr.nG;
+    R->n_prune_cand = c.pr.nP;
+    R->accept = acc;
+    R->n_leaves = c.pr.L;
+    R->log_r = sh.dec_logr;
+    R->ln_u = c.pr.ln_u;
+    R->log_r_scale = 0.0;
+    R->ssr = 0.0;
+    R->sigma2 = sh.sigma2;
+  }
+  if (t < 10) R->pad[t] = 0;
+}
+
+template <int V, int IB>
+__device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, const Launch &Lc,
+                                           Shared &sh) {
+  using IC = IdxChunk<IB>;
+  using ChunkT = typename IC::T;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, w = blockIdx.x;
+  const int G = A->G, H = A->H, m = A->m;
   const uint64_t seed = Lc.seed;
-  const int Wn = A->G - 1;  // worker workgroups 1..G-1
-  if (tracing)
-    for (int q = t; q < (int)(sizeof(bart_trace) / 4); q += kBlock) ((uint32_t *)&sh.rec)[q] = 0u;
+  const bool tracing = Lc.trace != nullptr;
+
+  float r[V][4];
+  uint32_t rk[V];   // ranks of the tree being decided, 4 x 8 bits per chunk
+  uint32_t rk2[V];  // ranks of the next tree
+  ChunkT rawc[V];
+  uint32_t rawx[V];
+  uint32_t okm[V];  // bit b: observation 4*chunk+b exists
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    const int32_t ch = (w * V + v) * kBlock + t;
+    okm[v] = 0;
+    r[v][0] = r[v][1] = r[v][2] = r[v][3] = 0.f;
+    if (ch < A->chunks) {
+      const int32_t rem = A->n - 4 * ch;
+      okm[v] = rem >= 4 ? 15u : ((1u << rem) - 1u);
+      const gptr<const float> q = gbl((const float *)A->resid) + 4 * (int64_t)ch;
+      r[v][0] = q[0];
+      r[v][1] = q[1];
+      r[v][2] = q[2];
+      r[v][3] = q[3];
+    }
+    rk[v] = rk2[v] = 0;
+    rawc[v] = 0;
+    rawx[v] = 0;
+  }
+  for (int k = t; k < kBinFloats; k += kBlock) sh.bins[k] = 0.f;
   if (t == 0) {
     sh.abort_flag = 0;
     sh.dev_err = 0;
+    sh.nr[0] = sh.nr[1] = 0;
     sh.sigma2 = A->ctl->sigma2;
   }
+  if (t < 6) sh.stats[t] = 0;
+
+  // ---- helpers over the pipeline ----
+  // issue the index-row and predictor-row loads of tree `tree` (its proposal in ctx)
+  auto issue_rows = [&](int tree) {
+    const Ctx &c = sh.ctx[tree & (kRing - 1)];
+    const gptr<const ChunkT> row =
+        gbl((const ChunkT *)((const char *)A->idx + (int64_t)tree * A->ldi * IB));
+    const gptr<const uint32_t> xrow = gbl((const uint32_t *)(A->X + (int64_t)c.pr.axis * A->ldx));
+#pragma unroll
+    for (int v = 0; v < V; ++v)
+      if (okm[v]) {
+        const int32_t ch = (w * V + v) * kBlock + t;
+        rawc[v] = row[ch];
+        rawx[v] = xrow[ch];
+      }
+  };
+  // route this workgroup's points through tree `tree` (rows already loaded):
+  // rank of each point's leaf in the larger tree, GROW right-count into nr
+  auto route = [&](int tree, uint32_t (&out)[V]) {
+    const Ctx &c = sh.ctx[tree & (kRing - 1)];
+    const int move = c.pr.move, eta = c.pr.eta, cutv = c.pr.cut;
+    const int grow_eta = move == kGrow ? eta : -1;
+    int nr = 0;
+    uint32_t bad = 0;
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+      uint32_t pk = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int ci = IC::get(rawc[v], b);
+        const int xi = (rawx[v] >> (8 * b)) & 0xff;
+        const uint32_t ok = (okm[v] >> b) & 1u;
+        const int in = ci == grow_eta;
+        const int right = xi >= cutv;
+        const int cp = in ? 2 * eta + right : ci;
+        const int r0 = c.rank_of[cp & 255];
+        bad |= ok & (r0 == 0xFF);
+        // padding observations and (invalid) non-leaf indices use rank 0
+        const int rnk = (ok && r0 != 0xFF) ? r0 : 0;
+        nr += __popcll(__ballot(ok && in && right));
+        pk |= (uint32_t)rnk << (8 * b);
+      }
+      out[v] = pk;
+    }
+    if (bad) sh.dev_err = 1;
+    if (lane == 0 && nr) atomicAdd(&sh.nr[tree & 1], nr);
+  };
+  // partial sums of tree `tree` from the current residuals into sh.red, via
+  // per-lane private bins and a fixed-order fp64 reduction (two barriers)
+  auto reduce = [&](int tree, const uint32_t (&rks)[V]) {
+    const int L = sh.ctx[tree & (kRing - 1)].pr.L;
+    const int setbits = L * kWaves * 64 <= kBinFloats ? 6 : 4;  // 64 or 16 lane sets per wave
+    const int setmask = (1 << setbits) - 1;
+#pragma unroll
+    for (int v = 0; v < V; ++v)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int rnk = (rks[v] >> (8 * b)) & 0xff;
+        // bins are private: a plain read-modify-write (LDS float atomics
+        // serialise across lanes and are many times slower).  With 16 lane
+        // sets, lanes l, l+16, l+32, l+48 share a set and take turns.
+        float &bin = sh.bins[((rnk * kWaves + wave) << setbits) | (lane & setmask)];
+        const float add = ((okm[v] >> b) & 1u) ? r[v][b] : 0.f;
+        if (setbits == 6) {
+          bin += add;
+        } else {
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+            if ((lane >> 4) == g) bin += add;
+        }
+      }
+    lds_barrier();
+    for (int k = wave; k < L; k += kWaves) {
+      double acc = 0.0;
+      if (lane <= setmask) {
+#pragma unroll
+        for (int u = 0; u < kWaves; ++u) {
+          const int q = ((k * kWaves + u) << setbits) | lane;
+          acc += (double)sh.bins[q];
+          sh.bins[q] = 0.f;
+        }
+      }
+      const double tot = wave_total63(acc);
+      if (lane == 63) sh.red[k] = tot;
+    }
+    lds_barrier();
+  };
+  // proposals of trees j0.. j0+2 into the ring, rank tables, rows of j0,
+  // route of j0, rows of j0+1, decision data of j0, partial sums of j0
+  auto refill = [&](int j0, int64_t s) {
+    for (int q = 0; q < 3; ++q)
+      if (j0 + q < m) {
+        const uint32_t wd = load_prop_word(A, j0 + q);
+        if (t < kPropWords) ((uint32_t *)&sh.ctx[(j0 + q) & (kRing - 1)].pr)[t] = wd;
+      }
+    lds_barrier();
+    for (int q = 0; q < 3; ++q)
+      if (j0 + q < m) build_ranks(A, sh.ctx[(j0 + q) & (kRing - 1)]);
+    lds_barrier();
+    issue_rows(j0);
+    const TdRegs tr0 = load_tree_data(A, sh.ctx[j0 & (kRing - 1)], j0, s);
+    route(j0, rk);
+    if (j0 + 1 < m) issue_rows(j0 + 1);
+    store_tree_data(sh.td[j0 & 1], sh.ctx[j0 & (kRing - 1)], tr0);
+    reduce(j0, rk);
+  };
+
+  // ---- prologue: proposals and normals of the first sweep, grid rendezvous
   int64_t s = Lc.s0;
   int j = Lc.j0;
-  if (j < A->m) {
+  if (j < m) {
     gen_proposals(A, seed, s, j);
     gen_normals(A, seed, s, j);
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   __syncthreads();
-  rendezvous(A, sh, 1, true);
-  int cb = 0;
-  MasterPre pre{0, 0, 0, 0.f, 0.f, 0.0, 0.0};
-  if (j < A->m) pre = master_prepare(A, sh, sh.ctx[cb], j, s);
+  if (t == 0) st_dev(mailbox(A, 1, w), mk_word(1, 0));
+  gather(A, sh, 1, 1, 1, 0);
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __syncthreads();
+  if (j < m && !sh.abort_flag) refill(j, s);
 
 #pragma unroll 1
   for (int step = 0; step < Lc.n_steps; ++step) {
     if (sh.abort_flag) break;
     const uint32_t seq = (uint32_t)step + 2;
-    if (j < A->m) {
-      // ================= tree step j: gather, decide, post =================
-      Ctx &c = sh.ctx[cb];
-      const int move = c.pr.move, eta = c.pr.eta, cutv = c.pr.cut, L = c.pr.L;
+    const int par = step & 1;
+    if (j < m) {
+      // ================= tree step j =================
+      Ctx &c = sh.ctx[j & (kRing - 1)];
+      const int move = c.pr.move, eta = c.pr.eta, L = c.pr.L;
       const int kl = c.pr.rank_l, kr = c.pr.rank_r;
+      const bool more1 = (j + 1 < m) && (step + 1 < Lc.n_steps);  // tree j+1 follows
+      const bool more2 = more1 && (j + 2 < m);
+      const bool more3 = more2 && (j + 3 < m);
+      // 1. post this workgroup's partial sums of tree j and its GROW right-count
+      if (t <= L) {
+        const uint64_t pay = t < L ? pack_f64(sh.red[t]) : (uint64_t)sh.nr[j & 1];
+        st_dev(mailbox(A, par, w) + t, mk_word(seq, pay));
+      }
+      // 2. while the mailboxes fill: route tree j+1, load rows of j+2, the
+      //    decision data of j+1 and the proposal of j+3
+      if (more1) route(j + 1, rk2);
+      if (more2) issue_rows(j + 2);
+      TdRegs tdn{0, 0.f, 0.0};
+      if (more1) tdn = load_tree_data(A, sh.ctx[(j + 1) & (kRing - 1)], j + 1, s);
+      const uint32_t pw3 = more3 ? load_prop_word(A, j + 3) : 0u;
+      lds_barrier();  // nr[j&1] read by the poster before it is cleared
+      if (t == L) sh.nr[j & 1] = 0;
+      // 3. totals of tree j, in the same order in every workgroup
+      gather(A, sh, par, seq, L + 1, L);
       const double s2 = sh.sigma2, v2 = A->sigma_mu * A->sigma_mu;
-      // gather: thread (seg, k) sums word k of the workers of its segment, in order,
-      // polling a batch of up to 8 mailboxes with all loads in flight at once
-      const int K1 = 2 * L + 1;
-      int nseg = kBlock / K1;
-      if (nseg > (Wn + 7) / 8) nseg = (Wn + 7) / 8;
-      if (nseg < 1) nseg = 1;
-      if (t < nseg * K1) {
-        const int k = t % K1, seg = t / K1;
-        const int g0 = 1 + (seg * Wn) / nseg, g1 = 1 + ((seg + 1) * Wn) / nseg;
-        double acc = 0.0;
-#pragma unroll 1
-        for (int gb = g0; gb < g1; gb += 8) {
-          uint64_t wv[8];
-          uint32_t pending = (g1 - gb >= 8) ? 0xFFu : ((1u << (g1 - gb)) - 1u);
-          uint32_t spins = 0;
-          while (pending) {
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-              if ((pending >> u) & 1u) wv[u] = ld_dev(&A->slots[(int64_t)(gb + u) * kSlot + k]);
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-              if (((pending >> u) & 1u) && (uint32_t)(wv[u] >> 32) == seq) pending &= ~(1u << u);
-            if (pending) {
-              __builtin_amdgcn_s_sleep(1);
-              if (++spins > kSpinLimit) {
-                sh.abort_flag = 1;
-                break;
-              }
-            }
-          }
-#pragma unroll
-          for (int u = 0; u < 8; ++u)
-            if (gb + u < g1)
-              acc += (k < 2 * L) ? (double)__uint_as_float((uint32_t)wv[u])
-                                 : (double)(uint32_t)wv[u];
-        }
-        sh.part[t] = acc;
-      }
-      lds_barrier();
-      if (t < K1) {
-        double acc = 0.0;
-        for (int seg = 0; seg < nseg; ++seg) acc += sh.part[seg * K1 + t];
-        sh.tot[t] = acc;
-      }
-      lds_barrier();
-      // partial sums S_h = R_h + n_h * (old value) (sec. 3.3 item 8)
-      const double nR = sh.tot[2 * L];
+      const TreeData &td = sh.td[j & 1];
+      const double nR = sh.tot[L];
       if (t < L) {
-        const int h = pre.h;
+        const int h = c.heap_of[t];
         const bool child = (move == kGrow) && ((h >> 1) == eta);
-        const double nk = child ? ((h & 1) ? nR : (double)pre.eta_cnt - nR) : (double)pre.cnt;
-        const float mo = child ? pre.eta_leaf : pre.leaf;
+        const double nk = child ? ((h & 1) ? nR : (double)td.eta_cnt - nR) : (double)td.cnt[t];
+        const float mo = child ? td.eta_mu : td.mu[t];
         sh.cntd[t] = nk;
         sh.mu_old[t] = mo;
-        sh.S[t] = (sh.tot[2 * t] + sh.tot[2 * t + 1]) + nk * (double)mo;
+        // partial sums S_h = R_h + n_h * (old value) (sec. 3.3 item 8)
+        sh.S[t] = sh.tot[t] + nk * (double)mo;
       }
       lds_barrier();
       // accept / reject (item 9)
@@ -427,301 +582,26 @@ __device__ __forceinline__ void master_loop(const SweepArgs *__restrict__ A, con
         sh.flags = acc | (merged << 1);
       }
       lds_barrier();
-      // leaf draws of the final tree (items 4, 5, 10); box word 0 holds the
-      // flags, words 1..L the residual deltas
+      // leaf draws of the final tree (items 4, 5, 10) and residual deltas
       const int flags = sh.flags, acc = flags & 1, merged = (flags >> 1) & 1;
-      if (t == 0) sh.res[0] = (uint32_t)flags;
       if (t < L) {
-        const int h = pre.h;
+        const int h = c.heap_of[t];
         const bool to_eta = merged && ((h >> 1) == eta);
         const double nf = to_eta ? sh.dec_n_eta : sh.cntd[t];
         const double Sf = to_eta ? sh.dec_S_eta : sh.S[t];
         const double prec = nf / s2 + 1.0 / v2;
         const double mean = (Sf / s2 + A->mu_mu / v2) / prec;
-        const float mu_new = (float)(mean + (to_eta ? pre.eta_z : pre.z) / sqrt(prec));
-        sh.res[1 + t] = __float_as_uint(sh.mu_old[t] - mu_new);
+        const float mu_new = (float)(mean + (to_eta ? td.eta_z : td.z[t]) / sqrt(prec));
+        sh.delta[t] = sh.mu_old[t] - mu_new;
         sh.newv[t] = mu_new;
+        sh.fin[t] = (uint16_t)(to_eta ? eta : h);
       }
+      // stage what later trees need
+      if (more3 && t < kPropWords) ((uint32_t *)&sh.ctx[(j + 3) & (kRing - 1)].pr)[t] = pw3;
+      if (more1) store_tree_data(sh.td[(j + 1) & 1], sh.ctx[(j + 1) & (kRing - 1)], tdn);
       lds_barrier();
-      // broadcast into every worker's box: word k of box g by thread (g, k)
-      for (int q = t; q < Wn * (L + 1); q += kBlock) {
-        const int g = 1 + q / (L + 1), k = q % (L + 1);
-        st_dev(&A->boxes[(int64_t)g * kSlot + k], word(seq, sh.res[k]));
-      }
-      // the final tree: values and counts of its leaves, structure change
-      if (t < L) {
-        const int h = pre.h;
-        const bool to_eta = merged && ((h >> 1) == eta);
-        const int f = to_eta ? eta : h;
-        const double nf = to_eta ? sh.dec_n_eta : sh.cntd[t];
-        gbl(A->leaf)[(int64_t)j * 2 * H + f] = sh.newv[t];
-        gbl(A->count)[(int64_t)j * 2 * H + f] = (int32_t)nf;
-        if (tracing) {
-          sh.rec.leaf_new[f] = sh.newv[t];
-          sh.rec.count[h] = (int32_t)sh.cntd[t];
-          sh.rec.sum[h] = sh.S[t];
-        }
-      }
-      if (t == 0) {
-        const gptr<uint8_t> ct = gbl(A->cut) + (int64_t)j * H;
-        const gptr<uint16_t> ax = gbl(A->axis) + (int64_t)j * H;
-        if (move == kGrow && acc) {
-          ax[eta] = (uint16_t)c.pr.axis;
-          ct[eta] = (uint8_t)cutv;
-          if (2 * eta < H) ct[2 * eta] = 0;
-          if (2 * eta + 1 < H) ct[2 * eta + 1] = 0;
-        }
-        if (move == kPrune && acc) ct[eta] = 0;
-        const gptr<uint64_t> st = gbl(A->ctl->stats);
-        st[0] += move == kGrow;
-        st[1] += move == kPrune;
-        st[2] += move == kGrow && acc;
-        st[3] += move == kPrune && acc;
-        st[4] += 1;
-        st[5] += (uint64_t)(L - merged);
-        if (tracing) {
-          bart_trace &R = sh.rec;
-          R.kind = 0;
-          R.tree = j;
-          R.sweep = s;
-          R.move = move;
-          R.eta = eta;
-          R.axis = c.pr.axis;
-          R.cut = cutv;
-          R.n_grow_cand = c.pr.nG;
-          R.n_prune_cand = c.pr.nP;
-          R.accept = acc;
-          R.n_leaves = L;
-          R.log_r = sh.dec_logr;
-          R.ln_u = c.pr.ln_u;
-          R.sigma2 = s2;
-        }
-      }
-      if (tracing) {
-        __syncthreads();
-        flush_trace(Lc.trace + step, &sh.rec);
-      }
-      ++j;
-      // next tree: its proposal and tree data, while the workers apply and route
-      if (j < A->m && step + 1 < Lc.n_steps) pre = master_prepare(A, sh, sh.ctx[cb ^ 1], j, s);
-      cb ^= 1;
-    } else {
-      // ================= sigma^2 step (sec. 3.3, "Sampling the error variance")
-      const bool more = step + 1 < Lc.n_steps;
-      if (more) {
-        gen_proposals(A, seed, s + 1, 0);
-        gen_normals(A, seed, s + 1, 0);
-      }
-#pragma unroll 1
-      for (int g = 1 + t; g < A->G; g += kBlock) {
-        uint64_t v;
-        if (!wait_word(&A->slots[(int64_t)g * kSlot], seq, v)) sh.abort_flag = 1;
-        sh.part[g] = (double)__uint_as_float((uint32_t)v);
-      }
-      __syncthreads();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-      if (t == 0) {
-        double acc = 0.0;
-        for (int g = 1; g < A->G; ++g) acc += sh.part[g];
-        const double s2 = draw_sigma2(A, seed, s, acc);
-        sh.sigma2 = s2;
-        A->ctl->sigma2 = s2;
-        A->ctl->sweep = s + 1;
-        if (tracing) {
-          sh.rec.kind = 1;
-          sh.rec.tree = A->m;
-          sh.rec.sweep = s;
-          sh.rec.ssr = acc;
-          sh.rec.sigma2 = s2;
-        }
-      }
-      __syncthreads();
-      if (tracing) flush_trace(Lc.trace + step, &sh.rec);
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-      __syncthreads();
-      for (int g = 1 + t; g < A->G; g += kBlock) st_dev(&A->boxes[(int64_t)g * kSlot], word(seq, 0));
-      j = 0;
-      ++s;
-      if (more) pre = master_prepare(A, sh, sh.ctx[cb], 0, s);
-    }
-    lds_barrier();
-  }
-  if (t == 0 && (sh.abort_flag || sh.dev_err))
-    atomicOr(&A->ctl->error, (sh.abort_flag ? BART_DEVERR_TIMEOUT : 0u) |
-                                 (sh.dev_err ? BART_DEVERR_CACHE : 0u));
-}
-
-// ------------------------------------------------------------------ workers
-template <int V, int IB>
-__device__ __forceinline__ void worker_loop(const SweepArgs *__restrict__ A, const Launch &Lc,
-                                            Shared &sh) {
-  using IC = IdxChunk<IB>;
-  using ChunkT = typename IC::T;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, w = blockIdx.x;
-  const int wk = w - 1;  // worker index
-  const uint64_t seed = Lc.seed;
-
-  float r[V][4];
-  uint32_t rk[V];
-  ChunkT rawc[V];
-  uint32_t rawx[V];
-  uint32_t okm[V];  // bit b: observation 4*chunk+b exists
-#pragma unroll
-  for (int v = 0; v < V; ++v) {
-    const int32_t ch = (wk * V + v) * kBlock + t;
-    okm[v] = 0;
-    r[v][0] = r[v][1] = r[v][2] = r[v][3] = 0.f;
-    if (ch < A->chunks) {
-      const int32_t rem = A->n - 4 * ch;
-      okm[v] = rem >= 4 ? 15u : ((1u << rem) - 1u);
-      const gptr<const float> q = gbl((const float *)A->resid) + 4 * (int64_t)ch;
-      r[v][0] = q[0];
-      r[v][1] = q[1];
-      r[v][2] = q[2];
-      r[v][3] = q[3];
-    }
-    rk[v] = 0;
-    rawc[v] = 0;
-    rawx[v] = 0;
-  }
-  for (int k = t; k < kBinFloats; k += kBlock) sh.bins[k] = 0.f;
-  if (t == 0) {
-    sh.abort_flag = 0;
-    sh.dev_err = 0;
-    sh.red_nr = 0;
-  }
-  int64_t s = Lc.s0;
-  int j = Lc.j0;
-  if (j < A->m) gen_normals(A, seed, s, j);
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
-  rendezvous(A, sh, 1, false);
-
-  int cb = 0;  // ctx buffer of the tree being stepped
-  // proposal word (already loaded) -> LDS, rank table, then the row loads of that tree
-  auto issue = [&](int tree, uint32_t wd, int buf) {
-    Ctx &c = sh.ctx[buf];
-    if (t < kPropWords) ((uint32_t *)&c.pr)[t] = wd;
-    lds_barrier();
-    build_ranks(A, c);
-    const gptr<const ChunkT> row =
-        gbl((const ChunkT *)((const char *)A->idx + (int64_t)tree * A->ldi * IB));
-    const gptr<const uint32_t> xrow = gbl((const uint32_t *)(A->X + (int64_t)c.pr.axis * A->ldx));
-#pragma unroll
-    for (int v = 0; v < V; ++v)
-      if (okm[v]) {
-        const int32_t ch = (wk * V + v) * kBlock + t;
-        rawc[v] = row[ch];
-        rawx[v] = xrow[ch];
-      }
-  };
-  if (j < A->m && !sh.abort_flag) issue(j, load_prop_word(A, j), cb);
-  __syncthreads();
-
-#pragma unroll 1
-  for (int step = 0; step < Lc.n_steps; ++step) {
-    if (sh.abort_flag) break;
-    const uint32_t seq = (uint32_t)step + 2;
-    if (j < A->m) {
-      // ================= tree step j =================
-      Ctx &c = sh.ctx[cb];
-      const int move = c.pr.move, eta = c.pr.eta, cutv = c.pr.cut, L = c.pr.L;
-      const int setbits = L <= 32 ? 6 : 4;  // 64 or 16 lane sets per wave
-      const int setmask = (1 << setbits) - 1;
-      const int grow_eta = move == kGrow ? eta : -1;
-      const bool next_tree = (j + 1 < A->m) && (step + 1 < Lc.n_steps);
-      // 1. route (branch-free) and 2. per-lane bins
-      int nr = 0;
-      uint32_t bad = 0;
-#pragma unroll
-      for (int v = 0; v < V; ++v) {
-        uint32_t pk = 0;
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const int ci = IC::get(rawc[v], b);
-          const int xi = (rawx[v] >> (8 * b)) & 0xff;
-          const uint32_t ok = (okm[v] >> b) & 1u;
-          const int in = ci == grow_eta;
-          const int right = xi >= cutv;
-          const int cp = in ? 2 * eta + right : ci;
-          const int r0 = c.rank_of[cp & 255];
-          bad |= ok & (r0 == 0xFF);
-          // padding observations and (invalid) non-leaf indices use rank 0
-          const int rnk = (ok && r0 != 0xFF) ? r0 : 0;
-          nr += __popcll(__ballot(ok && in && right));
-          pk |= (uint32_t)rnk << (8 * b);
-          // bins are private: a plain read-modify-write (LDS float atomics
-          // serialise across lanes and are many times slower).  With 16 lane
-          // sets, lanes l, l+16, l+32, l+48 share a set and take turns.
-          float &bin = sh.bins[((rnk * kWaves + wave) << setbits) | (lane & setmask)];
-          const float add = ok ? r[v][b] : 0.f;
-          if (setbits == 6) {
-            bin += add;
-          } else {
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-              if ((lane >> 4) == g) bin += add;
-          }
-        }
-        rk[v] = pk;
-      }
-      // next tree's proposal word: loaded after the route so that the wait for
-      // this step's row data does not also wait for it
-      const uint32_t nxt = next_tree ? load_prop_word(A, j + 1) : 0u;
-      if (bad) sh.dev_err = 1;
-      if (lane == 0 && nr) atomicAdd(&sh.red_nr, nr);
-      lds_barrier();
-      // 3. fixed-order workgroup reduction, bins zeroed for the next step
-      for (int k = wave; k < L; k += kWaves) {
-        double acc = 0.0;
-        if (lane <= setmask) {
-#pragma unroll
-          for (int u = 0; u < kWaves; ++u) {
-            const int q = ((k * kWaves + u) << setbits) | lane;
-            acc += (double)sh.bins[q];
-            sh.bins[q] = 0.f;
-          }
-        }
-        const double tot = wave_total63(acc);
-        if (lane == 63) sh.red[k] = tot;
-      }
-      lds_barrier();
-      // each partial as an fp32 (hi, lo) pair: hi + lo carries ~48 bits of the fp64 sum
-      if (t < 2 * L) {
-        const double x = sh.red[t >> 1];
-        const float hi = (float)x;
-        const float part = (t & 1) ? (float)(x - (double)hi) : hi;
-        st_dev(&A->slots[(int64_t)w * kSlot + t], word(seq, __float_as_uint(part)));
-      }
-      if (t == 2 * L) {
-        st_dev(&A->slots[(int64_t)w * kSlot + t], word(seq, (uint32_t)sh.red_nr));
-        sh.red_nr = 0;  // next added to after several barriers
-      }
-      // prefetch the next tree while the master decides
-      if (next_tree) issue(j + 1, nxt, cb ^ 1);
-      // 5. fetch flags and deltas, update residuals and the index row
-      if (wave == 0) {
-        const uint64_t v = poll_result(A, sh, seq, L + 1 < 64 ? L + 1 : 64);
-        if (lane == 0) sh.flags = (int)(uint32_t)v;
-        if (lane >= 1 && lane <= L) sh.delta[lane - 1] = __uint_as_float((uint32_t)v);
-        if (L + 1 > 64) {
-          // more than 63 leaves: the remaining deltas, already posted (seq checked)
-          for (int k = 64 + lane; k <= L; k += 64) {
-            uint64_t u;
-            if (!wait_word(&A->boxes[(int64_t)w * kSlot + k], seq, u)) sh.abort_flag = 1;
-            sh.delta[k - 1] = __uint_as_float((uint32_t)u);
-          }
-        }
-      }
-      lds_barrier();
-      const int acc = sh.flags & 1, merged = (sh.flags >> 1) & 1;
-      if (t < L) {
-        const int h = c.heap_of[t];
-        sh.fin[t] = (uint16_t)((merged && (h >> 1) == eta) ? eta : h);
-      }
-      lds_barrier();
+      // 4. residuals and index row (item 11)
       const bool changed = acc && move != kNone;
-      const int kl = c.pr.rank_l, kr = c.pr.rank_r;
       const gptr<ChunkT> row = gbl((ChunkT *)((char *)A->idx + (int64_t)j * A->ldi * IB));
 #pragma unroll
       for (int v = 0; v < V; ++v) {
@@ -735,12 +615,53 @@ __device__ __forceinline__ void worker_loop(const SweepArgs *__restrict__ A, con
           touch |= (rnk == kl) || (rnk == kr);
           out = IC::put(out, b, sh.fin[rnk]);
         }
-        if (changed && touch && okm[v]) row[(wk * V + v) * kBlock + t] = out;
+        if (changed && touch && okm[v]) row[(w * V + v) * kBlock + t] = out;
       }
-      cb ^= 1;
+      // the owner stores the final tree: values and counts of its leaves,
+      // structure change, move statistics and the trace record
+      if (j % G == w) {
+        if (t < L) {
+          const int h = c.heap_of[t];
+          const bool to_eta = merged && ((h >> 1) == eta);
+          const int f = to_eta ? eta : h;
+          const double nf = to_eta ? sh.dec_n_eta : sh.cntd[t];
+          gbl(A->leaf)[(int64_t)j * 2 * H + f] = sh.newv[t];
+          gbl(A->count)[(int64_t)j * 2 * H + f] = (int32_t)nf;
+        }
+        if (t == 0) {
+          const gptr<uint8_t> ct = gbl(A->cut) + (int64_t)j * H;
+          const gptr<uint16_t> ax = gbl(A->axis) + (int64_t)j * H;
+          if (move == kGrow && acc) {
+            ax[eta] = (uint16_t)c.pr.axis;
+            ct[eta] = (uint8_t)c.pr.cut;
+            if (2 * eta < H) ct[2 * eta] = 0;
+            if (2 * eta + 1 < H) ct[2 * eta + 1] = 0;
+          }
+          if (move == kPrune && acc) ct[eta] = 0;
+        }
+        if (tracing) trace_tree_step(Lc.trace + step, sh, c, j, s, H);
+      }
+      if (w == 0 && t == 0) {
+        sh.stats[0] += move == kGrow;
+        sh.stats[1] += move == kPrune;
+        sh.stats[2] += move == kGrow && acc;
+        sh.stats[3] += move == kPrune && acc;
+        sh.stats[4] += 1;
+        sh.stats[5] += (uint64_t)(L - merged);
+      }
+      // 5. tree j+1: rank table of j+3, partial sums from the updated residuals
+      if (more3) build_ranks(A, sh.ctx[(j + 3) & (kRing - 1)]);
+      if (more1) {
+        reduce(j + 1, rk2);
+#pragma unroll
+        for (int v = 0; v < V; ++v) rk[v] = rk2[v];
+      } else {
+        lds_barrier();
+      }
       ++j;
     } else {
-      // ================= sigma^2 step: partial sum of squared residuals
+      // ================= sigma^2 step (sec. 3.3, "Sampling the error variance")
+      __syncthreads();  // this workgroup's tree writes are visible to all its threads
       double ssr = 0.0;
 #pragma unroll
       for (int v = 0; v < V; ++v)
@@ -751,37 +672,72 @@ __device__ __forceinline__ void worker_loop(const SweepArgs *__restrict__ A, con
         }
       ssr = wave_total63(ssr);
       if (lane == 63) sh.wave_part[wave] = ssr;
-      const bool more = step + 1 < Lc.n_steps;
-      if (more) gen_normals(A, seed, s + 1, 0);
+      // the next sweep's proposals (owners) and normals, published by the
+      // release below together with this sweep's tree writes
+      gen_proposals(A, seed, s + 1, 0);
+      gen_normals(A, seed, s + 1, 0);
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
       __syncthreads();
       if (t == 0) {
         double acc = 0.0;
         for (int u = 0; u < kWaves; ++u) acc += sh.wave_part[u];
-        st_dev(&A->slots[(int64_t)w * kSlot], word(seq, __float_as_uint((float)acc)));
-        uint64_t v;
-        if (!wait_word(&A->boxes[(int64_t)w * kSlot], seq, v)) sh.abort_flag = 1;
+        st_dev(mailbox(A, par, w), mk_word(seq, pack_f64(acc)));
+      }
+      gather(A, sh, par, seq, 1, 1);
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      if (t == 0) {
+        const double ssr_all = sh.tot[0];
+        const double s2 = draw_sigma2(A, seed, s, ssr_all);
+        sh.sigma2 = s2;
+        if (w == 0) {
+          A->ctl->sigma2 = s2;
+          A->ctl->sweep = s + 1;
+          if (tracing) {
+            bart_trace *R = Lc.trace + step;
+            R->kind = 1;
+            R->tree = m;
+            R->sweep = s;
+            R->move = 0;
+            R->ssr = ssr_all;
+            R->sigma2 = s2;
+          }
+        }
+      }
+      if (tracing && w == 0) {
+        // the rest of the sigma^2 record is zero
+        bart_trace *R = Lc.trace + step;
+        if (t < 256) {
+          R->count[t] = 0;
+          R->sum[t] = 0.0;
+          R->leaf_new[t] = 0.f;
+        }
+        if (t >= 1 && t < 10) R->pad[t] = 0;
+        if (t == 1) {
+          R->eta = R->axis = R->cut = R->n_grow_cand = R->n_prune_cand = R->accept = 0;
+          R->n_leaves = 0;
+          R->log_r = R->ln_u = R->log_r_scale = 0.0;
+          R->pad[0] = 0;
+        }
       }
       __syncthreads();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       j = 0;
       ++s;
-      if (more) issue(0, load_prop_word(A, 0), cb);
+      if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s);
     }
-    lds_barrier();
   }
 
-  // ---- epilogue: residuals back to HBM, device errors
+  // ---- epilogue: residuals back to HBM, statistics, device errors
 #pragma unroll
   for (int v = 0; v < V; ++v)
     if (okm[v]) {
-      const int32_t ch = (wk * V + v) * kBlock + t;
+      const int32_t ch = (w * V + v) * kBlock + t;
       const gptr<float> q = gbl(A->resid) + 4 * (int64_t)ch;
       q[0] = r[v][0];
       q[1] = r[v][1];
       q[2] = r[v][2];
       q[3] = r[v][3];
     }
+  if (w == 0 && t < 6) A->ctl->stats[t] += sh.stats[t];
   if (t == 0 && (sh.abort_flag || sh.dev_err))
     atomicOr(&A->ctl->error, (sh.abort_flag ? BART_DEVERR_TIMEOUT : 0u) |
                                  (sh.dev_err ? BART_DEVERR_CACHE : 0u));
@@ -790,10 +746,7 @@ __device__ __forceinline__ void worker_loop(const SweepArgs *__restrict__ A, con
 template <int V, int IB>
 __global__ void __launch_bounds__(kBlock) sweep_kernel(const SweepArgs *__restrict__ A, Launch Lc) {
   __shared__ Shared sh;
-  if (blockIdx.x == 0)
-    master_loop(A, Lc, sh);
-  else
-    worker_loop<V, IB>(A, Lc, sh);
+  sweep_body<V, IB>(A, Lc, sh);
 }
 
 }  // namespace bart

@@ -29,6 +29,7 @@ CASES = {
     "w1_ragged_tiny": (1, dict(n=37, p=3, m=5), 2, 3 * 6, 0, COOP),
     "w2_ragged": (2, dict(n=20011, m=60), 2, 61 + 30, 0, COOP),
     "w2_many_wg": (2, dict(n=40003, p=30, m=40), 2, 41 * 2, 10, ORDINARY),
+    "w2_idle_wg": (2, dict(n=20011, p=30, m=30), 2, 31 * 2, 8, COOP),
     "w4_u16": (4, dict(n=30001, p=20, m=50), 2, 51 + 10, 0, COOP),
     "w5_depth8": (5, dict(n=25003, p=1000, m=120), 2, 121 + 5, 0, COOP),
 }

@@ -49,7 +49,7 @@ def _cfg(b, **kw):
 @pytest.mark.parametrize("bad", [dict(n=0), dict(max_depth=1), dict(max_depth=9),
                                  dict(idx_bytes=3), dict(x_stride=1000), dict(x_stride=512),
                                  dict(alpha=1.5), dict(sigma_mu=0.0), dict(nu=-1.0),
-                                 dict(p_grow=2.0), dict(grid=300), dict(grid=1), dict(lam=float("nan")),
+                                 dict(p_grow=2.0), dict(grid=300), dict(grid=-1), dict(lam=float("nan")),
                                  dict(launch=2), dict(launch=-1), dict(reserved=1)])
 def test_invalid_configs_are_rejected(b, bad):
     cfg = _cfg(b, **bad)
