@@ -135,13 +135,13 @@ struct Shared {
   double tot[kMaxLeaves + 1];
   double S[kMaxLeaves];
   double cntd[kMaxLeaves];
-  float mu_old[kMaxLeaves];
-  float delta[kMaxLeaves];
-  float newv[kMaxLeaves];
-  uint16_t fin[kMaxLeaves];
+  float newv[kMaxLeaves];      // new value of each larger-tree leaf if it stays a leaf
+  float dlt[kMaxLeaves];       // its residual delta: old value - new value
+  float newv_m;                // new value of eta if the move ends merged
+  float dlt_m[2];              // residual deltas of the two children in that case
   double wave_part[kWaves];
   double sigma2;
-  double dec_logr, dec_S_eta, dec_n_eta;
+  double dec_logr;
   uint64_t stats[6];  // workgroup 0: move statistics of this launch
   int nr[2];  // GROW right-counts of the trees being routed, by tree parity
   int flags;  // bit0 accept, bit1 merged
@@ -266,35 +266,38 @@ __device__ __forceinline__ uint64_t *mailbox(const SweepArgs *__restrict__ A, in
   return A->pub + ((int64_t)par * kMaxGrid + g) * kStride;
 }
 
-// Read word k < K of every mailbox of buffer par once all carry step number
-// seq, and sum them in a fixed order into sh.tot[k] (fp64; words k < nsum
-// are fp64 values, the others counts).  Thread (seg, k) sums the workgroups
-// of its segment in increasing order, polling up to 4 mailboxes at a time;
-// thread k then sums the segments in increasing order.  Every workgroup runs
-// the same partition, so every workgroup gets the same bits.  Ends with an
-// LDS barrier.
-__device__ __forceinline__ void gather(const SweepArgs *__restrict__ A, Shared &sh, int par,
-                                       uint32_t seq, int K, int nsum) {
+// Poll word k < K of every mailbox of buffer par until all carry step number
+// seq.  The workgroups are split into nseg segments of 8 nb consecutive
+// workgroups, nb the fewest batches of 8 that let nseg * K threads cover
+// them; thread (seg, k) sums word k of its segment in increasing workgroup
+// order in fp64 into sh.part[seg * K + k] (words k < nsum are fp64 values,
+// the others counts), with all loads of a batch in flight at once.  The
+// partition depends only on G and K, so every workgroup sums in the same
+// order.  Returns nseg.  Ends with an LDS barrier.
+__device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, Shared &sh, int par,
+                                            uint32_t seq, int K, int nsum) {
   const int t = threadIdx.x, G = A->G;
-  int nseg = kBlock / K;
-  if (nseg > G) nseg = G;
+  int nb = 1;
+  while (K * ((G + 8 * nb - 1) / (8 * nb)) > kBlock) ++nb;
+  const int span = 8 * nb;
+  const int nseg = (G + span - 1) / span;  // nseg * K <= kBlock
   if (t < nseg * K) {
     const int k = t % K, seg = t / K;
-    const int g0 = (seg * G) / nseg, g1 = ((seg + 1) * G) / nseg;
+    const int g0 = seg * span, g1 = min(G, g0 + span);
     const uint64_t *base = A->pub + (int64_t)par * kMaxGrid * kStride + k;
     double acc = 0.0;
 #pragma unroll 1
-    for (int gb = g0; gb < g1; gb += 4) {
-      uint64_t wv[4];
-      uint32_t pending = (g1 - gb >= 4) ? 0xFu : ((1u << (g1 - gb)) - 1u);
+    for (int gb = g0; gb < g1; gb += 8) {
+      uint64_t wv[8];
+      uint32_t pending = (g1 - gb >= 8) ? 0xFFu : ((1u << (g1 - gb)) - 1u);
       uint32_t spins = 0;
       const uint64_t *pb = base + (int64_t)gb * kStride;
       while (pending) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < 8; ++u)
           if ((pending >> u) & 1u) wv[u] = ld_dev(pb + u * kStride);
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < 8; ++u)
           if (((pending >> u) & 1u) && seq_of(wv[u]) == seq) pending &= ~(1u << u);
         if (pending) {
           __builtin_amdgcn_s_sleep(1);
@@ -305,18 +308,28 @@ __device__ __forceinline__ void gather(const SweepArgs *__restrict__ A, Shared &
         }
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < 8; ++u)
         if (gb + u < g1)
           acc += k < nsum ? unpack_f64(wv[u]) : (double)(wv[u] & kPayloadMask);
     }
     sh.part[t] = acc;
   }
   lds_barrier();
-  if (t < K) {
-    double acc = 0.0;
-    for (int seg = 0; seg < nseg; ++seg) acc += sh.part[seg * K + t];
-    sh.tot[t] = acc;
-  }
+  return nseg;
+}
+
+// Total of word k over all mailboxes: the segments summed in increasing order.
+__device__ __forceinline__ double seg_total(const Shared &sh, int nseg, int K, int k) {
+  double acc = 0.0;
+  for (int seg = 0; seg < nseg; ++seg) acc += sh.part[seg * K + k];
+  return acc;
+}
+
+// Grid-wide sum of one fp64 word per workgroup (sigma^2 step), into sh.tot[0].
+__device__ __forceinline__ void gather_total(const SweepArgs *__restrict__ A, Shared &sh, int par,
+                                             uint32_t seq, int nsum) {
+  const int nseg = gather_polls(A, sh, par, seq, 1, nsum);
+  if (threadIdx.x == 0) sh.tot[0] = seg_total(sh, nseg, 1, 0);
   lds_barrier();
 }
 
@@ -325,7 +338,7 @@ __device__ __forceinline__ void gather(const SweepArgs *__restrict__ A, Shared &
 __device__ __noinline__ void trace_tree_step(bart_trace *R, Shared &sh, const Ctx &c, int j,
                                              int64_t s, int H) {
   const int t = threadIdx.x;
-  const int eta = c.pr.eta, kl = c.pr.rank_l;
+  const int eta = c.pr.eta;
   const int acc = sh.flags & 1, merged = (sh.flags >> 1) & 1;
   if (t < 256) {
     const int rnk = c.rank_of[t];
@@ -334,7 +347,7 @@ __device__ __noinline__ void trace_tree_step(bart_trace *R, Shared &sh, const Ct
     R->sum[t] = in ? sh.S[rnk] : 0.0;
     float lv = 0.f;
     if (in && !(merged && (t >> 1) == eta)) lv = sh.newv[rnk];
-    if (merged && t == eta) lv = sh.newv[kl];
+    if (merged && t == eta) lv = sh.newv_m;
     R->leaf_new[t] = lv;
   }
   if (t == 0) {
@@ -517,7 +530,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   __syncthreads();
   if (t == 0) st_dev(mailbox(A, 1, w), mk_word(1, 0));
-  gather(A, sh, 1, 1, 1, 0);
+  gather_total(A, sh, 1, 1, 0);
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __syncthreads();
   if (j < m && !sh.abort_flag) refill(j, s);
@@ -549,59 +562,96 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       const uint32_t pw3 = more3 ? load_prop_word(A, j + 3) : 0u;
       lds_barrier();  // nr[j&1] read by the poster before it is cleared
       if (t == L) sh.nr[j & 1] = 0;
-      // 3. totals of tree j, in the same order in every workgroup
-      gather(A, sh, par, seq, L + 1, L);
+      // 3. totals of tree j, in the same order in every workgroup: polls into
+      //    per-segment partials, then one wave reduces a word over the
+      //    segments with the fixed-order DPP tree (nseg <= 32 lanes)
+      const int K = L + 1;
+      const int nseg = gather_polls(A, sh, par, seq, K, L);
       const double s2 = sh.sigma2, v2 = A->sigma_mu * A->sigma_mu;
       const TreeData &td = sh.td[j & 1];
-      const double nR = sh.tot[L];
-      if (t < L) {
-        const int h = c.heap_of[t];
+      auto total = [&](int k) {
+        return wave_total63(lane < nseg ? sh.part[lane * K + k] : 0.0);  // valid in lane 63
+      };
+      // count and partial sum S_h = R_h + n_h * (old value) of rank k (sec. 3.3
+      // item 8); nR is the GROW right-count
+      auto leaf_stats = [&](int k, double R, double nR, double &nk, float &mo) {
+        const int h = c.heap_of[k];
         const bool child = (move == kGrow) && ((h >> 1) == eta);
-        const double nk = child ? ((h & 1) ? nR : (double)td.eta_cnt - nR) : (double)td.cnt[t];
-        const float mo = child ? td.eta_mu : td.mu[t];
-        sh.cntd[t] = nk;
-        sh.mu_old[t] = mo;
-        // partial sums S_h = R_h + n_h * (old value) (sec. 3.3 item 8)
-        sh.S[t] = sh.tot[t] + nk * (double)mo;
-      }
-      lds_barrier();
-      // accept / reject (item 9)
-      if (t == 0) {
-        int acc = 0, merged = 0;
-        double logr = 0.0;
-        if (move != kNone) {
-          const double llr =
-              split_llr(s2, A->mu_mu, v2, sh.cntd[kl], sh.S[kl], sh.cntd[kr], sh.S[kr]);
-          logr = c.pr.c_prior + (move == kGrow ? llr : -llr);
-          acc = c.pr.ln_u < logr ? 1 : 0;
-          merged = (move == kGrow && !acc) || (move == kPrune && acc);
-          sh.dec_S_eta = sh.S[kl] + sh.S[kr];
-          sh.dec_n_eta = sh.cntd[kl] + sh.cntd[kr];
-        }
-        sh.dec_logr = logr;
-        sh.flags = acc | (merged << 1);
-      }
-      lds_barrier();
-      // leaf draws of the final tree (items 4, 5, 10) and residual deltas
-      const int flags = sh.flags, acc = flags & 1, merged = (flags >> 1) & 1;
-      if (t < L) {
-        const int h = c.heap_of[t];
-        const bool to_eta = merged && ((h >> 1) == eta);
-        const double nf = to_eta ? sh.dec_n_eta : sh.cntd[t];
-        const double Sf = to_eta ? sh.dec_S_eta : sh.S[t];
+        nk = child ? ((h & 1) ? nR : (double)td.eta_cnt - nR) : (double)td.cnt[k];
+        mo = child ? td.eta_mu : td.mu[k];
+        return R + nk * (double)mo;
+      };
+      // conditional draw of a leaf value (items 4, 5, 10)
+      auto draw_leaf = [&](double nf, double Sf, double z) {
         const double prec = nf / s2 + 1.0 / v2;
         const double mean = (Sf / s2 + A->mu_mu / v2) / prec;
-        const float mu_new = (float)(mean + (to_eta ? td.eta_z : td.z[t]) / sqrt(prec));
-        sh.delta[t] = sh.mu_old[t] - mu_new;
-        sh.newv[t] = mu_new;
-        sh.fin[t] = (uint16_t)(to_eta ? eta : h);
+        return (float)(mean + z / sqrt(prec));
+      };
+      // The decision (item 9) and every draw are computed at once by
+      // different waves: the draws do not depend on the decision, only which
+      // of them is used.  Waves 0-3 handle the two leaves of the move
+      // (decision, each child's own draw, the merged draw), waves 4-7 the
+      // other leaves.
+      if (move != kNone && wave < 4) {
+        const double nR = move == kGrow ? total(L) : 0.0;
+        const double Rl = total(kl), Rr = total(kr);
+        if (lane == 63) {
+          double nl, nr;
+          float mol, mor;
+          const double Sl = leaf_stats(kl, Rl, nR, nl, mol);
+          const double Sr = leaf_stats(kr, Rr, nR, nr, mor);
+          if (wave == 0) {
+            const double llr = split_llr(s2, A->mu_mu, v2, nl, Sl, nr, Sr);
+            const double logr = c.pr.c_prior + (move == kGrow ? llr : -llr);
+            const int acc = c.pr.ln_u < logr ? 1 : 0;
+            const int merged = (move == kGrow && !acc) || (move == kPrune && acc);
+            sh.dec_logr = logr;
+            sh.flags = acc | (merged << 1);
+          } else if (wave == 3) {
+            const float vm = draw_leaf(nl + nr, Sl + Sr, td.eta_z);
+            sh.newv_m = vm;
+            sh.dlt_m[0] = mol - vm;
+            sh.dlt_m[1] = mor - vm;
+          } else {
+            const int k = wave == 1 ? kl : kr;
+            const double nk = wave == 1 ? nl : nr, Sk = wave == 1 ? Sl : Sr;
+            const float mo = wave == 1 ? mol : mor;
+            const float v = draw_leaf(nk, Sk, td.z[k]);
+            sh.cntd[k] = nk;
+            sh.S[k] = Sk;
+            sh.newv[k] = v;
+            sh.dlt[k] = mo - v;
+          }
+        }
+      }
+      if (move == kNone && t == 0) {
+        sh.dec_logr = 0.0;
+        sh.flags = 0;
+      }
+      const int first = move != kNone ? wave - 4 : wave, stride = move != kNone ? 4 : kWaves;
+      for (int k = first < 0 ? L : first; k < L; k += stride) {
+        if (k == kl || k == kr) continue;
+        const double R = total(k);
+        if (lane == 63) {
+          double nk;
+          float mo;
+          const double Sk = leaf_stats(k, R, 0.0, nk, mo);
+          const float v = draw_leaf(nk, Sk, td.z[k]);
+          sh.cntd[k] = nk;
+          sh.S[k] = Sk;
+          sh.newv[k] = v;
+          sh.dlt[k] = mo - v;
+        }
       }
       // stage what later trees need
       if (more3 && t < kPropWords) ((uint32_t *)&sh.ctx[(j + 3) & (kRing - 1)].pr)[t] = pw3;
       if (more1) store_tree_data(sh.td[(j + 1) & 1], sh.ctx[(j + 1) & (kRing - 1)], tdn);
       lds_barrier();
-      // 4. residuals and index row (item 11)
+      // 4. residuals and index row (item 11): a point in a child of eta of a
+      //    merged move takes the merged value and the index eta
+      const int flags = sh.flags, acc = flags & 1, merged = (flags >> 1) & 1;
       const bool changed = acc && move != kNone;
+      const float vm = sh.newv_m, dml = sh.dlt_m[0], dmr = sh.dlt_m[1];
       const gptr<ChunkT> row = gbl((ChunkT *)((char *)A->idx + (int64_t)j * A->ldi * IB));
 #pragma unroll
       for (int v = 0; v < V; ++v) {
@@ -610,10 +660,12 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
           const int rnk = (rk[v] >> (8 * b)) & 0xff;
-          const float d = sh.delta[rnk];
+          const bool pair = (rnk == kl) || (rnk == kr);
+          const bool to_eta = merged && pair;
+          const float d = to_eta ? (rnk == kl ? dml : dmr) : sh.dlt[rnk];
           r[v][b] += ((okm[v] >> b) & 1u) ? d : 0.f;
-          touch |= (rnk == kl) || (rnk == kr);
-          out = IC::put(out, b, sh.fin[rnk]);
+          touch |= pair;
+          out = IC::put(out, b, to_eta ? eta : (int)c.heap_of[rnk]);
         }
         if (changed && touch && okm[v]) row[(w * V + v) * kBlock + t] = out;
       }
@@ -622,10 +674,10 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       if (j % G == w) {
         if (t < L) {
           const int h = c.heap_of[t];
-          const bool to_eta = merged && ((h >> 1) == eta);
+          const bool to_eta = merged && (t == kl || t == kr);
           const int f = to_eta ? eta : h;
-          const double nf = to_eta ? sh.dec_n_eta : sh.cntd[t];
-          gbl(A->leaf)[(int64_t)j * 2 * H + f] = sh.newv[t];
+          const double nf = to_eta ? sh.cntd[kl] + sh.cntd[kr] : sh.cntd[t];
+          gbl(A->leaf)[(int64_t)j * 2 * H + f] = to_eta ? vm : sh.newv[t];
           gbl(A->count)[(int64_t)j * 2 * H + f] = (int32_t)nf;
         }
         if (t == 0) {
@@ -683,7 +735,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
         for (int u = 0; u < kWaves; ++u) acc += sh.wave_part[u];
         st_dev(mailbox(A, par, w), mk_word(seq, pack_f64(acc)));
       }
-      gather(A, sh, par, seq, 1, 1);
+      gather_total(A, sh, par, seq, 1);
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       if (t == 0) {
         const double ssr_all = sh.tot[0];
