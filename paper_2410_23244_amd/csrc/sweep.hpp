@@ -38,6 +38,7 @@ namespace bart {
 
 constexpr uint32_t kSpinLimit = 1u << 21;
 constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
+constexpr int kRegLeaves = 8;  // trees with at most this many leaves are reduced in registers
 
 __device__ __forceinline__ uint64_t ld_dev(const uint64_t *p) {
   return __hip_atomic_load(gbl(const_cast<uint64_t *>(p)), __ATOMIC_RELAXED,
@@ -131,6 +132,7 @@ struct Shared {
   Ctx ctx[kRing];
   TreeData td[2];
   double red[kMaxLeaves + 1];  // this workgroup's partial sums of the tree to post next
+  double red_w[kRegLeaves][kWaves];  // the same per wave, for small trees
   double part[kBlock];
   double tot[kMaxLeaves + 1];
   double S[kMaxLeaves];
@@ -435,11 +437,11 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     const Ctx &c = sh.ctx[tree & (kRing - 1)];
     const int move = c.pr.move, eta = c.pr.eta, cutv = c.pr.cut;
     const int grow_eta = move == kGrow ? eta : -1;
+    // leaf of every point in the larger tree, then all rank lookups at once
+    int cp[V][4];
     int nr = 0;
-    uint32_t bad = 0;
 #pragma unroll
-    for (int v = 0; v < V; ++v) {
-      uint32_t pk = 0;
+    for (int v = 0; v < V; ++v)
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         const int ci = IC::get(rawc[v], b);
@@ -447,12 +449,24 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
         const uint32_t ok = (okm[v] >> b) & 1u;
         const int in = ci == grow_eta;
         const int right = xi >= cutv;
-        const int cp = in ? 2 * eta + right : ci;
-        const int r0 = c.rank_of[cp & 255];
-        bad |= ok & (r0 == 0xFF);
-        // padding observations and (invalid) non-leaf indices use rank 0
-        const int rnk = (ok && r0 != 0xFF) ? r0 : 0;
+        cp[v][b] = (in ? 2 * eta + right : ci) & 255;
         nr += __popcll(__ballot(ok && in && right));
+      }
+    int r0[V][4];
+#pragma unroll
+    for (int v = 0; v < V; ++v)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) r0[v][b] = c.rank_of[cp[v][b]];
+    uint32_t bad = 0;
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+      uint32_t pk = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const uint32_t ok = (okm[v] >> b) & 1u;
+        bad |= ok & (r0[v][b] == 0xFF);
+        // padding observations and (invalid) non-leaf indices use rank 0
+        const int rnk = (ok && r0[v][b] != 0xFF) ? r0[v][b] : 0;
         pk |= (uint32_t)rnk << (8 * b);
       }
       out[v] = pk;
@@ -460,10 +474,36 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     if (bad) sh.dev_err = 1;
     if (lane == 0 && nr) atomicAdd(&sh.nr[tree & 1], nr);
   };
-  // partial sums of tree `tree` from the current residuals into sh.red, via
-  // per-lane private bins and a fixed-order fp64 reduction (two barriers)
+  // partial sums of tree `tree` from the current residuals.  Up to kRegLeaves
+  // leaves: per-lane fp32 sums in registers, a fixed-order fp64 DPP sum per
+  // wave into sh.red_w[k][wave] (the poster adds the waves); more leaves:
+  // per-lane private LDS bins and a fixed-order fp64 reduction into sh.red.
+  // Ends with an LDS barrier.
   auto reduce = [&](int tree, const uint32_t (&rks)[V]) {
     const int L = sh.ctx[tree & (kRing - 1)].pr.L;
+    if (L <= kRegLeaves) {
+      float acc[kRegLeaves];
+#pragma unroll
+      for (int k = 0; k < kRegLeaves; ++k) acc[k] = 0.f;
+#pragma unroll
+      for (int v = 0; v < V; ++v)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int rnk = (rks[v] >> (8 * b)) & 0xff;
+          const float add = ((okm[v] >> b) & 1u) ? r[v][b] : 0.f;
+#pragma unroll
+          for (int k = 0; k < kRegLeaves; ++k)
+            if (k < L && rnk == k) acc[k] += add;
+        }
+#pragma unroll
+      for (int k = 0; k < kRegLeaves; ++k)
+        if (k < L) {
+          const double tot = wave_total63((double)acc[k]);
+          if (lane == 63) sh.red_w[k][wave] = tot;
+        }
+      lds_barrier();
+      return;
+    }
     const int setbits = L * kWaves * 64 <= kBinFloats ? 6 : 4;  // 64 or 16 lane sets per wave
     const int setmask = (1 << setbits) - 1;
 #pragma unroll
@@ -499,6 +539,14 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       if (lane == 63) sh.red[k] = tot;
     }
     lds_barrier();
+  };
+  // this workgroup's partial sum of rank k of a tree with L leaves (after reduce)
+  auto partial = [&](int L, int k) {
+    if (L > kRegLeaves) return sh.red[k];
+    double acc = 0.0;
+#pragma unroll
+    for (int u = 0; u < kWaves; ++u) acc += sh.red_w[k][u];
+    return acc;
   };
   // proposals of trees j0.. j0+2 into the ring, rank tables, rows of j0,
   // route of j0, rows of j0+1, decision data of j0, partial sums of j0
@@ -548,14 +596,15 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       const bool more1 = (j + 1 < m) && (step + 1 < Lc.n_steps);  // tree j+1 follows
       const bool more2 = more1 && (j + 2 < m);
       const bool more3 = more2 && (j + 3 < m);
-      // 1. post this workgroup's partial sums of tree j and its GROW right-count
+      // 1. route tree j+1 (its rows were loaded a step ago), then post this
+      //    workgroup's partial sums of tree j and its GROW right-count
+      if (more1) route(j + 1, rk2);
       if (t <= L) {
-        const uint64_t pay = t < L ? pack_f64(sh.red[t]) : (uint64_t)sh.nr[j & 1];
+        const uint64_t pay = t < L ? pack_f64(partial(L, t)) : (uint64_t)sh.nr[j & 1];
         st_dev(mailbox(A, par, w) + t, mk_word(seq, pay));
       }
-      // 2. while the mailboxes fill: route tree j+1, load rows of j+2, the
-      //    decision data of j+1 and the proposal of j+3
-      if (more1) route(j + 1, rk2);
+      // 2. while the mailboxes fill: load rows of j+2, the decision data of
+      //    j+1 and the proposal of j+3
       if (more2) issue_rows(j + 2);
       TdRegs tdn{0, 0.f, 0.0};
       if (more1) tdn = load_tree_data(A, sh.ctx[(j + 1) & (kRing - 1)], j + 1, s);
@@ -653,21 +702,34 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       const bool changed = acc && move != kNone;
       const float vm = sh.newv_m, dml = sh.dlt_m[0], dmr = sh.dlt_m[1];
       const gptr<ChunkT> row = gbl((ChunkT *)((char *)A->idx + (int64_t)j * A->ldi * IB));
+      float dl[V][4];
 #pragma unroll
-      for (int v = 0; v < V; ++v) {
-        bool touch = false;
-        ChunkT out = 0;
+      for (int v = 0; v < V; ++v)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) dl[v][b] = sh.dlt[(rk[v] >> (8 * b)) & 0xff];
+#pragma unroll
+      for (int v = 0; v < V; ++v)
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
           const int rnk = (rk[v] >> (8 * b)) & 0xff;
-          const bool pair = (rnk == kl) || (rnk == kr);
-          const bool to_eta = merged && pair;
-          const float d = to_eta ? (rnk == kl ? dml : dmr) : sh.dlt[rnk];
+          const bool to_eta = merged && ((rnk == kl) || (rnk == kr));
+          const float d = to_eta ? (rnk == kl ? dml : dmr) : dl[v][b];
           r[v][b] += ((okm[v] >> b) & 1u) ? d : 0.f;
-          touch |= pair;
-          out = IC::put(out, b, to_eta ? eta : (int)c.heap_of[rnk]);
         }
-        if (changed && touch && okm[v]) row[(w * V + v) * kBlock + t] = out;
+      if (changed) {
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+          bool touch = false;
+          ChunkT out = 0;
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const int rnk = (rk[v] >> (8 * b)) & 0xff;
+            const bool pair = (rnk == kl) || (rnk == kr);
+            touch |= pair;
+            out = IC::put(out, b, (merged && pair) ? eta : (int)c.heap_of[rnk]);
+          }
+          if (touch && okm[v]) row[(w * V + v) * kBlock + t] = out;
+        }
       }
       // the owner stores the final tree: values and counts of its leaves,
       // structure change, move statistics and the trace record
