@@ -63,6 +63,16 @@ extern "C" {
 #define BART_LAUNCH_COOPERATIVE 0
 #define BART_LAUNCH_ORDINARY 1
 
+/* Where the sweep kernel keeps the residual cache during a launch.
+ *  REGISTERS: in the registers of the workgroups that own the observations,
+ *    read at launch start and written back at launch end (up to about 4.2M
+ *    observations on 256 compute units).
+ *  STREAMED: in HBM, read and written once per tree step (any n).
+ *  AUTO: registers when they fit, else streamed. */
+#define BART_RESID_AUTO 0
+#define BART_RESID_REGISTERS 1
+#define BART_RESID_STREAMED 2
+
 typedef struct bart_handle bart_handle;
 
 /* Model and problem configuration. */
@@ -75,7 +85,7 @@ typedef struct {
   int32_t grid;       /* workgroups of the sweep kernel (one decides, the rest own
                          the observations): 0 = automatic, else in [2, 256] */
   int32_t launch;     /* BART_LAUNCH_COOPERATIVE or BART_LAUNCH_ORDINARY */
-  int32_t reserved;   /* must be 0 */
+  int32_t residency;  /* BART_RESID_AUTO, BART_RESID_REGISTERS or BART_RESID_STREAMED */
   int64_t x_stride;   /* elements between predictor rows of X_b: >= n, multiple of 16 */
   double alpha, beta; /* tree prior P_d = alpha (1+d)^-beta, alpha in [0,1], beta >= 0 */
   double mu_mu;       /* leaf prior mean (sec. 2.1 "Prior over leaf values") */
@@ -125,7 +135,7 @@ typedef struct {
 /* Launch shape chosen by bart_init. */
 typedef struct {
   int32_t grid, block, chunks_per_thread, lds_bytes;
-  int32_t obs_per_thread, max_leaves, launch, pad;
+  int32_t obs_per_thread, max_leaves, launch, residency;
 } bart_launch;
 
 /* Bytes of device workspace bart_init needs for cfg (0 if cfg is invalid). */

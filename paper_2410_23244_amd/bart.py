@@ -28,12 +28,13 @@ class BartError(RuntimeError):
 
 BART_LAUNCH_COOPERATIVE = 0
 BART_LAUNCH_ORDINARY = 1
+BART_RESID_AUTO, BART_RESID_REGISTERS, BART_RESID_STREAMED = 0, 1, 2
 
 
 class Config(C.Structure):
     _fields_ = [("n", C.c_int32), ("p", C.c_int32), ("ntree", C.c_int32),
                 ("max_depth", C.c_int32), ("idx_bytes", C.c_int32), ("grid", C.c_int32),
-                ("launch", C.c_int32), ("reserved", C.c_int32), ("x_stride", C.c_int64),
+                ("launch", C.c_int32), ("residency", C.c_int32), ("x_stride", C.c_int64),
                 ("alpha", C.c_double), ("beta", C.c_double),
                 ("mu_mu", C.c_double), ("sigma_mu", C.c_double), ("nu", C.c_double),
                 ("lam", C.c_double), ("sigma2_init", C.c_double), ("p_grow", C.c_double)]
@@ -48,7 +49,7 @@ class State(C.Structure):
 class LaunchInfo(C.Structure):
     _fields_ = [("grid", C.c_int32), ("block", C.c_int32), ("chunks_per_thread", C.c_int32),
                 ("lds_bytes", C.c_int32), ("obs_per_thread", C.c_int32),
-                ("max_leaves", C.c_int32), ("launch", C.c_int32), ("pad", C.c_int32)]
+                ("max_leaves", C.c_int32), ("launch", C.c_int32), ("residency", C.c_int32)]
 
 
 # bart_trace, 4224 bytes (include/bart.h)
@@ -167,7 +168,7 @@ class Bart:
                  idx_bytes: int = 1, alpha: float = 0.95, beta: float = 2.0,
                  mu_mu: float = 0.0, sigma_mu: float = 1.0, nu: float = 3.0,
                  lam: float = 1.0, sigma2_init: float = 1.0, p_grow: float = 0.5,
-                 grid: int = 0, launch: int = 0, device: str = "cuda"):
+                 grid: int = 0, launch: int = 0, residency: int = 0, device: str = "cuda"):
         import torch
 
         if not torch.cuda.is_available():
@@ -185,7 +186,7 @@ class Bart:
         yn = y_c.cpu().numpy() if hasattr(y_c, "cpu") else np.asarray(y_c)
         self.y = torch.from_numpy(np.ascontiguousarray(yn, dtype=np.float32)).to(self.device)
         self.n_cuts = np.ascontiguousarray(n_cuts, dtype=np.int32)
-        self.cfg = Config(n, p, ntree, max_depth, idx_bytes, grid, launch, 0, self.x_stride,
+        self.cfg = Config(n, p, ntree, max_depth, idx_bytes, grid, launch, residency, self.x_stride,
                           alpha, beta,
                           mu_mu, sigma_mu, nu, lam, sigma2_init, p_grow)
         nbytes = bart_workspace_bytes(self.cfg)
@@ -275,10 +276,10 @@ class Bart:
             pass
 
 
-def from_inputs(inp, grid: int = 0, launch: int = 0) -> Bart:
+def from_inputs(inp, grid: int = 0, launch: int = 0, residency: int = 0) -> Bart:
     """A chain for a generated workload (paper_2410_23244_amd.inputs.Inputs)."""
     h = inp.hyper
     return Bart(inp.X_b, inp.y_c, inp.n_cuts, ntree=inp.m, max_depth=inp.D,
                 idx_bytes=inp.idx_bytes, alpha=h.alpha, beta=h.beta, mu_mu=h.mu_mu,
                 sigma_mu=h.sigma_mu, nu=h.nu, lam=h.lam, sigma2_init=h.sigma2_init,
-                p_grow=h.p_grow, grid=grid, launch=launch)
+                p_grow=h.p_grow, grid=grid, launch=launch, residency=residency)

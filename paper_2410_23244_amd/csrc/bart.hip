@@ -55,7 +55,8 @@ const char *check_config(const bart_config *c) {
   if (c->grid < 0 || c->grid > kMaxGrid) return "grid must be 0 or in [1, 256]";
   if (c->launch != BART_LAUNCH_COOPERATIVE && c->launch != BART_LAUNCH_ORDINARY)
     return "launch must be BART_LAUNCH_COOPERATIVE or BART_LAUNCH_ORDINARY";
-  if (c->reserved != 0) return "reserved must be 0";
+  if (c->residency < BART_RESID_AUTO || c->residency > BART_RESID_STREAMED)
+    return "residency must be BART_RESID_AUTO, BART_RESID_REGISTERS or BART_RESID_STREAMED";
   if (c->x_stride < c->n || c->x_stride % 16) return "x_stride must be >= n and a multiple of 16";
   if (!(c->alpha >= 0.0 && c->alpha <= 1.0)) return "alpha must be in [0, 1]";
   if (!(c->beta >= 0.0 && std::isfinite(c->beta))) return "beta must be finite and >= 0";
@@ -118,6 +119,10 @@ SweepFn sweep_fn(int V, int IB) {
     }
   }
   return nullptr;
+}
+
+SweepFn stream_fn(int IB) {
+  return IB == 1 ? sweep_kernel_stream<1> : sweep_kernel_stream<2>;
 }
 
 // ---------------------------------------------------------------- kernels
@@ -231,7 +236,8 @@ struct bart_handle {
   const uint8_t *X;
   hipStream_t stream;
   int device;
-  int H, p_nz, V, G, lds;
+  int H, p_nz, V, G, lds;  // V: chunks of 4 observations per thread
+  bool streamed;           // residuals streamed from HBM instead of kept in registers
   int64_t chunks;
   int64_t sweep;
   int32_t next;
@@ -273,6 +279,7 @@ SweepArgs make_args(bart_handle *h) {
   A.p_nz = h->p_nz;
   A.G = h->G;
   A.chunks = (int32_t)h->chunks;
+  A.cpt = h->V;
   A.alpha = c.alpha;
   A.beta = c.beta;
   A.mu_mu = c.mu_mu;
@@ -358,24 +365,35 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
   HIP_TRY(hipGetDevice(&device));
   hipDeviceProp_t prop;
   HIP_TRY(hipGetDeviceProperties(&prop, device));
-  // launch shape: workgroup 0 decides, workgroups 1..G-1 own the observations;
-  // fewest chunks of 4 observations per thread with one workgroup per CU
-  int gmax = std::min(prop.multiProcessorCount, kMaxGrid);
+  // launch shape: one workgroup per CU at most, every workgroup owns a slice
+  // of the observations.  Residuals in registers: the fewest chunks of 4
+  // observations per thread (V) that fit; streamed from HBM otherwise.
+  const int gmax = std::min(prop.multiProcessorCount, kMaxGrid);
+  if (cfg->grid > gmax)
+    return fail(BART_ENOTSUP, "grid=%d exceeds the %d compute units", cfg->grid, gmax);
   int V = 0, G = 0;
-  for (int v : kVs) {
-    const int64_t need = (chunks + (int64_t)v * kBlock - 1) / ((int64_t)v * kBlock);
-    const int g = cfg->grid > 0 ? cfg->grid : (int)need;
-    if (need <= g && g <= gmax) {
-      V = v;
-      G = g;
-      break;
+  if (cfg->residency != BART_RESID_STREAMED) {
+    for (int v : kVs) {
+      const int64_t need = (chunks + (int64_t)v * kBlock - 1) / ((int64_t)v * kBlock);
+      const int g = cfg->grid > 0 ? cfg->grid : (int)std::max<int64_t>(need, 1);
+      if (need <= g && g <= gmax) {
+        V = v;
+        G = g;
+        break;
+      }
     }
+    if (!V && cfg->residency == BART_RESID_REGISTERS)
+      return fail(BART_ENOTSUP,
+                  "n=%d needs more than %d workgroups x %d chunks of 4 observations in registers",
+                  cfg->n, gmax, kVs[3]);
   }
-  if (!V)
-    return fail(BART_ENOTSUP,
-                "n=%d needs more than %d workgroups x %d chunks of 4 observations",
-                cfg->n, gmax, kVs[3]);
-  SweepFn fn = sweep_fn(V, cfg->idx_bytes);
+  const bool streamed = !V;
+  int cpt = V;
+  if (streamed) {
+    G = cfg->grid > 0 ? cfg->grid : gmax;
+    cpt = (int)((chunks + (int64_t)G * kBlock - 1) / ((int64_t)G * kBlock));
+  }
+  SweepFn fn = streamed ? stream_fn(cfg->idx_bytes) : sweep_fn(V, cfg->idx_bytes);
   int per_cu = 0;
   HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)fn, kBlock, 0));
   if (per_cu < 1) return fail(BART_ENOTSUP, "sweep kernel does not fit on a compute unit");
@@ -391,7 +409,8 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
   h->device = device;
   h->H = 1 << (cfg->max_depth - 1);
   h->p_nz = (int)nzl.size();
-  h->V = V;
+  h->V = cpt;
+  h->streamed = streamed;
   h->G = G;
   h->lds = (int)fa.sharedSizeBytes;
   h->chunks = chunks;
@@ -539,6 +558,7 @@ int bart_launch_info(const bart_handle *h, bart_launch *o) {
   o->grid = h->G;
   o->block = kBlock;
   o->chunks_per_thread = h->V;
+  o->residency = h->streamed ? BART_RESID_STREAMED : BART_RESID_REGISTERS;
   o->lds_bytes = h->lds;
   o->obs_per_thread = 4 * h->V;
   o->max_leaves = std::min(h->H, kMaxLeaves);

@@ -67,6 +67,8 @@ struct SweepArgs {
   Ctl *ctl;
   uint64_t *pub;     // [2][kMaxGrid][kStride] mailboxes, by step parity
   int32_t n, p, m, D, H, p_nz, G, chunks;
+  int32_t cpt;  // chunks of 4 observations per thread
+  int32_t pad_;
   double alpha, beta, mu_mu, sigma_mu, nu, lambda, p_grow;
 };
 

@@ -39,6 +39,7 @@ namespace bart {
 constexpr uint32_t kSpinLimit = 1u << 21;
 constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
 constexpr int kRegLeaves = 8;  // trees with at most this many leaves are reduced in registers
+constexpr int kBinRanks = kBinFloats / (kWaves * 64);  // ranks per pass of the LDS bins (64)
 
 __device__ __forceinline__ uint64_t ld_dev(const uint64_t *p) {
   return __hip_atomic_load(gbl(const_cast<uint64_t *>(p)), __ATOMIC_RELAXED,
@@ -373,6 +374,198 @@ __device__ __noinline__ void trace_tree_step(bart_trace *R, Shared &sh, const Ct
   if (t < 10) R->pad[t] = 0;
 }
 
+// Decision and leaf draws of one tree from the gathered per-segment partials
+// (sh.part, nseg segments of K = L+1 words), the same in every workgroup.
+// The MH decision (item 9) and every draw (items 4, 5, 10) are computed at
+// once by different waves: the draws do not depend on the decision, only
+// which of them is used.  Waves 0-3 handle the two leaves of the move (the
+// decision, each child's own draw, the merged draw), waves 4-7 the other
+// leaves; each wave sums the segments of the words it needs with the
+// fixed-order DPP tree (nseg <= 32).  Writes sh.flags, dec_logr, and per
+// rank cntd, S, newv, dlt, plus newv_m and dlt_m for a merged move.
+__device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Shared &sh,
+                                            const Ctx &c, const TreeData &td, int nseg) {
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int move = c.pr.move, eta = c.pr.eta, L = c.pr.L;
+  const int kl = c.pr.rank_l, kr = c.pr.rank_r;
+  const int K = L + 1;
+  const double s2 = sh.sigma2, v2 = A->sigma_mu * A->sigma_mu;
+  auto total = [&](int k) {
+    return wave_total63(lane < nseg ? sh.part[lane * K + k] : 0.0);  // valid in lane 63
+  };
+  // count and partial sum S_h = R_h + n_h * (old value) of rank k (sec. 3.3
+  // item 8); nR is the GROW right-count
+  auto leaf_stats = [&](int k, double R, double nR, double &nk, float &mo) {
+    const int h = c.heap_of[k];
+    const bool child = (move == kGrow) && ((h >> 1) == eta);
+    nk = child ? ((h & 1) ? nR : (double)td.eta_cnt - nR) : (double)td.cnt[k];
+    mo = child ? td.eta_mu : td.mu[k];
+    return R + nk * (double)mo;
+  };
+  // conditional draw of a leaf value (items 4, 5, 10)
+  auto draw_leaf = [&](double nf, double Sf, double z) {
+    const double prec = nf / s2 + 1.0 / v2;
+    const double mean = (Sf / s2 + A->mu_mu / v2) / prec;
+    return (float)(mean + z / sqrt(prec));
+  };
+  if (move != kNone && wave < 4) {
+    const double nR = move == kGrow ? total(L) : 0.0;
+    const double Rl = total(kl), Rr = total(kr);
+    if (lane == 63) {
+      double nl, nr;
+      float mol, mor;
+      const double Sl = leaf_stats(kl, Rl, nR, nl, mol);
+      const double Sr = leaf_stats(kr, Rr, nR, nr, mor);
+      if (wave == 0) {
+        const double llr = split_llr(s2, A->mu_mu, v2, nl, Sl, nr, Sr);
+        const double logr = c.pr.c_prior + (move == kGrow ? llr : -llr);
+        const int acc = c.pr.ln_u < logr ? 1 : 0;
+        const int merged = (move == kGrow && !acc) || (move == kPrune && acc);
+        sh.dec_logr = logr;
+        sh.flags = acc | (merged << 1);
+      } else if (wave == 3) {
+        const float vm = draw_leaf(nl + nr, Sl + Sr, td.eta_z);
+        sh.newv_m = vm;
+        sh.dlt_m[0] = mol - vm;
+        sh.dlt_m[1] = mor - vm;
+      } else {
+        const int k = wave == 1 ? kl : kr;
+        const double nk = wave == 1 ? nl : nr, Sk = wave == 1 ? Sl : Sr;
+        const float mo = wave == 1 ? mol : mor;
+        const float v = draw_leaf(nk, Sk, td.z[k]);
+        sh.cntd[k] = nk;
+        sh.S[k] = Sk;
+        sh.newv[k] = v;
+        sh.dlt[k] = mo - v;
+      }
+    }
+  }
+  if (move == kNone && t == 0) {
+    sh.dec_logr = 0.0;
+    sh.flags = 0;
+  }
+  const int first = move != kNone ? wave - 4 : wave, stride = move != kNone ? 4 : kWaves;
+  for (int k = first < 0 ? L : first; k < L; k += stride) {
+    if (k == kl || k == kr) continue;
+    const double R = total(k);
+    if (lane == 63) {
+      double nk;
+      float mo;
+      const double Sk = leaf_stats(k, R, 0.0, nk, mo);
+      const float v = draw_leaf(nk, Sk, td.z[k]);
+      sh.cntd[k] = nk;
+      sh.S[k] = Sk;
+      sh.newv[k] = v;
+      sh.dlt[k] = mo - v;
+    }
+  }
+}
+
+// After the decision of tree j: its owner workgroup (j mod G) stores the
+// final tree (values and counts of its leaves, structure change) and the
+// trace record; workgroup 0 counts the move.
+__device__ __forceinline__ void finish_tree(const SweepArgs *__restrict__ A, const Launch &Lc,
+                                            Shared &sh, const Ctx &c, int j, int64_t s,
+                                            int step) {
+  const int t = threadIdx.x, w = blockIdx.x, G = A->G, H = A->H;
+  const int move = c.pr.move, eta = c.pr.eta, L = c.pr.L;
+  const int kl = c.pr.rank_l, kr = c.pr.rank_r;
+  const int acc = sh.flags & 1, merged = (sh.flags >> 1) & 1;
+  const float vm = sh.newv_m;
+  // the owner stores the final tree: values and counts of its leaves,
+  // structure change, move statistics and the trace record
+  if (j % G == w) {
+    if (t < L) {
+      const int h = c.heap_of[t];
+      const bool to_eta = merged && (t == kl || t == kr);
+      const int f = to_eta ? eta : h;
+      const double nf = to_eta ? sh.cntd[kl] + sh.cntd[kr] : sh.cntd[t];
+      gbl(A->leaf)[(int64_t)j * 2 * H + f] = to_eta ? vm : sh.newv[t];
+      gbl(A->count)[(int64_t)j * 2 * H + f] = (int32_t)nf;
+    }
+    if (t == 0) {
+      const gptr<uint8_t> ct = gbl(A->cut) + (int64_t)j * H;
+      const gptr<uint16_t> ax = gbl(A->axis) + (int64_t)j * H;
+      if (move == kGrow && acc) {
+        ax[eta] = (uint16_t)c.pr.axis;
+        ct[eta] = (uint8_t)c.pr.cut;
+        if (2 * eta < H) ct[2 * eta] = 0;
+        if (2 * eta + 1 < H) ct[2 * eta + 1] = 0;
+      }
+      if (move == kPrune && acc) ct[eta] = 0;
+    }
+    if (Lc.trace) trace_tree_step(Lc.trace + step, sh, c, j, s, H);
+  }
+  if (w == 0 && t == 0) {
+    sh.stats[0] += move == kGrow;
+    sh.stats[1] += move == kPrune;
+    sh.stats[2] += move == kGrow && acc;
+    sh.stats[3] += move == kPrune && acc;
+    sh.stats[4] += 1;
+    sh.stats[5] += (uint64_t)(L - merged);
+  }
+}
+
+// The sigma^2 step after this workgroup's per-wave sums of squared
+// residuals are in sh.wave_part: the next sweep's proposals (owners) and
+// normals, the grid-wide SSR in a fixed order, and the draw, made by every
+// workgroup alike.
+__device__ __forceinline__ void sigma2_tail(const SweepArgs *__restrict__ A, const Launch &Lc,
+                                            Shared &sh, int64_t s, int step, uint32_t seq,
+                                            int par) {
+  const int t = threadIdx.x, w = blockIdx.x, m = A->m;
+  const uint64_t seed = Lc.seed;
+  const bool tracing = Lc.trace != nullptr;
+  // the next sweep's proposals (owners) and normals, published by the
+  // release below together with this sweep's tree writes
+  gen_proposals(A, seed, s + 1, 0);
+  gen_normals(A, seed, s + 1, 0);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (t == 0) {
+    double acc = 0.0;
+    for (int u = 0; u < kWaves; ++u) acc += sh.wave_part[u];
+    st_dev(mailbox(A, par, w), mk_word(seq, pack_f64(acc)));
+  }
+  gather_total(A, sh, par, seq, 1);
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  if (t == 0) {
+    const double ssr_all = sh.tot[0];
+    const double s2 = draw_sigma2(A, seed, s, ssr_all);
+    sh.sigma2 = s2;
+    if (w == 0) {
+      A->ctl->sigma2 = s2;
+      A->ctl->sweep = s + 1;
+      if (tracing) {
+        bart_trace *R = Lc.trace + step;
+        R->kind = 1;
+        R->tree = m;
+        R->sweep = s;
+        R->move = 0;
+        R->ssr = ssr_all;
+        R->sigma2 = s2;
+      }
+    }
+  }
+  if (tracing && w == 0) {
+    // the rest of the sigma^2 record is zero
+    bart_trace *R = Lc.trace + step;
+    if (t < 256) {
+      R->count[t] = 0;
+      R->sum[t] = 0.0;
+      R->leaf_new[t] = 0.f;
+    }
+    if (t >= 1 && t < 10) R->pad[t] = 0;
+    if (t == 1) {
+      R->eta = R->axis = R->cut = R->n_grow_cand = R->n_prune_cand = R->accept = 0;
+      R->n_leaves = 0;
+      R->log_r = R->ln_u = R->log_r_scale = 0.0;
+      R->pad[0] = 0;
+    }
+  }
+  __syncthreads();
+}
+
 template <int V, int IB>
 __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, const Launch &Lc,
                                            Shared &sh) {
@@ -504,41 +697,32 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       lds_barrier();
       return;
     }
-    const int setbits = L * kWaves * 64 <= kBinFloats ? 6 : 4;  // 64 or 16 lane sets per wave
-    const int setmask = (1 << setbits) - 1;
+    // private bins of every lane for up to kBinRanks ranks at a time: a plain
+    // read-modify-write (LDS float atomics serialise across lanes and are
+    // many times slower); larger trees take several passes
+    for (int base = 0; base < L; base += kBinRanks) {
 #pragma unroll
-    for (int v = 0; v < V; ++v)
+      for (int v = 0; v < V; ++v)
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int rnk = (rks[v] >> (8 * b)) & 0xff;
-        // bins are private: a plain read-modify-write (LDS float atomics
-        // serialise across lanes and are many times slower).  With 16 lane
-        // sets, lanes l, l+16, l+32, l+48 share a set and take turns.
-        float &bin = sh.bins[((rnk * kWaves + wave) << setbits) | (lane & setmask)];
-        const float add = ((okm[v] >> b) & 1u) ? r[v][b] : 0.f;
-        if (setbits == 6) {
-          bin += add;
-        } else {
-#pragma unroll
-          for (int g = 0; g < 4; ++g)
-            if ((lane >> 4) == g) bin += add;
+        for (int b = 0; b < 4; ++b) {
+          const int rnk = ((rks[v] >> (8 * b)) & 0xff) - base;
+          if (rnk >= 0 && rnk < kBinRanks && ((okm[v] >> b) & 1u))
+            sh.bins[((rnk * kWaves + wave) << 6) | lane] += r[v][b];
         }
-      }
-    lds_barrier();
-    for (int k = wave; k < L; k += kWaves) {
-      double acc = 0.0;
-      if (lane <= setmask) {
+      lds_barrier();
+      for (int k = base + wave; k < min(L, base + kBinRanks); k += kWaves) {
+        double acc = 0.0;
 #pragma unroll
         for (int u = 0; u < kWaves; ++u) {
-          const int q = ((k * kWaves + u) << setbits) | lane;
+          const int q = (((k - base) * kWaves + u) << 6) | lane;
           acc += (double)sh.bins[q];
           sh.bins[q] = 0.f;
         }
+        const double tot = wave_total63(acc);
+        if (lane == 63) sh.red[k] = tot;
       }
-      const double tot = wave_total63(acc);
-      if (lane == 63) sh.red[k] = tot;
+      lds_barrier();
     }
-    lds_barrier();
   };
   // this workgroup's partial sum of rank k of a tree with L leaves (after reduce)
   auto partial = [&](int L, int k) {
@@ -616,82 +800,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       //    segments with the fixed-order DPP tree (nseg <= 32 lanes)
       const int K = L + 1;
       const int nseg = gather_polls(A, sh, par, seq, K, L);
-      const double s2 = sh.sigma2, v2 = A->sigma_mu * A->sigma_mu;
-      const TreeData &td = sh.td[j & 1];
-      auto total = [&](int k) {
-        return wave_total63(lane < nseg ? sh.part[lane * K + k] : 0.0);  // valid in lane 63
-      };
-      // count and partial sum S_h = R_h + n_h * (old value) of rank k (sec. 3.3
-      // item 8); nR is the GROW right-count
-      auto leaf_stats = [&](int k, double R, double nR, double &nk, float &mo) {
-        const int h = c.heap_of[k];
-        const bool child = (move == kGrow) && ((h >> 1) == eta);
-        nk = child ? ((h & 1) ? nR : (double)td.eta_cnt - nR) : (double)td.cnt[k];
-        mo = child ? td.eta_mu : td.mu[k];
-        return R + nk * (double)mo;
-      };
-      // conditional draw of a leaf value (items 4, 5, 10)
-      auto draw_leaf = [&](double nf, double Sf, double z) {
-        const double prec = nf / s2 + 1.0 / v2;
-        const double mean = (Sf / s2 + A->mu_mu / v2) / prec;
-        return (float)(mean + z / sqrt(prec));
-      };
-      // The decision (item 9) and every draw are computed at once by
-      // different waves: the draws do not depend on the decision, only which
-      // of them is used.  Waves 0-3 handle the two leaves of the move
-      // (decision, each child's own draw, the merged draw), waves 4-7 the
-      // other leaves.
-      if (move != kNone && wave < 4) {
-        const double nR = move == kGrow ? total(L) : 0.0;
-        const double Rl = total(kl), Rr = total(kr);
-        if (lane == 63) {
-          double nl, nr;
-          float mol, mor;
-          const double Sl = leaf_stats(kl, Rl, nR, nl, mol);
-          const double Sr = leaf_stats(kr, Rr, nR, nr, mor);
-          if (wave == 0) {
-            const double llr = split_llr(s2, A->mu_mu, v2, nl, Sl, nr, Sr);
-            const double logr = c.pr.c_prior + (move == kGrow ? llr : -llr);
-            const int acc = c.pr.ln_u < logr ? 1 : 0;
-            const int merged = (move == kGrow && !acc) || (move == kPrune && acc);
-            sh.dec_logr = logr;
-            sh.flags = acc | (merged << 1);
-          } else if (wave == 3) {
-            const float vm = draw_leaf(nl + nr, Sl + Sr, td.eta_z);
-            sh.newv_m = vm;
-            sh.dlt_m[0] = mol - vm;
-            sh.dlt_m[1] = mor - vm;
-          } else {
-            const int k = wave == 1 ? kl : kr;
-            const double nk = wave == 1 ? nl : nr, Sk = wave == 1 ? Sl : Sr;
-            const float mo = wave == 1 ? mol : mor;
-            const float v = draw_leaf(nk, Sk, td.z[k]);
-            sh.cntd[k] = nk;
-            sh.S[k] = Sk;
-            sh.newv[k] = v;
-            sh.dlt[k] = mo - v;
-          }
-        }
-      }
-      if (move == kNone && t == 0) {
-        sh.dec_logr = 0.0;
-        sh.flags = 0;
-      }
-      const int first = move != kNone ? wave - 4 : wave, stride = move != kNone ? 4 : kWaves;
-      for (int k = first < 0 ? L : first; k < L; k += stride) {
-        if (k == kl || k == kr) continue;
-        const double R = total(k);
-        if (lane == 63) {
-          double nk;
-          float mo;
-          const double Sk = leaf_stats(k, R, 0.0, nk, mo);
-          const float v = draw_leaf(nk, Sk, td.z[k]);
-          sh.cntd[k] = nk;
-          sh.S[k] = Sk;
-          sh.newv[k] = v;
-          sh.dlt[k] = mo - v;
-        }
-      }
+      decide_step(A, sh, c, sh.td[j & 1], nseg);
       // stage what later trees need
       if (more3 && t < kPropWords) ((uint32_t *)&sh.ctx[(j + 3) & (kRing - 1)].pr)[t] = pw3;
       if (more1) store_tree_data(sh.td[(j + 1) & 1], sh.ctx[(j + 1) & (kRing - 1)], tdn);
@@ -731,38 +840,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
           if (touch && okm[v]) row[(w * V + v) * kBlock + t] = out;
         }
       }
-      // the owner stores the final tree: values and counts of its leaves,
-      // structure change, move statistics and the trace record
-      if (j % G == w) {
-        if (t < L) {
-          const int h = c.heap_of[t];
-          const bool to_eta = merged && (t == kl || t == kr);
-          const int f = to_eta ? eta : h;
-          const double nf = to_eta ? sh.cntd[kl] + sh.cntd[kr] : sh.cntd[t];
-          gbl(A->leaf)[(int64_t)j * 2 * H + f] = to_eta ? vm : sh.newv[t];
-          gbl(A->count)[(int64_t)j * 2 * H + f] = (int32_t)nf;
-        }
-        if (t == 0) {
-          const gptr<uint8_t> ct = gbl(A->cut) + (int64_t)j * H;
-          const gptr<uint16_t> ax = gbl(A->axis) + (int64_t)j * H;
-          if (move == kGrow && acc) {
-            ax[eta] = (uint16_t)c.pr.axis;
-            ct[eta] = (uint8_t)c.pr.cut;
-            if (2 * eta < H) ct[2 * eta] = 0;
-            if (2 * eta + 1 < H) ct[2 * eta + 1] = 0;
-          }
-          if (move == kPrune && acc) ct[eta] = 0;
-        }
-        if (tracing) trace_tree_step(Lc.trace + step, sh, c, j, s, H);
-      }
-      if (w == 0 && t == 0) {
-        sh.stats[0] += move == kGrow;
-        sh.stats[1] += move == kPrune;
-        sh.stats[2] += move == kGrow && acc;
-        sh.stats[3] += move == kPrune && acc;
-        sh.stats[4] += 1;
-        sh.stats[5] += (uint64_t)(L - merged);
-      }
+      finish_tree(A, Lc, sh, c, j, s, step);
       // 5. tree j+1: rank table of j+3, partial sums from the updated residuals
       if (more3) build_ranks(A, sh.ctx[(j + 3) & (kRing - 1)]);
       if (more1) {
@@ -786,54 +864,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
         }
       ssr = wave_total63(ssr);
       if (lane == 63) sh.wave_part[wave] = ssr;
-      // the next sweep's proposals (owners) and normals, published by the
-      // release below together with this sweep's tree writes
-      gen_proposals(A, seed, s + 1, 0);
-      gen_normals(A, seed, s + 1, 0);
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-      __syncthreads();
-      if (t == 0) {
-        double acc = 0.0;
-        for (int u = 0; u < kWaves; ++u) acc += sh.wave_part[u];
-        st_dev(mailbox(A, par, w), mk_word(seq, pack_f64(acc)));
-      }
-      gather_total(A, sh, par, seq, 1);
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-      if (t == 0) {
-        const double ssr_all = sh.tot[0];
-        const double s2 = draw_sigma2(A, seed, s, ssr_all);
-        sh.sigma2 = s2;
-        if (w == 0) {
-          A->ctl->sigma2 = s2;
-          A->ctl->sweep = s + 1;
-          if (tracing) {
-            bart_trace *R = Lc.trace + step;
-            R->kind = 1;
-            R->tree = m;
-            R->sweep = s;
-            R->move = 0;
-            R->ssr = ssr_all;
-            R->sigma2 = s2;
-          }
-        }
-      }
-      if (tracing && w == 0) {
-        // the rest of the sigma^2 record is zero
-        bart_trace *R = Lc.trace + step;
-        if (t < 256) {
-          R->count[t] = 0;
-          R->sum[t] = 0.0;
-          R->leaf_new[t] = 0.f;
-        }
-        if (t >= 1 && t < 10) R->pad[t] = 0;
-        if (t == 1) {
-          R->eta = R->axis = R->cut = R->n_grow_cand = R->n_prune_cand = R->accept = 0;
-          R->n_leaves = 0;
-          R->log_r = R->ln_u = R->log_r_scale = 0.0;
-          R->pad[0] = 0;
-        }
-      }
-      __syncthreads();
+      sigma2_tail(A, Lc, sh, s, step, seq, par);
       j = 0;
       ++s;
       if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s);
@@ -861,6 +892,287 @@ template <int V, int IB>
 __global__ void __launch_bounds__(kBlock) sweep_kernel(const SweepArgs *__restrict__ A, Launch Lc) {
   __shared__ Shared sh;
   sweep_body<V, IB>(A, Lc, sh);
+}
+
+// ------------------------------------------------------------------ streamed
+// Residual cache in HBM (sec. 3.3 "Residuals cache"), for problems whose
+// residuals do not fit in the registers of the grid.  The step structure and
+// the grid protocol are those of sweep_body; the difference is the data
+// pass: per tree step j one pass over this workgroup's points reads each
+// residual once, adds tree j's delta (its route recomputed from the index
+// row and predictor row), writes it back, rewrites the index row where the
+// tree changed, and accumulates tree j+1's partial sums from the updated
+// value (route of j+1 from its rows).  Partial sums are fp64 per lane.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int IB>
+__device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ A, const Launch &Lc,
+                                                  Shared &sh) {
+  using IC = IdxChunk<IB>;
+  using ChunkT = typename IC::T;
+  constexpr int U = 4;  // chunks of 4 points in flight per thread
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, w = blockIdx.x;
+  const int m = A->m, cpt = A->cpt;
+  const uint64_t seed = Lc.seed;
+  for (int k = t; k < kBinFloats; k += kBlock) sh.bins[k] = 0.f;
+  if (t == 0) {
+    sh.abort_flag = 0;
+    sh.dev_err = 0;
+    sh.nr[0] = sh.nr[1] = 0;
+    sh.sigma2 = A->ctl->sigma2;
+  }
+  if (t < 6) sh.stats[t] = 0;
+
+  // leaf ranks in tree c's larger tree of the 4 points of a chunk (0 for
+  // padding); GROW right-count into nr
+  auto ranks4 = [&](const Ctx &c, ChunkT rc, uint32_t rx, uint32_t ok, int &nr,
+                    uint32_t &bad) -> uint32_t {
+    const int move = c.pr.move, eta = c.pr.eta, cutv = c.pr.cut;
+    const int grow_eta = move == kGrow ? eta : -1;
+    uint32_t pk = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int ci = IC::get(rc, b);
+      const int xi = (rx >> (8 * b)) & 0xff;
+      const uint32_t okb = (ok >> b) & 1u;
+      const int in = ci == grow_eta;
+      const int right = xi >= cutv;
+      const int r0 = c.rank_of[(in ? 2 * eta + right : ci) & 255];
+      nr += __popcll(__ballot(okb && in && right));
+      bad |= okb & (r0 == 0xFF);
+      pk |= (uint32_t)((okb && r0 != 0xFF) ? r0 : 0) << (8 * b);
+    }
+    return pk;
+  };
+
+  // one pass: apply tree ja (-1: none), accumulate tree jn (-1: none) into
+  // sh.red_w (<= kRegLeaves leaves; fp64 per lane) or, for ranks in
+  // [lo, lo + kBinRanks), into sh.red (private fp32 bins per lane), sum of
+  // squares into sh.wave_part if want_ssr.  Ends with an LDS barrier.
+  auto pass = [&](int ja, int jn, bool want_ssr, int lo) {
+    const Ctx &ca = sh.ctx[(ja < 0 ? 0 : ja) & (kRing - 1)];
+    const Ctx &cn = sh.ctx[(jn < 0 ? 0 : jn) & (kRing - 1)];
+    const bool do_a = ja >= 0, do_n = jn >= 0;
+    const int flags = sh.flags, acc = flags & 1, merged = (flags >> 1) & 1;
+    const int kl = ca.pr.rank_l, kr = ca.pr.rank_r, eta_a = ca.pr.eta;
+    const bool changed = do_a && acc && ca.pr.move != kNone;
+    const float dml = sh.dlt_m[0], dmr = sh.dlt_m[1];
+    const bool xa = do_a && ca.pr.move == kGrow, xn = do_n && cn.pr.move == kGrow;
+    const int Ln = do_n ? cn.pr.L : 0;
+    const bool regs = Ln <= kRegLeaves;
+    const gptr<ChunkT> rowa =
+        gbl((ChunkT *)((char *)A->idx + (int64_t)(do_a ? ja : 0) * A->ldi * IB));
+    const gptr<const ChunkT> rown =
+        gbl((const ChunkT *)((const char *)A->idx + (int64_t)(do_n ? jn : 0) * A->ldi * IB));
+    const gptr<const uint32_t> xra = gbl((const uint32_t *)(A->X + (int64_t)ca.pr.axis * A->ldx));
+    const gptr<const uint32_t> xrn = gbl((const uint32_t *)(A->X + (int64_t)cn.pr.axis * A->ldx));
+    const gptr<f32x4> res = gbl((f32x4 *)A->resid);
+    double accd[kRegLeaves];
+#pragma unroll
+    for (int k = 0; k < kRegLeaves; ++k) accd[k] = 0.0;
+    double ssr = 0.0;
+    int nr = 0;
+    uint32_t bad = 0;
+#pragma unroll 1
+    for (int i0 = 0; i0 < cpt; i0 += U) {
+      int32_t ch[U];
+      uint32_t ok[U];
+      f32x4 rv[U];
+      ChunkT ra[U], rn[U];
+      uint32_t xa4[U], xn4[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        ch[u] = (w * cpt + i0 + u) * kBlock + t;
+        ok[u] = 0;
+        if (i0 + u < cpt && ch[u] < A->chunks) {
+          const int32_t rem = A->n - 4 * ch[u];
+          ok[u] = rem >= 4 ? 15u : ((1u << rem) - 1u);
+        }
+        rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+        ra[u] = rn[u] = 0;
+        xa4[u] = xn4[u] = 0;
+        if (ok[u]) {
+          rv[u] = res[ch[u]];
+          if (do_a) ra[u] = rowa[ch[u]];
+          if (xa) xa4[u] = xra[ch[u]];
+          if (do_n) rn[u] = rown[ch[u]];
+          if (xn) xn4[u] = xrn[ch[u]];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        int nra = 0;
+        if (do_a) {
+          const uint32_t rk = ranks4(ca, ra[u], xa4[u], ok[u], nra, bad);
+          float dl[4];
+#pragma unroll
+          for (int b = 0; b < 4; ++b) dl[b] = sh.dlt[(rk >> (8 * b)) & 0xff];
+          bool touch = false;
+          ChunkT out = 0;
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const int rnk = (rk >> (8 * b)) & 0xff;
+            const bool pair = (rnk == kl) || (rnk == kr);
+            const float d = (merged && pair) ? (rnk == kl ? dml : dmr) : dl[b];
+            rv[u][b] += ((ok[u] >> b) & 1u) ? d : 0.f;
+            touch |= pair;
+            if (changed) out = IC::put(out, b, (merged && pair) ? eta_a : (int)ca.heap_of[rnk]);
+          }
+          if (ok[u]) res[ch[u]] = rv[u];
+          if (changed && touch && ok[u]) rowa[ch[u]] = out;
+        }
+        if (want_ssr) {
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const double x = ((ok[u] >> b) & 1u) ? (double)rv[u][b] : 0.0;
+            ssr += x * x;
+          }
+        }
+        if (do_n) {
+          const uint32_t rk = ranks4(cn, rn[u], xn4[u], ok[u], nr, bad);
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const int rnk = (rk >> (8 * b)) & 0xff;
+            const double add = ((ok[u] >> b) & 1u) ? (double)rv[u][b] : 0.0;
+            if (regs) {
+#pragma unroll
+              for (int k = 0; k < kRegLeaves; ++k)
+                if (k < Ln && rnk == k) accd[k] += add;
+            } else if (rnk >= lo && rnk < lo + kBinRanks && ((ok[u] >> b) & 1u)) {
+              sh.bins[(((rnk - lo) * kWaves + wave) << 6) | lane] += rv[u][b];
+            }
+          }
+        }
+      }
+    }
+    if (bad) sh.dev_err = 1;
+    if (do_n && lo == 0 && lane == 0 && nr) atomicAdd(&sh.nr[jn & 1], nr);
+    if (want_ssr) {
+      const double tot = wave_total63(ssr);
+      if (lane == 63) sh.wave_part[wave] = tot;
+    }
+    if (do_n && regs) {
+#pragma unroll
+      for (int k = 0; k < kRegLeaves; ++k)
+        if (k < Ln) {
+          const double tot = wave_total63(accd[k]);
+          if (lane == 63) sh.red_w[k][wave] = tot;
+        }
+    }
+    lds_barrier();
+    if (do_n && !regs) {
+      for (int k = lo + wave; k < min(Ln, lo + kBinRanks); k += kWaves) {
+        double a = 0.0;
+#pragma unroll
+        for (int u = 0; u < kWaves; ++u) {
+          const int q = (((k - lo) * kWaves + u) << 6) | lane;
+          a += (double)sh.bins[q];
+          sh.bins[q] = 0.f;
+        }
+        const double tot = wave_total63(a);
+        if (lane == 63) sh.red[k] = tot;
+      }
+      lds_barrier();
+    }
+  };
+  // all partial sums of tree jn: trees with more leaves than one bin pass
+  // holds take extra accumulate-only passes over the data
+  auto pass_all = [&](int ja, int jn, bool want_ssr) {
+    pass(ja, jn, want_ssr, 0);
+    const int Ln = jn >= 0 ? sh.ctx[jn & (kRing - 1)].pr.L : 0;
+    if (Ln > kRegLeaves)
+      for (int lo = kBinRanks; lo < Ln; lo += kBinRanks) pass(-1, jn, false, lo);
+  };
+  auto partial = [&](int L, int k) {
+    if (L > kRegLeaves) return sh.red[k];
+    double a = 0.0;
+#pragma unroll
+    for (int u = 0; u < kWaves; ++u) a += sh.red_w[k][u];
+    return a;
+  };
+  // proposals of trees j0..j0+2, their rank tables, the decision data of j0
+  // and tree j0's partial sums
+  auto refill = [&](int j0, int64_t s) {
+    for (int q = 0; q < 3; ++q)
+      if (j0 + q < m) {
+        const uint32_t wd = load_prop_word(A, j0 + q);
+        if (t < kPropWords) ((uint32_t *)&sh.ctx[(j0 + q) & (kRing - 1)].pr)[t] = wd;
+      }
+    lds_barrier();
+    for (int q = 0; q < 3; ++q)
+      if (j0 + q < m) build_ranks(A, sh.ctx[(j0 + q) & (kRing - 1)]);
+    lds_barrier();
+    const TdRegs tr0 = load_tree_data(A, sh.ctx[j0 & (kRing - 1)], j0, s);
+    store_tree_data(sh.td[j0 & 1], sh.ctx[j0 & (kRing - 1)], tr0);
+    pass_all(-1, j0, false);
+  };
+
+  // ---- prologue
+  int64_t s = Lc.s0;
+  int j = Lc.j0;
+  if (j < m) {
+    gen_proposals(A, seed, s, j);
+    gen_normals(A, seed, s, j);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (t == 0) st_dev(mailbox(A, 1, w), mk_word(1, 0));
+  gather_total(A, sh, 1, 1, 0);
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  __syncthreads();
+  if (j < m && !sh.abort_flag) refill(j, s);
+  bool have_ssr = false;
+
+#pragma unroll 1
+  for (int step = 0; step < Lc.n_steps; ++step) {
+    if (sh.abort_flag) break;
+    const uint32_t seq = (uint32_t)step + 2;
+    const int par = step & 1;
+    if (j < m) {
+      Ctx &c = sh.ctx[j & (kRing - 1)];
+      const int L = c.pr.L;
+      const bool more1 = (j + 1 < m) && (step + 1 < Lc.n_steps);
+      const bool more3 = more1 && (j + 3 < m);
+      if (t <= L) {
+        const uint64_t pay = t < L ? pack_f64(partial(L, t)) : (uint64_t)sh.nr[j & 1];
+        st_dev(mailbox(A, par, w) + t, mk_word(seq, pay));
+      }
+      TdRegs tdn{0, 0.f, 0.0};
+      if (more1) tdn = load_tree_data(A, sh.ctx[(j + 1) & (kRing - 1)], j + 1, s);
+      const uint32_t pw3 = more3 ? load_prop_word(A, j + 3) : 0u;
+      lds_barrier();
+      if (t == L) sh.nr[j & 1] = 0;
+      const int nseg = gather_polls(A, sh, par, seq, L + 1, L);
+      decide_step(A, sh, c, sh.td[j & 1], nseg);
+      if (more3 && t < kPropWords) ((uint32_t *)&sh.ctx[(j + 3) & (kRing - 1)].pr)[t] = pw3;
+      if (more1) store_tree_data(sh.td[(j + 1) & 1], sh.ctx[(j + 1) & (kRing - 1)], tdn);
+      lds_barrier();
+      finish_tree(A, Lc, sh, c, j, s, step);
+      if (more3) build_ranks(A, sh.ctx[(j + 3) & (kRing - 1)]);
+      have_ssr = j == m - 1;
+      pass_all(j, more1 ? j + 1 : -1, have_ssr);
+      ++j;
+    } else {
+      __syncthreads();
+      if (!have_ssr) pass(-1, -1, true, 0);
+      have_ssr = false;
+      sigma2_tail(A, Lc, sh, s, step, seq, par);
+      j = 0;
+      ++s;
+      if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s);
+    }
+  }
+  if (w == 0 && t < 6) A->ctl->stats[t] += sh.stats[t];
+  if (t == 0 && (sh.abort_flag || sh.dev_err))
+    atomicOr(&A->ctl->error, (sh.abort_flag ? BART_DEVERR_TIMEOUT : 0u) |
+                                 (sh.dev_err ? BART_DEVERR_CACHE : 0u));
+}
+
+template <int IB>
+__global__ void __launch_bounds__(kBlock) sweep_kernel_stream(const SweepArgs *__restrict__ A,
+                                                              Launch Lc) {
+  __shared__ Shared sh;
+  sweep_body_stream<IB>(A, Lc, sh);
 }
 
 }  // namespace bart

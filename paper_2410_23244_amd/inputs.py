@@ -24,6 +24,7 @@ matrix whole.
 from __future__ import annotations
 
 import math
+import os
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -140,15 +141,26 @@ def make_inputs(config: int, n: int | None = None, p: int | None = None,
     idx_bytes = int(idx_bytes if idx_bytes is not None else w["idx_bytes"])
     needed = 5 if w["gen"] == "sin5" else 12
     X_b = np.empty((p, n), np.uint8)
-    n_cuts = np.empty(p, np.int32)
+    n_cuts = np.full(p, w["K"], np.int32)
     cols = {}
-    for a in range(p):
+
+    def one(a: int) -> None:
+        # each column is generated, cut and binned on its own (numpy releases
+        # the GIL in the heavy calls, so columns run in parallel threads)
         x = column(config, a, n)
         if a < needed:
             cols[a] = x
-        cuts = cutpoints(x, w["K"], w["grid"])
-        X_b[a] = bin_column(x, cuts)
-        n_cuts[a] = w["K"]
+        X_b[a] = bin_column(x, cutpoints(x, w["K"], w["grid"]))
+
+    threads = min(16, os.cpu_count() or 1, max(p, 1))
+    if threads > 1 and n * p >= 1 << 22:
+        from concurrent.futures import ThreadPoolExecutor
+
+        with ThreadPoolExecutor(threads) as ex:
+            list(ex.map(one, range(p)))
+    else:
+        for a in range(p):
+            one(a)
     for a in range(p, needed):  # informative columns beyond p (tiny test shapes)
         cols[a] = column(config, a, n)
     f = _response(w["gen"], cols, n)

@@ -15,16 +15,17 @@ pytestmark = pytest.mark.gpu
 
 
 COOP, ORDINARY = 0, 1  # BART_LAUNCH_COOPERATIVE, BART_LAUNCH_ORDINARY
+AUTO, REGS, STREAM = 0, 1, 2  # BART_RESID_AUTO, BART_RESID_REGISTERS, BART_RESID_STREAMED
 
 
-def _gpu(inp, grid=0, launch=COOP):
+def _gpu(inp, grid=0, launch=COOP, residency=AUTO):
     from paper_2410_23244_amd.bart import from_inputs
 
-    return from_inputs(inp, grid=grid, launch=launch)
+    return from_inputs(inp, grid=grid, launch=launch, residency=residency)
 
 
 CASES = {
-    # name: (config, overrides, warm sweeps, lockstep steps, grid, launch)
+    # name: (config, overrides, warm sweeps, lockstep steps, grid, launch[, residency])
     "w1_full": (1, dict(), 3, 2 * 51, 0, COOP),
     "w1_ragged_tiny": (1, dict(n=37, p=3, m=5), 2, 3 * 6, 0, COOP),
     "w2_ragged": (2, dict(n=20011, m=60), 2, 61 + 30, 0, COOP),
@@ -32,17 +33,26 @@ CASES = {
     "w2_idle_wg": (2, dict(n=20011, p=30, m=30), 2, 31 * 2, 8, COOP),
     "w4_u16": (4, dict(n=30001, p=20, m=50), 2, 51 + 10, 0, COOP),
     "w5_depth8": (5, dict(n=25003, p=1000, m=120), 2, 121 + 5, 0, COOP),
+    # residuals streamed from HBM: ragged chunks per thread, u16 cache, depth 8
+    "w2_stream": (2, dict(n=40003, p=30, m=40), 2, 41 * 2, 4, ORDINARY, STREAM),
+    "w1_stream_tiny": (1, dict(n=37, p=3, m=5), 2, 3 * 6, 0, COOP, STREAM),
+    "w4_stream_u16": (4, dict(n=70001, p=20, m=50), 2, 51 + 10, 0, COOP, STREAM),
+    "w5_stream_depth8": (5, dict(n=25003, p=1000, m=120), 2, 121 + 5, 3, COOP, STREAM),
 }
 
 
 @pytest.mark.parametrize("name", list(CASES))
 def test_lockstep_small(name):
-    cfg, over, warm, steps, grid, launch = CASES[name]
+    cfg, over, warm, steps, grid, launch, *rest = CASES[name]
+    residency = rest[0] if rest else AUTO
     inp = make_inputs(cfg, **over)
     print(f"case {name}: n={inp.n} p={inp.p} m={inp.m} D={inp.D} idx={inp.idx_bytes}", flush=True)
-    g = _gpu(inp, grid, launch)
+    g = _gpu(inp, grid, launch, residency)
     info = g.launch_info()
-    print(f"  grid={info.grid} chunks/thread={info.chunks_per_thread}", flush=True)
+    print(f"  grid={info.grid} chunks/thread={info.chunks_per_thread} "
+          f"residency={info.residency}", flush=True)
+    if residency == STREAM:
+        assert info.residency == STREAM
     rep = parity.lockstep(inp, g, seed=inp.seed + 100, warm_sweeps=warm, n_steps=steps)
     print(f"  {rep}", flush=True)
     assert rep.tree_steps > 0 and rep.moves > 0
@@ -103,7 +113,7 @@ def test_launch_modes_agree():
     assert sa["sigma2"] == sb["sigma2"]
 
 
-@pytest.mark.parametrize("cfg", [2, 3])
+@pytest.mark.parametrize("cfg", [2, 3, 5])
 def test_lockstep_full_size(cfg):
     """Full size, in the launch mode the benchmark times, after the benchmark's
     warm-up length (trees near their stationary size)."""
@@ -111,4 +121,72 @@ def test_lockstep_full_size(cfg):
     print(f"full workload {cfg}: n={inp.n} p={inp.p} m={inp.m}", flush=True)
     g = _gpu(inp, launch=ORDINARY)
     rep = parity.lockstep(inp, g, seed=inp.seed, warm_sweeps=100, n_steps=inp.m + 1)
+    print(f"  {rep}", flush=True)
+
+
+def _full_trees(inp, depth, rng):
+    """A state whose trees are all complete to `depth` (2**depth leaves), with
+    random axes, cuts and leaf values, the index cache routed by brute force
+    and residuals y_c - sum of trees."""
+    m, H, n, p = inp.m, 1 << (inp.D - 1), inp.n, inp.p
+    axis = np.zeros((m, H), np.uint16)
+    cut = np.zeros((m, H), np.uint8)
+    leaf = np.zeros((m, 2 * H), np.float32)
+    idx = np.zeros((m, n), np.uint8 if inp.idx_bytes == 1 else np.uint16)
+    f = np.zeros(n)
+    for j in range(m):
+        for h in range(1, 1 << depth):
+            # region of h: the ancestors' rules bound each axis to [lo, hi]
+            lo, hi = np.zeros(p, np.int64), inp.n_cuts.astype(np.int64).copy()
+            q = h
+            while q > 1:
+                par_, right = q >> 1, q & 1
+                a_ = axis[j, par_]
+                if right:
+                    lo[a_] = max(lo[a_], int(cut[j, par_]))
+                else:
+                    hi[a_] = min(hi[a_], int(cut[j, par_]) - 1)
+                q = par_
+            ok = np.flatnonzero(hi > lo)
+            a = int(ok[rng.integers(ok.size)])
+            axis[j, h] = a
+            cut[j, h] = int(rng.integers(lo[a] + 1, hi[a] + 1))
+        leaf[j, 1 << depth:2 << depth] = rng.normal(0.0, inp.hyper.sigma_mu, 1 << depth)
+        hh = np.ones(n, np.int64)
+        for _ in range(depth):
+            a = axis[j, hh]
+            right = inp.X_b[a, np.arange(n)] >= cut[j, hh]
+            hh = 2 * hh + right
+        idx[j] = hh
+        f += leaf[j, hh].astype(np.float64)
+    resid = (inp.y_c.astype(np.float64) - f).astype(np.float32)
+    return dict(axis=axis, cut=cut, leaf=leaf, idx=idx, resid=resid,
+                sigma2=inp.hyper.sigma2_init, sweep=0, next=0)
+
+
+@pytest.mark.parametrize("residency", [REGS, STREAM])
+@pytest.mark.parametrize("shape", ["d6_32_leaves", "d8_128_leaves"])
+def test_lockstep_big_trees(shape, residency):
+    """Trees far larger than the sampler grows by itself: 32 and 128 leaves
+    take the LDS-bin reductions and mailboxes of up to 129 words."""
+    if shape == "d6_32_leaves":
+        inp, depth = make_inputs(2, n=20011, p=12, m=12), 5
+    else:
+        inp, depth = make_inputs(5, n=30011, p=40, m=6), 7
+    g = _gpu(inp, residency=residency)
+    print(f"{shape}: grid={g.launch_info().grid} residency={g.launch_info().residency}",
+          flush=True)
+    g.set_state(_full_trees(inp, depth, np.random.default_rng(7)))
+    rep = parity.lockstep(inp, g, seed=5, warm_sweeps=0, n_steps=2 * (inp.m + 1))
+    print(f"  {rep}", flush=True)
+    assert rep.moves > 0
+
+
+def test_lockstep_full_size_streamed():
+    """Workload 4 (n = 1e7, u16 index cache): residuals streamed from HBM."""
+    inp = make_inputs(4)
+    print(f"full workload 4: n={inp.n} p={inp.p} m={inp.m}", flush=True)
+    g = _gpu(inp, launch=ORDINARY)
+    assert g.launch_info().residency == STREAM
+    rep = parity.lockstep(inp, g, seed=inp.seed, warm_sweeps=20, n_steps=inp.m + 1)
     print(f"  {rep}", flush=True)

@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(b):
 
 def _cfg(b, **kw):
     base = dict(n=1000, p=4, ntree=10, max_depth=6, idx_bytes=1, grid=0, launch=0,
-                reserved=0, x_stride=1024,
+                residency=0, x_stride=1024,
                 alpha=0.95, beta=2.0, mu_mu=0.0, sigma_mu=0.1, nu=3.0, lam=0.5,
                 sigma2_init=1.0, p_grow=0.5)
     base.update(kw)
@@ -50,7 +50,8 @@ def _cfg(b, **kw):
                                  dict(idx_bytes=3), dict(x_stride=1000), dict(x_stride=512),
                                  dict(alpha=1.5), dict(sigma_mu=0.0), dict(nu=-1.0),
                                  dict(p_grow=2.0), dict(grid=300), dict(grid=-1), dict(lam=float("nan")),
-                                 dict(launch=2), dict(launch=-1), dict(reserved=1)])
+                                 dict(launch=2), dict(launch=-1), dict(residency=3),
+                                 dict(residency=-1)])
 def test_invalid_configs_are_rejected(b, bad):
     cfg = _cfg(b, **bad)
     assert b.bart_workspace_bytes(cfg) == 0
