@@ -102,24 +102,18 @@ Layout make_layout(const bart_config &c) {
 using SweepFn = void (*)(const SweepArgs *, Launch);
 constexpr int kVs[] = {1, 2, 4, 8};
 
-SweepFn sweep_fn(int V, int IB) {
-  if (IB == 1) {
-    switch (V) {
-      case 1: return sweep_kernel<1, 1>;
-      case 2: return sweep_kernel<2, 1>;
-      case 4: return sweep_kernel<4, 1>;
-      case 8: return sweep_kernel<8, 1>;
-    }
-  } else {
-    switch (V) {
-      case 1: return sweep_kernel<1, 2>;
-      case 2: return sweep_kernel<2, 2>;
-      case 4: return sweep_kernel<4, 2>;
-      case 8: return sweep_kernel<8, 2>;
-    }
+template <int IB>
+SweepFn regs_fn(int V) {
+  switch (V) {
+    case 1: return sweep_kernel<1, IB>;
+    case 2: return sweep_kernel<2, IB>;
+    case 4: return sweep_kernel<4, IB>;
+    case 8: return sweep_kernel<8, IB>;
   }
   return nullptr;
 }
+
+SweepFn sweep_fn(int V, int IB) { return IB == 1 ? regs_fn<1>(V) : regs_fn<2>(V); }
 
 SweepFn stream_fn(int IB) {
   return IB == 1 ? sweep_kernel_stream<1> : sweep_kernel_stream<2>;

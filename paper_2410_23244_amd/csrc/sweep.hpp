@@ -39,6 +39,7 @@ namespace bart {
 constexpr uint32_t kSpinLimit = 1u << 21;
 constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
 constexpr int kRegLeaves = 8;  // trees with at most this many leaves are reduced in registers
+constexpr int kRegPath = 0;
 constexpr int kBinRanks = kBinFloats / (kWaves * 64);  // ranks per pass of the LDS bins (64)
 
 __device__ __forceinline__ uint64_t ld_dev(const uint64_t *p) {
@@ -169,11 +170,12 @@ struct IdxChunk<2> {
 
 constexpr int kPropWords = (int)(sizeof(Prop) / 4);
 
-// Word t (< 24) of tree j's proposal record: a lane-varying load, so nothing
-// waits for it until it is stored to LDS.
+// Word t mod 24 of tree j's proposal record: a lane-varying load, so nothing
+// waits for it until it is stored to LDS.  Every thread loads (a register
+// that is either loaded or set would make the compiler wait for all
+// outstanding loads before setting it).
 __device__ __forceinline__ uint32_t load_prop_word(const SweepArgs *__restrict__ A, int j) {
-  const int t = threadIdx.x;
-  return t < kPropWords ? (gbl((const uint32_t *)(A->prop + j)))[t] : 0u;
+  return (gbl((const uint32_t *)(A->prop + j)))[threadIdx.x % kPropWords];
 }
 
 // Rank table of the larger tree from the proposal record already in LDS.
@@ -204,16 +206,15 @@ struct TdRegs {
 __device__ __forceinline__ TdRegs load_tree_data(const SweepArgs *__restrict__ A, const Ctx &c,
                                                  int j, int64_t s) {
   const int t = threadIdx.x, H = A->H;
-  TdRegs r{0, 0.f, 0.0};
-  int h = -1;
+  // every thread loads (slot 1 when it has no rank), see load_prop_word
+  int h = 1;
   if (t < c.pr.L) h = c.heap_of[t];
   if (t == kBlock - 1 && c.pr.move != kNone) h = c.pr.eta;
-  if (h >= 0) {
-    const int64_t o = (int64_t)j * 2 * H + h;
-    r.cnt = gbl((const int32_t *)A->count)[o];
-    r.mu = gbl((const float *)A->leaf)[o];
-    r.z = gbl((const double *)A->z)[(int64_t)(s & 1) * A->m * 2 * H + o];
-  }
+  const int64_t o = (int64_t)j * 2 * H + h;
+  TdRegs r;
+  r.cnt = gbl((const int32_t *)A->count)[o];
+  r.mu = gbl((const float *)A->leaf)[o];
+  r.z = gbl((const double *)A->z)[(int64_t)(s & 1) * A->m * 2 * H + o];
   return r;
 }
 
@@ -277,7 +278,8 @@ __device__ __forceinline__ uint64_t *mailbox(const SweepArgs *__restrict__ A, in
 // the others counts), with all loads of a batch in flight at once.  The
 // partition depends only on G and K, so every workgroup sums in the same
 // order.  Returns nseg.  Ends with an LDS barrier.
-__device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, Shared &sh, int par,
+template <class SH>
+__device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH &sh, int par,
                                             uint32_t seq, int K, int nsum) {
   const int t = threadIdx.x, G = A->G;
   int nb = 1;
@@ -322,14 +324,16 @@ __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, Sha
 }
 
 // Total of word k over all mailboxes: the segments summed in increasing order.
-__device__ __forceinline__ double seg_total(const Shared &sh, int nseg, int K, int k) {
+template <class SH>
+__device__ __forceinline__ double seg_total(const SH &sh, int nseg, int K, int k) {
   double acc = 0.0;
   for (int seg = 0; seg < nseg; ++seg) acc += sh.part[seg * K + k];
   return acc;
 }
 
 // Grid-wide sum of one fp64 word per workgroup (sigma^2 step), into sh.tot[0].
-__device__ __forceinline__ void gather_total(const SweepArgs *__restrict__ A, Shared &sh, int par,
+template <class SH>
+__device__ __forceinline__ void gather_total(const SweepArgs *__restrict__ A, SH &sh, int par,
                                              uint32_t seq, int nsum) {
   const int nseg = gather_polls(A, sh, par, seq, 1, nsum);
   if (threadIdx.x == 0) sh.tot[0] = seg_total(sh, nseg, 1, 0);
@@ -510,8 +514,9 @@ __device__ __forceinline__ void finish_tree(const SweepArgs *__restrict__ A, con
 // residuals are in sh.wave_part: the next sweep's proposals (owners) and
 // normals, the grid-wide SSR in a fixed order, and the draw, made by every
 // workgroup alike.
+template <class SH>
 __device__ __forceinline__ void sigma2_tail(const SweepArgs *__restrict__ A, const Launch &Lc,
-                                            Shared &sh, int64_t s, int step, uint32_t seq,
+                                            SH &sh, int64_t s, int step, uint32_t seq,
                                             int par) {
   const int t = threadIdx.x, w = blockIdx.x, m = A->m;
   const uint64_t seed = Lc.seed;
@@ -674,7 +679,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   // Ends with an LDS barrier.
   auto reduce = [&](int tree, const uint32_t (&rks)[V]) {
     const int L = sh.ctx[tree & (kRing - 1)].pr.L;
-    if (L <= kRegLeaves) {
+    if (L <= kRegPath) {
       float acc[kRegLeaves];
 #pragma unroll
       for (int k = 0; k < kRegLeaves; ++k) acc[k] = 0.f;
@@ -726,7 +731,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   };
   // this workgroup's partial sum of rank k of a tree with L leaves (after reduce)
   auto partial = [&](int L, int k) {
-    if (L > kRegLeaves) return sh.red[k];
+    if (L > kRegPath) return sh.red[k];
     double acc = 0.0;
 #pragma unroll
     for (int u = 0; u < kWaves; ++u) acc += sh.red_w[k][u];
@@ -790,9 +795,9 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       // 2. while the mailboxes fill: load rows of j+2, the decision data of
       //    j+1 and the proposal of j+3
       if (more2) issue_rows(j + 2);
-      TdRegs tdn{0, 0.f, 0.0};
-      if (more1) tdn = load_tree_data(A, sh.ctx[(j + 1) & (kRing - 1)], j + 1, s);
-      const uint32_t pw3 = more3 ? load_prop_word(A, j + 3) : 0u;
+      const int j1 = more1 ? j + 1 : j, j3 = more3 ? j + 3 : j;
+      const TdRegs tdn = load_tree_data(A, sh.ctx[j1 & (kRing - 1)], j1, s);
+      const uint32_t pw3 = load_prop_word(A, j3);
       lds_barrier();  // nr[j&1] read by the poster before it is cleared
       if (t == L) sh.nr[j & 1] = 0;
       // 3. totals of tree j, in the same order in every workgroup: polls into
@@ -1137,9 +1142,9 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
         const uint64_t pay = t < L ? pack_f64(partial(L, t)) : (uint64_t)sh.nr[j & 1];
         st_dev(mailbox(A, par, w) + t, mk_word(seq, pay));
       }
-      TdRegs tdn{0, 0.f, 0.0};
-      if (more1) tdn = load_tree_data(A, sh.ctx[(j + 1) & (kRing - 1)], j + 1, s);
-      const uint32_t pw3 = more3 ? load_prop_word(A, j + 3) : 0u;
+      const int j1 = more1 ? j + 1 : j, j3 = more3 ? j + 3 : j;
+      const TdRegs tdn = load_tree_data(A, sh.ctx[j1 & (kRing - 1)], j1, s);
+      const uint32_t pw3 = load_prop_word(A, j3);
       lds_barrier();
       if (t == L) sh.nr[j & 1] = 0;
       const int nseg = gather_polls(A, sh, par, seq, L + 1, L);
