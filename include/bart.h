@@ -27,6 +27,11 @@
  *    of the calling thread.
  *  - Work is enqueued asynchronously on the handle's HIP stream; only
  *    bart_get_state() and bart_status() synchronise it.
+ *  - A handle holds nchain >= 1 independent chains of the same model and
+ *    data (sec. 2.2, "Behavior of the BART MCMC", advises running several
+ *    and comparing them).  They share X_b and advance together, one sweep
+ *    kernel launch serving all of them; each has its own trees, index cache,
+ *    residuals, sigma^2 and random stream.
  */
 #ifndef BART_H
 #define BART_H
@@ -82,10 +87,14 @@ typedef struct {
   int32_t ntree;      /* trees m (sec. 2.1 "Hyperparameters"), >= 1 */
   int32_t max_depth;  /* D in [2, 8]; nodes at depth D-1 are leaves */
   int32_t idx_bytes;  /* 1 or 2: width of the index cache entries */
-  int32_t grid;       /* workgroups of the sweep kernel (one decides, the rest own
-                         the observations): 0 = automatic, else in [2, 256] */
+  int32_t grid;       /* workgroups of the sweep kernel per chain, each owning a
+                         slice of the observations: 0 = automatic, else in
+                         [1, 256] with grid x nchain <= compute units */
   int32_t launch;     /* BART_LAUNCH_COOPERATIVE or BART_LAUNCH_ORDINARY */
   int32_t residency;  /* BART_RESID_AUTO, BART_RESID_REGISTERS or BART_RESID_STREAMED */
+  int32_t nchain;     /* independent chains: 0 or 1 = one, else in [1, 256] (at most
+                         one per compute unit) */
+  int32_t reserved;   /* set to 0 */
   int64_t x_stride;   /* elements between predictor rows of X_b: >= n, multiple of 16 */
   double alpha, beta; /* tree prior P_d = alpha (1+d)^-beta, alpha in [0,1], beta >= 0 */
   double mu_mu;       /* leaf prior mean (sec. 2.1 "Prior over leaf values") */
@@ -95,9 +104,10 @@ typedef struct {
   double p_grow;      /* P(GROW) when both GROW and PRUNE are possible, in [0,1] */
 } bart_config;
 
-/* Chain state, in the layouts above.  For bart_get_state the array pointers
- * are caller-owned device buffers that receive copies; for bart_set_state
- * they are read.  idx is dense [ntree][n] of idx_bytes-wide entries. */
+/* State of one chain, in the layouts above.  For bart_get_state the array
+ * pointers are caller-owned device buffers that receive copies; for
+ * bart_set_state they are read.  idx is dense [ntree][n] of idx_bytes-wide
+ * entries.  chain selects the chain (input of both calls). */
 typedef struct {
   uint16_t *axis;
   uint8_t *cut;
@@ -107,7 +117,7 @@ typedef struct {
   double sigma2;
   int64_t sweep;  /* index of the sweep in progress */
   int32_t next;   /* next step of that sweep: 0..ntree-1 trees, ntree = sigma^2 */
-  int32_t pad;
+  int32_t chain;  /* in [0, nchain) */
 } bart_state;
 
 /* Per-step record written by bart_debug_steps (4224 bytes).  Slots are heap
@@ -132,56 +142,61 @@ typedef struct {
   float leaf_new[256];
 } bart_trace;
 
-/* Launch shape chosen by bart_init. */
+/* Launch shape chosen by bart_init (grid: workgroups per chain; the launch
+ * has grid x nchain workgroups). */
 typedef struct {
   int32_t grid, block, chunks_per_thread, lds_bytes;
   int32_t obs_per_thread, max_leaves, launch, residency;
+  int32_t nchain, reserved;
 } bart_launch;
 
 /* Bytes of device workspace bart_init needs for cfg (0 if cfg is invalid). */
 size_t bart_workspace_bytes(const bart_config *cfg);
 
-/* Create a chain.  X_b: device u8 [p][x_stride], borrowed.  y_c: device f32
- * [n], the centred response, copied into the residual cache.  n_cuts: HOST
+/* Create nchain chains.  X_b: device u8 [p][x_stride], borrowed.  y_c: device
+ * f32 [n], the centred response, copied into every chain's residual cache.  n_cuts: HOST
  * int32 [p], number of cutpoints K_a in [0, 255] of each axis, copied.
  * workspace: device, >= bart_workspace_bytes(cfg), 256-byte aligned,
- * borrowed.  stream: a hipStream_t (NULL = default stream).  Initial state:
- * every tree root-only with leaf 0, index cache 1, residuals = y_c,
- * sigma^2 = sigma2_init, sweep 0 (sec. 3.3 "Residuals cache").  On success
- * *out receives the handle. */
+ * borrowed.  stream: a hipStream_t (NULL = default stream).  Initial state of
+ * every chain: every tree root-only with leaf 0, index cache 1, residuals =
+ * y_c, sigma^2 = sigma2_init, sweep 0 (sec. 3.3 "Residuals cache").  On
+ * success *out receives the handle. */
 int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c,
               const int32_t *n_cuts, void *workspace, size_t ws_bytes, void *stream,
               bart_handle **out);
 
-/* Run k_sweeps >= 0 whole sweeps (each: every tree in order, then sigma^2;
- * sec. 2.2 "The BART MCMC").  The chain must be at a sweep boundary
- * (BART_ESTATE otherwise).  Random draws of sweep s, tree j are a pure
- * function of (seed, s, j): two calls of k sweeps equal one call of 2k. */
+/* Run k_sweeps >= 0 whole sweeps of every chain (each: every tree in order,
+ * then sigma^2; sec. 2.2 "The BART MCMC").  The chains must be at a sweep
+ * boundary (BART_ESTATE otherwise).  Random draws of chain c, sweep s, tree j
+ * are a pure function of (seed, c, s, j): Philox4x64-10 with key (seed,
+ * 0x42415254 + c 2^32), so chain 0 draws what a lone chain draws, and two
+ * calls of k sweeps equal one call of 2k. */
 int bart_step(bart_handle *h, int32_t k_sweeps, uint64_t seed);
 
 /* Sum-of-trees prediction f(x) = offset + sum_j g(x; T_j, M_j) (eq. bartdef),
  * each tree traversed by Algorithm 1, summed in fp64 in tree order and
- * rounded to f32.  Xt: device u8 [p][xt_stride] binned like X_b,
- * xt_stride >= n_t and a multiple of 16; out: device f32 [n_t]. */
+ * rounded to f32, for every chain.  Xt: device u8 [p][xt_stride] binned like
+ * X_b, xt_stride >= n_t and a multiple of 16; out: device f32 [nchain][n_t]. */
 int bart_predict(bart_handle *h, const uint8_t *Xt, int64_t xt_stride, int64_t n_t,
                  double offset, float *out);
 
-/* Copy the state into caller device buffers and fill the scalars; this
- * synchronises the handle's stream. */
+/* Copy the state of chain dst->chain into caller device buffers and fill
+ * the scalars; this synchronises the handle's stream. */
 int bart_get_state(bart_handle *h, bart_state *dst);
 
-/* Replace the state from caller device buffers (index cache and trees must
- * be consistent: every idx entry a leaf of its tree).  Per-leaf counts are
- * recomputed on the device. */
+/* Replace the state of chain src->chain from caller device buffers (index
+ * cache and trees must be consistent: every idx entry a leaf of its tree).
+ * Per-leaf counts are recomputed on the device.  The position (sweep, next)
+ * is shared by all chains: setting it moves every chain. */
 int bart_set_state(bart_handle *h, const bart_state *src);
 
 /* Run the next n_steps steps (tree steps and sigma^2 steps, in order, from
  * any position) with the same kernel as bart_step, writing one record per
- * step into trace (device bart_trace [n_steps]). */
+ * step and chain into trace (device bart_trace [nchain][n_steps]). */
 int bart_debug_steps(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace);
 
 /* Synchronise the stream and return BART_OK, or BART_EDEVICE with the device
- * error bits in *bits (may be NULL). */
+ * error bits of all chains (or-ed) in *bits (may be NULL). */
 int bart_status(bart_handle *h, uint32_t *bits);
 
 /* Launch shape of the sweep kernel. */

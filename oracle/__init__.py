@@ -33,7 +33,7 @@ def build(force: bool = True) -> str:
 class Config(C.Structure):
     _fields_ = [("n", C.c_int32), ("p", C.c_int32), ("m", C.c_int32), ("D", C.c_int32),
                 ("idx_bytes", C.c_int32), ("fix_sigma2", C.c_int32),
-                ("alpha", C.c_double), ("beta", C.c_double), ("mu_mu", C.c_double),
+                ("chain", C.c_int32), ("pad", C.c_int32), ("alpha", C.c_double), ("beta", C.c_double), ("mu_mu", C.c_double),
                 ("sigma_mu", C.c_double), ("nu", C.c_double), ("lam", C.c_double),
                 ("p_grow", C.c_double)]
 
@@ -97,9 +97,10 @@ def _ptr(a: np.ndarray) -> int:
 
 
 def make_config(n, p, m, D, idx_bytes=1, alpha=0.95, beta=2.0, mu_mu=0.0, sigma_mu=1.0,
-                nu=3.0, lam=1.0, p_grow=0.5, fix_sigma2=False) -> Config:
+                nu=3.0, lam=1.0, p_grow=0.5, fix_sigma2=False, chain=0) -> Config:
+    """chain selects the random stream: counter word 3 offset by chain * 2^32."""
     return Config(int(n), int(p), int(m), int(D), int(idx_bytes), int(bool(fix_sigma2)),
-                  float(alpha), float(beta), float(mu_mu), float(sigma_mu), float(nu),
+                  int(chain), 0, float(alpha), float(beta), float(mu_mu), float(sigma_mu), float(nu),
                   float(lam), float(p_grow))
 
 

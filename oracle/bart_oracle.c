@@ -65,13 +65,15 @@ void oc_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out
   out[3] = x3;
 }
 
-/* Stream layout: counter (s, j, q, t), key (seed, "BART").
+/* Stream layout of chain c: counter (s, j, q, c 2^32 + t), key (seed,
+ * "BART"); every t is below 2^32, so no two chains share a counter and
+ * chain 0 is the stream of a lone chain.
  *   q = 0, t = 0     proposal words of tree j in sweep s
  *   q = 1, t = h>>1  the two leaf normals of heap slots 2t, 2t+1
  *   q = 2, j = ~0    sigma^2 gamma attempts t = 0, 1, ...            */
-static void block(uint64_t seed, uint64_t s, uint64_t j, uint64_t q, uint64_t t,
-                  uint64_t out[4]) {
-  uint64_t ctr[4] = {s, j, q, t};
+static void block(uint64_t seed, uint32_t chain, uint64_t s, uint64_t j, uint64_t q,
+                  uint64_t t, uint64_t out[4]) {
+  uint64_t ctr[4] = {s, j, q, ((uint64_t)chain << 32) + t};
   uint64_t key[2] = {seed, KEY_TAG};
   oc_philox4x64_10(ctr, key, out);
 }
@@ -92,19 +94,23 @@ static double box_muller(uint64_t w_a, uint64_t w_b) {
   return sqrt(-2.0 * log(u1)) * cos(2.0 * M_PI * u2);
 }
 
-double oc_normal(uint64_t seed, uint64_t s, uint64_t j, uint64_t slot) {
+static double normal_of(uint64_t seed, uint32_t chain, uint64_t s, uint64_t j, uint64_t slot) {
   uint64_t w[4];
-  block(seed, s, j, 1, slot >> 1, w);
+  block(seed, chain, s, j, 1, slot >> 1, w);
   return (slot & 1) ? box_muller(w[2], w[3]) : box_muller(w[0], w[1]);
 }
 
+double oc_normal(uint64_t seed, uint64_t s, uint64_t j, uint64_t slot) {
+  return normal_of(seed, 0, s, j, slot);
+}
+
 /* Gamma(shape, 1) by Marsaglia & Tsang (2000), shape >= 1. */
-double oc_gamma_draw(uint64_t seed, uint64_t s, double shape) {
+static double gamma_of(uint64_t seed, uint32_t chain, uint64_t s, double shape) {
   double d = shape - 1.0 / 3.0;
   double c = 1.0 / sqrt(9.0 * d);
   for (uint64_t t = 0; t < 4096; t++) {
     uint64_t w[4];
-    block(seed, s, ~0ULL, 2, t, w);
+    block(seed, chain, s, ~0ULL, 2, t, w);
     double z = box_muller(w[0], w[1]);
     double u = u01(w[2]);
     double v = 1.0 + c * z;
@@ -118,11 +124,20 @@ double oc_gamma_draw(uint64_t seed, uint64_t s, double shape) {
  * lambda*nu/sigma^2 ~ chi^2_nu of eq. (bartdef) is InvGamma(nu/2,
  * nu*lambda/2), conjugate to the normal errors (sec. 3.3 "Sampling the
  * error variance"). */
-double oc_sigma2_draw(uint64_t seed, uint64_t s, double nu, double lambda, int64_t n,
-                      double ssr) {
+double oc_gamma_draw(uint64_t seed, uint64_t s, double shape) {
+  return gamma_of(seed, 0, s, shape);
+}
+
+static double sigma2_of(uint64_t seed, uint32_t chain, uint64_t s, double nu, double lambda,
+                        int64_t n, double ssr) {
   double shape = 0.5 * (nu + (double)n);
   double scale = 0.5 * (nu * lambda + ssr);
-  return scale / oc_gamma_draw(seed, s, shape);
+  return scale / gamma_of(seed, chain, s, shape);
+}
+
+double oc_sigma2_draw(uint64_t seed, uint64_t s, double nu, double lambda, int64_t n,
+                      double ssr) {
+  return sigma2_of(seed, 0, s, nu, lambda, n, ssr);
 }
 
 /* ------------------------------------------------------------------ */
@@ -479,7 +494,7 @@ static void tree_step(const oc_config *c, const int32_t *n_cuts, const uint8_t *
 
   /* 1-2: propose (sec. 3.3 item 1) */
   uint64_t w[4];
-  block(seed, s, (uint64_t)j, 0, 0, w);
+  block(seed, (uint32_t)c->chain, s, (uint64_t)j, 0, 0, w);
   int32_t prop[6];
   oc_propose(c, n_cuts, axis, cut, w, prop);
   int32_t move = prop[0], eta = prop[1], a = prop[2], sc = prop[3];
@@ -563,7 +578,7 @@ static void tree_step(const oc_config *c, const int32_t *n_cuts, const uint8_t *
     if (!fin_leaf[h]) continue;
     double mean, prec;
     oc_leaf_posterior((double)cnt[h], S[h], st->sigma2, c->mu_mu, c->sigma_mu, &mean, &prec);
-    double z = oc_normal(seed, s, (uint64_t)j, (uint64_t)h);
+    double z = normal_of(seed, (uint32_t)c->chain, s, (uint64_t)j, (uint64_t)h);
     fresh[h] = (float)(mean + z / sqrt(prec));
     if (tr) tr->leaf_new[h] = fresh[h];
     /* lockstep hook: carry on from another implementation's draws */
@@ -592,7 +607,8 @@ static void sigma_step(const oc_config *c, oc_state *st, uint64_t seed, oc_trace
   double ssr = 0.0;
   for (int64_t i = 0; i < c->n; i++) ssr += (double)st->resid[i] * (double)st->resid[i];
   if (!c->fix_sigma2)
-    st->sigma2 = oc_sigma2_draw(seed, (uint64_t)st->sweep, c->nu, c->lambda, c->n, ssr);
+    st->sigma2 = sigma2_of(seed, (uint32_t)c->chain, (uint64_t)st->sweep, c->nu, c->lambda, c->n,
+                           ssr);
   if (tr) {
     memset(tr, 0, sizeof(*tr));
     tr->kind = 1;
@@ -605,7 +621,7 @@ static void sigma_step(const oc_config *c, oc_state *st, uint64_t seed, oc_trace
 
 int oc_step(const oc_config *c, const int32_t *n_cuts, const uint8_t *X, int64_t ldx,
             oc_state *st, uint64_t seed, int32_t force, const float *adopt, oc_trace *trace) {
-  if (c->D < 2 || c->D > 8 || st->next < 0 || st->next > c->m) return -1;
+  if (c->D < 2 || c->D > 8 || c->chain < 0 || st->next < 0 || st->next > c->m) return -1;
   if (st->next < c->m) {
     tree_step(c, n_cuts, X, ldx, st, seed, force, adopt, trace);
     st->next += 1;

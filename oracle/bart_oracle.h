@@ -31,6 +31,8 @@ extern "C" {
 typedef struct {
   int32_t n, p, m, D, idx_bytes;  /* observations, predictors, trees, depth, 1|2 */
   int32_t fix_sigma2;             /* test hook: 1 = keep sigma^2 fixed (no Gibbs draw) */
+  int32_t chain;                  /* which chain's random stream (>= 0) */
+  int32_t pad;
   double alpha, beta;             /* tree prior P_d = alpha/(1+d)^beta (sec. 2.1) */
   double mu_mu, sigma_mu;         /* leaf prior N(mu_mu, sigma_mu^2) (sec. 2.1) */
   double nu, lambda;              /* lambda*nu/sigma^2 ~ chi^2_nu (eq. bartdef) */
@@ -91,7 +93,8 @@ double oc_log_ratio(const oc_config *c, const int32_t *n_cuts, const uint8_t *X,
                     int32_t eta, int32_t a, int32_t s, double *scale);
 int32_t oc_route(int32_t D, const uint16_t *axis, const uint8_t *cut, const uint8_t *X,
                  int64_t ldx, int64_t i);
-/* One step (tree step `next`, or the sigma^2 step).  Lockstep hooks for
+/* oc_normal, oc_gamma_draw and oc_sigma2_draw draw from chain 0's stream.
+ * One step (tree step `next`, or the sigma^2 step) of chain c->chain.  Lockstep hooks for
  * comparing another implementation step by step: force >= 0 replaces the
  * accept decision of a tree step; adopt (256 floats, or NULL) replaces the
  * new leaf values used to update the state after they were drawn and

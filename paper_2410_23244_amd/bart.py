@@ -34,7 +34,8 @@ BART_RESID_AUTO, BART_RESID_REGISTERS, BART_RESID_STREAMED = 0, 1, 2
 class Config(C.Structure):
     _fields_ = [("n", C.c_int32), ("p", C.c_int32), ("ntree", C.c_int32),
                 ("max_depth", C.c_int32), ("idx_bytes", C.c_int32), ("grid", C.c_int32),
-                ("launch", C.c_int32), ("residency", C.c_int32), ("x_stride", C.c_int64),
+                ("launch", C.c_int32), ("residency", C.c_int32), ("nchain", C.c_int32),
+                ("reserved", C.c_int32), ("x_stride", C.c_int64),
                 ("alpha", C.c_double), ("beta", C.c_double),
                 ("mu_mu", C.c_double), ("sigma_mu", C.c_double), ("nu", C.c_double),
                 ("lam", C.c_double), ("sigma2_init", C.c_double), ("p_grow", C.c_double)]
@@ -43,13 +44,14 @@ class Config(C.Structure):
 class State(C.Structure):
     _fields_ = [("axis", C.c_void_p), ("cut", C.c_void_p), ("leaf", C.c_void_p),
                 ("idx", C.c_void_p), ("resid", C.c_void_p), ("sigma2", C.c_double),
-                ("sweep", C.c_int64), ("next", C.c_int32), ("pad", C.c_int32)]
+                ("sweep", C.c_int64), ("next", C.c_int32), ("chain", C.c_int32)]
 
 
 class LaunchInfo(C.Structure):
     _fields_ = [("grid", C.c_int32), ("block", C.c_int32), ("chunks_per_thread", C.c_int32),
                 ("lds_bytes", C.c_int32), ("obs_per_thread", C.c_int32),
-                ("max_leaves", C.c_int32), ("launch", C.c_int32), ("residency", C.c_int32)]
+                ("max_leaves", C.c_int32), ("launch", C.c_int32), ("residency", C.c_int32),
+                ("nchain", C.c_int32), ("reserved", C.c_int32)]
 
 
 # bart_trace, 4224 bytes (include/bart.h)
@@ -158,17 +160,20 @@ def x_stride_for(n: int) -> int:
 
 
 class Bart:
-    """A BART chain on the current HIP device.
+    """nchain BART chains of one model on the current HIP device.
 
     X_b: uint8 [p][n] (numpy or torch); y_c: float32 [n]; n_cuts: int [p].
     The binned predictors are copied once to the device with a row stride that
-    is a multiple of 256; the workspace is one torch uint8 tensor."""
+    is a multiple of 256; the workspace is one torch uint8 tensor.  With one
+    chain, traces and predictions are [n_steps] and [n_t]; with several they
+    gain a leading chain axis."""
 
     def __init__(self, X_b, y_c, n_cuts, *, ntree: int, max_depth: int = 6,
                  idx_bytes: int = 1, alpha: float = 0.95, beta: float = 2.0,
                  mu_mu: float = 0.0, sigma_mu: float = 1.0, nu: float = 3.0,
                  lam: float = 1.0, sigma2_init: float = 1.0, p_grow: float = 0.5,
-                 grid: int = 0, launch: int = 0, residency: int = 0, device: str = "cuda"):
+                 grid: int = 0, launch: int = 0, residency: int = 0, nchain: int = 1,
+                 device: str = "cuda"):
         import torch
 
         if not torch.cuda.is_available():
@@ -186,9 +191,10 @@ class Bart:
         yn = y_c.cpu().numpy() if hasattr(y_c, "cpu") else np.asarray(y_c)
         self.y = torch.from_numpy(np.ascontiguousarray(yn, dtype=np.float32)).to(self.device)
         self.n_cuts = np.ascontiguousarray(n_cuts, dtype=np.int32)
-        self.cfg = Config(n, p, ntree, max_depth, idx_bytes, grid, launch, residency, self.x_stride,
-                          alpha, beta,
-                          mu_mu, sigma_mu, nu, lam, sigma2_init, p_grow)
+        self.nchain = nchain
+        self.cfg = Config(n, p, ntree, max_depth, idx_bytes, grid, launch, residency, nchain, 0,
+                          self.x_stride, alpha, beta, mu_mu, sigma_mu, nu, lam, sigma2_init,
+                          p_grow)
         nbytes = bart_workspace_bytes(self.cfg)
         if nbytes == 0:
             raise BartError(BART_EINVAL, "invalid configuration")
@@ -206,10 +212,13 @@ class Bart:
 
     def debug_steps(self, n_steps: int, seed: int) -> np.ndarray:
         torch = self.torch
-        buf = torch.zeros(n_steps * TRACE_DTYPE.itemsize, dtype=torch.uint8, device=self.device)
+        C_ = self.nchain
+        buf = torch.zeros(C_ * n_steps * TRACE_DTYPE.itemsize, dtype=torch.uint8,
+                          device=self.device)
         bart_debug_steps(self.h, n_steps, seed, buf.data_ptr())
         self.stream.synchronize()
-        return buf.cpu().numpy().view(TRACE_DTYPE)
+        tr = buf.cpu().numpy().view(TRACE_DTYPE)
+        return tr if C_ == 1 else tr.reshape(C_, n_steps)
 
     def predict(self, Xt, offset: float = 0.0):
         torch = self.torch
@@ -219,10 +228,10 @@ class Bart:
         stride = x_stride_for(nt)
         Xd = torch.zeros((p, stride), dtype=torch.uint8, device=self.device)
         Xd[:, :nt] = torch.from_numpy(np.ascontiguousarray(Xn, dtype=np.uint8)).to(self.device)
-        out = torch.empty(nt, dtype=torch.float32, device=self.device)
+        out = torch.empty((self.nchain, nt), dtype=torch.float32, device=self.device)
         bart_predict(self.h, Xd.data_ptr(), stride, nt, offset, out.data_ptr())
         self.stream.synchronize()
-        return out
+        return out[0] if self.nchain == 1 else out
 
     def status(self) -> int:
         return bart_status(self.h)
@@ -231,7 +240,7 @@ class Bart:
         return bart_launch_info(self.h)
 
     # -- state
-    def get_state(self) -> dict:
+    def get_state(self, chain: int = 0) -> dict:
         torch = self.torch
         m, H, n = self.m, self.H, self.n
         it = torch.uint8 if self.idx_bytes == 1 else torch.int16
@@ -241,7 +250,7 @@ class Bart:
                     idx=torch.empty((m, n), dtype=it, device=self.device),
                     resid=torch.empty(n, dtype=torch.float32, device=self.device))
         st = State(bufs["axis"].data_ptr(), bufs["cut"].data_ptr(), bufs["leaf"].data_ptr(),
-                   bufs["idx"].data_ptr(), bufs["resid"].data_ptr(), 0.0, 0, 0, 0)
+                   bufs["idx"].data_ptr(), bufs["resid"].data_ptr(), 0.0, 0, 0, int(chain))
         bart_get_state(self.h, st)
         out = {k: v.cpu().numpy() for k, v in bufs.items()}
         out["axis"] = out["axis"].view(np.uint16)
@@ -250,7 +259,7 @@ class Bart:
         out.update(sigma2=st.sigma2, sweep=st.sweep, next=st.next)
         return out
 
-    def set_state(self, s: dict) -> None:
+    def set_state(self, s: dict, chain: int = 0) -> None:
         torch = self.torch
         dev = {}
         for k in ["axis", "cut", "leaf", "idx", "resid"]:
@@ -260,7 +269,7 @@ class Bart:
             dev[k] = torch.from_numpy(a).to(self.device)
         st = State(dev["axis"].data_ptr(), dev["cut"].data_ptr(), dev["leaf"].data_ptr(),
                    dev["idx"].data_ptr(), dev["resid"].data_ptr(), float(s["sigma2"]),
-                   int(s["sweep"]), int(s.get("next", 0)), 0)
+                   int(s["sweep"]), int(s.get("next", 0)), int(chain))
         bart_set_state(self.h, st)
         self.stream.synchronize()
 
@@ -276,10 +285,10 @@ class Bart:
             pass
 
 
-def from_inputs(inp, grid: int = 0, launch: int = 0, residency: int = 0) -> Bart:
-    """A chain for a generated workload (paper_2410_23244_amd.inputs.Inputs)."""
+def from_inputs(inp, grid: int = 0, launch: int = 0, residency: int = 0, nchain: int = 1) -> Bart:
+    """Chains for a generated workload (paper_2410_23244_amd.inputs.Inputs)."""
     h = inp.hyper
     return Bart(inp.X_b, inp.y_c, inp.n_cuts, ntree=inp.m, max_depth=inp.D,
                 idx_bytes=inp.idx_bytes, alpha=h.alpha, beta=h.beta, mu_mu=h.mu_mu,
                 sigma_mu=h.sigma_mu, nu=h.nu, lam=h.lam, sigma2_init=h.sigma2_init,
-                p_grow=h.p_grow, grid=grid, launch=launch, residency=residency)
+                p_grow=h.p_grow, grid=grid, launch=launch, residency=residency, nchain=nchain)

@@ -39,11 +39,17 @@ int fail(int code, const char *fmt, ...) {
 constexpr size_t kAlign = 256;
 size_t up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+// Workspace: nchain chain blocks of chain_bytes each (offsets resid..pub are
+// relative to a block), then the shared part (offsets n_cuts..args absolute).
 struct Layout {
   int64_t n_pad;
-  size_t resid, idx, axis, cut, leaf, count, prop, z, n_cuts, nz_list, nz_rank, ctl, pub,
-      args, total;
+  int32_t nchain;
+  int32_t gcap;  // workgroups per chain the mailboxes are sized for
+  size_t resid, idx, axis, cut, leaf, count, prop, z, ctl, pub, chain_bytes;
+  size_t n_cuts, nz_list, nz_rank, args, total;
 };
+
+int nchain_of(const bart_config &c) { return c.nchain > 0 ? c.nchain : 1; }
 
 const char *check_config(const bart_config *c) {
   if (!c) return "config is NULL";
@@ -53,6 +59,9 @@ const char *check_config(const bart_config *c) {
   if (c->max_depth < 2 || c->max_depth > 8) return "max_depth must be in [2, 8]";
   if (c->idx_bytes != 1 && c->idx_bytes != 2) return "idx_bytes must be 1 or 2";
   if (c->grid < 0 || c->grid > kMaxGrid) return "grid must be 0 or in [1, 256]";
+  if (c->nchain < 0 || c->nchain > kMaxGrid) return "nchain must be 0 or in [1, 256]";
+  if (c->grid > 0 && (int64_t)c->grid * nchain_of(*c) > kMaxGrid)
+    return "grid x nchain must not exceed 256";
   if (c->launch != BART_LAUNCH_COOPERATIVE && c->launch != BART_LAUNCH_ORDINARY)
     return "launch must be BART_LAUNCH_COOPERATIVE or BART_LAUNCH_ORDINARY";
   if (c->residency < BART_RESID_AUTO || c->residency > BART_RESID_STREAMED)
@@ -81,6 +90,8 @@ Layout make_layout(const bart_config &c) {
     o = up(o + bytes, kAlign);
     return at;
   };
+  L.nchain = nchain_of(c);
+  L.gcap = kMaxGrid / L.nchain;
   L.resid = take(sizeof(float) * L.n_pad);
   L.idx = take((size_t)m * L.n_pad * c.idx_bytes);
   L.axis = take(sizeof(uint16_t) * m * H);
@@ -89,12 +100,14 @@ Layout make_layout(const bart_config &c) {
   L.count = take(sizeof(int32_t) * m * 2 * H);
   L.prop = take(sizeof(Prop) * m);
   L.z = take(sizeof(double) * 2 * m * 2 * H);
+  L.ctl = take(sizeof(Ctl));
+  L.pub = take(sizeof(uint64_t) * 2 * L.gcap * kStride);
+  L.chain_bytes = o;
+  o = L.chain_bytes * L.nchain;
   L.n_cuts = take(sizeof(int32_t) * c.p);
   L.nz_list = take(sizeof(int32_t) * c.p);
   L.nz_rank = take(sizeof(int32_t) * c.p);
-  L.ctl = take(sizeof(Ctl));
-  L.pub = take(sizeof(uint64_t) * 2 * kMaxGrid * kStride);
-  L.args = take(sizeof(SweepArgs));
+  L.args = take(sizeof(SweepArgs) * L.nchain);
   L.total = o;
   return L;
 }
@@ -152,9 +165,10 @@ __global__ void k_init_trees(uint16_t *axis, uint8_t *cut, float *leaf, int32_t 
   }
 }
 
+// sigma2 < 0 keeps the current value
 __global__ void k_set_ctl(Ctl *ctl, double sigma2, int64_t sweep, int reset_stats) {
   if (threadIdx.x == 0 && blockIdx.x == 0) {
-    ctl->sigma2 = sigma2;
+    if (sigma2 >= 0.0) ctl->sigma2 = sigma2;
     ctl->sweep = sweep;
     if (reset_stats) {
       ctl->error = 0;
@@ -164,6 +178,15 @@ __global__ void k_set_ctl(Ctl *ctl, double sigma2, int64_t sweep, int reset_stat
 }
 
 __global__ void k_clear_words(uint64_t *p, int64_t words) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < words;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0;
+}
+
+// The mailboxes of every chain: words at byte offset off of each chain block
+// (blockIdx.y = chain).
+__global__ void k_clear_mailboxes(char *ws, size_t off, size_t chain_bytes, int64_t words) {
+  uint64_t *p = (uint64_t *)(ws + blockIdx.y * chain_bytes + off);
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < words;
        i += (int64_t)gridDim.x * blockDim.x)
     p[i] = 0;
@@ -192,12 +215,19 @@ __global__ void k_recount(const uint8_t *idx, int64_t ldi, int ib, int32_t *coun
     if (hist[k]) atomicAdd(&count[(int64_t)j * 2 * H + k], hist[k]);
 }
 
-// f(x) = offset + sum_j g(x; T_j, M_j): Algorithm 1 per tree, fp64 sum in tree order.
+// f(x) = offset + sum_j g(x; T_j, M_j): Algorithm 1 per tree, fp64 sum in
+// tree order.  blockIdx.y = chain: its trees sit chain_bytes further on and
+// its predictions nt further on.
 __global__ void k_predict(const uint8_t *Xt, int64_t ldx, int64_t nt, int p,
-                          const uint16_t *axis, const uint8_t *cut, const float *leaf, int m,
-                          int D, int H, double offset, float *out) {
+                          const uint16_t *axis0, const uint8_t *cut0, const float *leaf0, int m,
+                          int D, int H, double offset, size_t chain_bytes, float *out0) {
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (i >= nt) return;
+  const size_t cb = blockIdx.y * chain_bytes;
+  const uint16_t *axis = (const uint16_t *)((const char *)axis0 + cb);
+  const uint8_t *cut = cut0 + cb;
+  const float *leaf = (const float *)((const char *)leaf0 + cb);
+  float *out = out0 + blockIdx.y * nt;
   double acc = 0.0;
   for (int j = 0; j < m; ++j) {
     const uint16_t *ax = axis + (int64_t)j * H;
@@ -230,7 +260,8 @@ struct bart_handle {
   const uint8_t *X;
   hipStream_t stream;
   int device;
-  int H, p_nz, V, G, lds;  // V: chunks of 4 observations per thread
+  int H, p_nz, V, G, lds;  // V: chunks of 4 observations per thread; G: workgroups per chain
+  int nchain;
   bool streamed;           // residuals streamed from HBM instead of kept in registers
   int64_t chunks;
   int64_t sweep;
@@ -241,30 +272,38 @@ struct bart_handle {
 
 namespace {
 
+// shared part of the workspace
 template <class T>
 T *at(bart_handle *h, size_t off) {
   return (T *)(h->ws + off);
 }
 
-SweepArgs make_args(bart_handle *h) {
+// block of chain c
+template <class T>
+T *atc(bart_handle *h, int c, size_t off) {
+  return (T *)(h->ws + (size_t)c * h->lay.chain_bytes + off);
+}
+
+SweepArgs make_args(bart_handle *h, int ch) {
   const bart_config &c = h->cfg;
   SweepArgs A{};
   A.X = h->X;
   A.ldx = c.x_stride;
-  A.resid = at<float>(h, h->lay.resid);
-  A.idx = at<void>(h, h->lay.idx);
+  A.resid = atc<float>(h, ch, h->lay.resid);
+  A.idx = atc<void>(h, ch, h->lay.idx);
   A.ldi = h->lay.n_pad;
-  A.axis = at<uint16_t>(h, h->lay.axis);
-  A.cut = at<uint8_t>(h, h->lay.cut);
-  A.leaf = at<float>(h, h->lay.leaf);
-  A.count = at<int32_t>(h, h->lay.count);
-  A.prop = at<Prop>(h, h->lay.prop);
-  A.z = at<double>(h, h->lay.z);
+  A.axis = atc<uint16_t>(h, ch, h->lay.axis);
+  A.cut = atc<uint8_t>(h, ch, h->lay.cut);
+  A.leaf = atc<float>(h, ch, h->lay.leaf);
+  A.count = atc<int32_t>(h, ch, h->lay.count);
+  A.prop = atc<Prop>(h, ch, h->lay.prop);
+  A.z = atc<double>(h, ch, h->lay.z);
   A.n_cuts = at<int32_t>(h, h->lay.n_cuts);
   A.nz_list = at<int32_t>(h, h->lay.nz_list);
   A.nz_rank = at<int32_t>(h, h->lay.nz_rank);
-  A.ctl = at<Ctl>(h, h->lay.ctl);
-  A.pub = at<uint64_t>(h, h->lay.pub);
+  A.ctl = atc<Ctl>(h, ch, h->lay.ctl);
+  A.pub = atc<uint64_t>(h, ch, h->lay.pub);
+  A.chain = ch;
   A.n = c.n;
   A.p = c.p;
   A.m = c.ntree;
@@ -284,22 +323,24 @@ SweepArgs make_args(bart_handle *h) {
   return A;
 }
 
-int launch_sweep(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace) {
+int launch_sweep(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace,
+                 int64_t trace_stride) {
   HIP_TRY(hipSetDevice(h->device));
   // mailbox words carry launch-relative step numbers: clear both buffers
-  const int64_t words = 2 * (int64_t)kMaxGrid * kStride;
-  k_clear_words<<<grid_for(words, 256), 256, 0, h->stream>>>(at<uint64_t>(h, h->lay.pub),
-                                                               words);
+  const int64_t words = 2 * (int64_t)h->G * kStride;
+  k_clear_mailboxes<<<dim3(grid_for(words, 256), h->nchain), 256, 0, h->stream>>>(
+      h->ws, h->lay.pub, h->lay.chain_bytes, words);
   HIP_TRY(hipGetLastError());
   const SweepArgs *A = at<SweepArgs>(h, h->lay.args);
-  Launch Lc{h->sweep, h->next, n_steps, seed, trace};
+  Launch Lc{h->sweep, h->next, n_steps, seed, trace, trace_stride};
   void *args[] = {&A, &Lc};
   // the grid holds at most one workgroup per compute unit (checked at init)
+  const dim3 grid(h->G * h->nchain);
   if (h->cfg.launch == BART_LAUNCH_COOPERATIVE)
-    HIP_TRY(hipLaunchCooperativeKernel((const void *)h->fn, dim3(h->G), dim3(kBlock), args, 0,
+    HIP_TRY(hipLaunchCooperativeKernel((const void *)h->fn, grid, dim3(kBlock), args, 0,
                                        h->stream));
   else
-    HIP_TRY(hipLaunchKernel((const void *)h->fn, dim3(h->G), dim3(kBlock), args, 0, h->stream));
+    HIP_TRY(hipLaunchKernel((const void *)h->fn, grid, dim3(kBlock), args, 0, h->stream));
   return BART_OK;
 }
 
@@ -316,7 +357,7 @@ int run_steps(bart_handle *h, int64_t steps, uint64_t seed, bart_trace *trace) {
   int64_t done = 0;
   while (done < steps) {
     const int32_t k = (int32_t)std::min<int64_t>(steps - done, kMaxLaunchSteps);
-    const int rc = launch_sweep(h, k, seed, trace ? trace + done : nullptr);
+    const int rc = launch_sweep(h, k, seed, trace ? trace + done : nullptr, steps);
     if (rc) return rc;
     advance(h, k);
     done += k;
@@ -360,11 +401,17 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
   hipDeviceProp_t prop;
   HIP_TRY(hipGetDeviceProperties(&prop, device));
   // launch shape: one workgroup per CU at most, every workgroup owns a slice
-  // of the observations.  Residuals in registers: the fewest chunks of 4
-  // observations per thread (V) that fit; streamed from HBM otherwise.
-  const int gmax = std::min(prop.multiProcessorCount, kMaxGrid);
+  // of the observations of its chain.  Residuals in registers: the fewest
+  // chunks of 4 observations per thread (V) that fit; streamed from HBM
+  // otherwise.
+  const int nchain = lay.nchain;
+  const int gmax = std::min(prop.multiProcessorCount, kMaxGrid) / nchain;
+  if (gmax < 1)
+    return fail(BART_ENOTSUP, "nchain=%d exceeds the %d compute units", nchain,
+                prop.multiProcessorCount);
   if (cfg->grid > gmax)
-    return fail(BART_ENOTSUP, "grid=%d exceeds the %d compute units", cfg->grid, gmax);
+    return fail(BART_ENOTSUP, "grid=%d x nchain=%d exceeds the %d compute units", cfg->grid,
+                nchain, prop.multiProcessorCount);
   int V = 0, G = 0;
   if (cfg->residency != BART_RESID_STREAMED) {
     for (int v : kVs) {
@@ -406,6 +453,7 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
   h->V = cpt;
   h->streamed = streamed;
   h->G = G;
+  h->nchain = nchain;
   h->lds = (int)fa.sharedSizeBytes;
   h->chunks = chunks;
   h->sweep = 0;
@@ -425,18 +473,22 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
                            hipMemcpyHostToDevice, st));
     HIP_TRY(hipMemcpyAsync(at<int32_t>(h, lay.nz_rank), h->nz_rank.data(), sizeof(int32_t) * cfg->p,
                            hipMemcpyHostToDevice, st));
-    k_init_resid<<<grid_for(lay.n_pad, 256), 256, 0, st>>>(at<float>(h, lay.resid), y_c, cfg->n,
-                                                             lay.n_pad);
     const int64_t entries = (int64_t)cfg->ntree * lay.n_pad;
-    k_fill_idx<<<grid_for(entries, 256), 256, 0, st>>>(at<uint8_t>(h, lay.idx), entries,
-                                                         cfg->idx_bytes);
-    k_init_trees<<<grid_for((int64_t)cfg->ntree * 2 * h->H, 256), 256, 0, st>>>(
-        at<uint16_t>(h, lay.axis), at<uint8_t>(h, lay.cut), at<float>(h, lay.leaf),
-        at<int32_t>(h, lay.count), cfg->ntree, h->H, cfg->n);
-    k_set_ctl<<<1, 64, 0, st>>>(at<Ctl>(h, lay.ctl), cfg->sigma2_init, 0, 1);
-    HIP_TRY(hipGetLastError());
-    const SweepArgs args = make_args(h);
-    HIP_TRY(hipMemcpyAsync(at<SweepArgs>(h, lay.args), &args, sizeof args, hipMemcpyHostToDevice, st));
+    std::vector<SweepArgs> args(nchain);
+    for (int c = 0; c < nchain; ++c) {
+      k_init_resid<<<grid_for(lay.n_pad, 256), 256, 0, st>>>(atc<float>(h, c, lay.resid), y_c,
+                                                               cfg->n, lay.n_pad);
+      k_fill_idx<<<grid_for(entries, 256), 256, 0, st>>>(atc<uint8_t>(h, c, lay.idx), entries,
+                                                           cfg->idx_bytes);
+      k_init_trees<<<grid_for((int64_t)cfg->ntree * 2 * h->H, 256), 256, 0, st>>>(
+          atc<uint16_t>(h, c, lay.axis), atc<uint8_t>(h, c, lay.cut), atc<float>(h, c, lay.leaf),
+          atc<int32_t>(h, c, lay.count), cfg->ntree, h->H, cfg->n);
+      k_set_ctl<<<1, 64, 0, st>>>(atc<Ctl>(h, c, lay.ctl), cfg->sigma2_init, 0, 1);
+      HIP_TRY(hipGetLastError());
+      args[c] = make_args(h, c);
+    }
+    HIP_TRY(hipMemcpyAsync(at<SweepArgs>(h, lay.args), args.data(), sizeof(SweepArgs) * nchain,
+                           hipMemcpyHostToDevice, st));
     // the host copies of n_cuts must stay valid until the copies ran
     HIP_TRY(hipStreamSynchronize(st));
     return BART_OK;
@@ -474,9 +526,10 @@ int bart_predict(bart_handle *h, const uint8_t *Xt, int64_t xt_stride, int64_t n
   if (!Xt || !out) return fail(BART_EINVAL, "NULL pointer argument");
   if (xt_stride < n_t || xt_stride % 16) return fail(BART_EINVAL, "xt_stride must be >= n_t and a multiple of 16");
   HIP_TRY(hipSetDevice(h->device));
-  k_predict<<<grid_for(n_t, 256), 256, 0, h->stream>>>(
-      Xt, xt_stride, n_t, h->cfg.p, at<uint16_t>(h, h->lay.axis), at<uint8_t>(h, h->lay.cut),
-      at<float>(h, h->lay.leaf), h->cfg.ntree, h->cfg.max_depth, h->H, offset, out);
+  k_predict<<<dim3(grid_for(n_t, 256), h->nchain), 256, 0, h->stream>>>(
+      Xt, xt_stride, n_t, h->cfg.p, atc<uint16_t>(h, 0, h->lay.axis),
+      atc<uint8_t>(h, 0, h->lay.cut), atc<float>(h, 0, h->lay.leaf), h->cfg.ntree,
+      h->cfg.max_depth, h->H, offset, h->lay.chain_bytes, out);
   HIP_TRY(hipGetLastError());
   return BART_OK;
 }
@@ -485,24 +538,29 @@ int bart_get_state(bart_handle *h, bart_state *d) {
   if (!h || !d) return fail(BART_EINVAL, "NULL argument");
   if (!d->axis || !d->cut || !d->leaf || !d->idx || !d->resid)
     return fail(BART_EINVAL, "NULL state buffer");
+  const int ch = d->chain;
+  if (ch < 0 || ch >= h->nchain)
+    return fail(BART_EINVAL, "chain %d not in [0, %d)", ch, h->nchain);
   HIP_TRY(hipSetDevice(h->device));
   const bart_config &c = h->cfg;
   const size_t m = c.ntree, H = h->H;
   hipStream_t st = h->stream;
-  HIP_TRY(hipMemcpyAsync(d->axis, at<void>(h, h->lay.axis), 2 * m * H, hipMemcpyDeviceToDevice, st));
-  HIP_TRY(hipMemcpyAsync(d->cut, at<void>(h, h->lay.cut), m * H, hipMemcpyDeviceToDevice, st));
-  HIP_TRY(hipMemcpyAsync(d->leaf, at<void>(h, h->lay.leaf), 4 * m * 2 * H, hipMemcpyDeviceToDevice, st));
-  HIP_TRY(hipMemcpy2DAsync(d->idx, (size_t)c.n * c.idx_bytes, at<void>(h, h->lay.idx),
-                           (size_t)h->lay.n_pad * c.idx_bytes, (size_t)c.n * c.idx_bytes, m,
+  const Layout &L = h->lay;
+  HIP_TRY(hipMemcpyAsync(d->axis, atc<void>(h, ch, L.axis), 2 * m * H, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(d->cut, atc<void>(h, ch, L.cut), m * H, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(d->leaf, atc<void>(h, ch, L.leaf), 4 * m * 2 * H, hipMemcpyDeviceToDevice,
+                         st));
+  HIP_TRY(hipMemcpy2DAsync(d->idx, (size_t)c.n * c.idx_bytes, atc<void>(h, ch, L.idx),
+                           (size_t)L.n_pad * c.idx_bytes, (size_t)c.n * c.idx_bytes, m,
                            hipMemcpyDeviceToDevice, st));
-  HIP_TRY(hipMemcpyAsync(d->resid, at<void>(h, h->lay.resid), 4 * (size_t)c.n, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(d->resid, atc<void>(h, ch, L.resid), 4 * (size_t)c.n,
+                         hipMemcpyDeviceToDevice, st));
   Ctl ctl;
-  HIP_TRY(hipMemcpyAsync(&ctl, at<void>(h, h->lay.ctl), sizeof(Ctl), hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipMemcpyAsync(&ctl, atc<void>(h, ch, L.ctl), sizeof(Ctl), hipMemcpyDeviceToHost, st));
   HIP_TRY(hipStreamSynchronize(st));
   d->sigma2 = ctl.sigma2;
   d->sweep = h->sweep;
   d->next = h->next;
-  d->pad = 0;
   return BART_OK;
 }
 
@@ -511,24 +569,32 @@ int bart_set_state(bart_handle *h, const bart_state *s) {
   if (!s->axis || !s->cut || !s->leaf || !s->idx || !s->resid)
     return fail(BART_EINVAL, "NULL state buffer");
   const bart_config &c = h->cfg;
+  const int ch = s->chain;
+  if (ch < 0 || ch >= h->nchain)
+    return fail(BART_EINVAL, "chain %d not in [0, %d)", ch, h->nchain);
   if (!(s->sigma2 > 0.0 && std::isfinite(s->sigma2))) return fail(BART_EINVAL, "sigma2 must be > 0");
   if (s->sweep < 0 || s->next < 0 || s->next > c.ntree) return fail(BART_EINVAL, "bad position");
   HIP_TRY(hipSetDevice(h->device));
   const size_t m = c.ntree, H = h->H;
   hipStream_t st = h->stream;
-  HIP_TRY(hipMemcpyAsync(at<void>(h, h->lay.axis), s->axis, 2 * m * H, hipMemcpyDeviceToDevice, st));
-  HIP_TRY(hipMemcpyAsync(at<void>(h, h->lay.cut), s->cut, m * H, hipMemcpyDeviceToDevice, st));
-  HIP_TRY(hipMemcpyAsync(at<void>(h, h->lay.leaf), s->leaf, 4 * m * 2 * H, hipMemcpyDeviceToDevice, st));
-  HIP_TRY(hipMemcpy2DAsync(at<void>(h, h->lay.idx), (size_t)h->lay.n_pad * c.idx_bytes, s->idx,
+  const Layout &L = h->lay;
+  HIP_TRY(hipMemcpyAsync(atc<void>(h, ch, L.axis), s->axis, 2 * m * H, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(atc<void>(h, ch, L.cut), s->cut, m * H, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(atc<void>(h, ch, L.leaf), s->leaf, 4 * m * 2 * H, hipMemcpyDeviceToDevice,
+                         st));
+  HIP_TRY(hipMemcpy2DAsync(atc<void>(h, ch, L.idx), (size_t)L.n_pad * c.idx_bytes, s->idx,
                            (size_t)c.n * c.idx_bytes, (size_t)c.n * c.idx_bytes, m,
                            hipMemcpyDeviceToDevice, st));
-  HIP_TRY(hipMemcpyAsync(at<void>(h, h->lay.resid), s->resid, 4 * (size_t)c.n, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipMemcpyAsync(atc<void>(h, ch, L.resid), s->resid, 4 * (size_t)c.n,
+                         hipMemcpyDeviceToDevice, st));
   const int64_t cells = (int64_t)m * 2 * H;
-  k_zero_i32<<<grid_for(cells, 256), 256, 0, st>>>(at<int32_t>(h, h->lay.count), cells);
+  k_zero_i32<<<grid_for(cells, 256), 256, 0, st>>>(atc<int32_t>(h, ch, L.count), cells);
   dim3 g(std::min<int64_t>(((int64_t)c.n + 1023) / 1024, 64), (unsigned)m);
-  k_recount<<<g, 1024, 0, st>>>(at<uint8_t>(h, h->lay.idx), h->lay.n_pad, c.idx_bytes,
-                                at<int32_t>(h, h->lay.count), c.n, h->H);
-  k_set_ctl<<<1, 64, 0, st>>>(at<Ctl>(h, h->lay.ctl), s->sigma2, s->sweep, 0);
+  k_recount<<<g, 1024, 0, st>>>(atc<uint8_t>(h, ch, L.idx), L.n_pad, c.idx_bytes,
+                                atc<int32_t>(h, ch, L.count), c.n, h->H);
+  // the position is shared by all chains
+  for (int k = 0; k < h->nchain; ++k)
+    k_set_ctl<<<1, 64, 0, st>>>(atc<Ctl>(h, k, L.ctl), k == ch ? s->sigma2 : -1.0, s->sweep, 0);
   HIP_TRY(hipGetLastError());
   h->sweep = s->sweep;
   h->next = s->next;
@@ -538,11 +604,15 @@ int bart_set_state(bart_handle *h, const bart_state *s) {
 int bart_status(bart_handle *h, uint32_t *bits) {
   if (!h) return fail(BART_EINVAL, "handle is NULL");
   HIP_TRY(hipSetDevice(h->device));
-  Ctl ctl;
-  HIP_TRY(hipMemcpyAsync(&ctl, at<void>(h, h->lay.ctl), sizeof(Ctl), hipMemcpyDeviceToHost, h->stream));
+  std::vector<Ctl> ctl(h->nchain);
+  for (int c = 0; c < h->nchain; ++c)
+    HIP_TRY(hipMemcpyAsync(&ctl[c], atc<void>(h, c, h->lay.ctl), sizeof(Ctl),
+                           hipMemcpyDeviceToHost, h->stream));
   HIP_TRY(hipStreamSynchronize(h->stream));
-  if (bits) *bits = ctl.error;
-  if (ctl.error) return fail(BART_EDEVICE, "device error bits 0x%x", ctl.error);
+  uint32_t err = 0;
+  for (const Ctl &x : ctl) err |= x.error;
+  if (bits) *bits = err;
+  if (err) return fail(BART_EDEVICE, "device error bits 0x%x", err);
   return BART_OK;
 }
 
@@ -557,6 +627,7 @@ int bart_launch_info(const bart_handle *h, bart_launch *o) {
   o->obs_per_thread = 4 * h->V;
   o->max_leaves = std::min(h->H, kMaxLeaves);
   o->launch = h->cfg.launch;
+  o->nchain = h->nchain;
   return BART_OK;
 }
 

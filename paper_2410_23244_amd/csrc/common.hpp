@@ -49,6 +49,10 @@ struct Ctl {
   uint64_t stats[6];  // GROW proposed, PRUNE proposed, GROW accepted, PRUNE accepted, tree steps, leaves
 };
 
+// Arguments of one chain.  A launch covers nchain chains with G workgroups
+// each; workgroup b serves chain b / G, whose arguments are entry b / G of
+// the array the kernel receives.  Per-chain buffers are disjoint; X, n_cuts,
+// nz_list and nz_rank are shared.
 struct SweepArgs {
   const uint8_t *X;
   int64_t ldx;
@@ -65,10 +69,10 @@ struct SweepArgs {
   const int32_t *nz_list;
   const int32_t *nz_rank;
   Ctl *ctl;
-  uint64_t *pub;     // [2][kMaxGrid][kStride] mailboxes, by step parity
+  uint64_t *pub;     // [2][G][kStride] mailboxes, by step parity
   int32_t n, p, m, D, H, p_nz, G, chunks;
-  int32_t cpt;  // chunks of 4 observations per thread
-  int32_t pad_;
+  int32_t cpt;    // chunks of 4 observations per thread
+  int32_t chain;  // index of this chain in the launch
   double alpha, beta, mu_mu, sigma_mu, nu, lambda, p_grow;
 };
 
@@ -78,7 +82,13 @@ struct Launch {
   int32_t j0;         // first step inside that sweep (0..m-1 trees, m = sigma^2)
   int32_t n_steps;
   uint64_t seed;
-  bart_trace *trace;  // NULL: no trace
+  bart_trace *trace;  // NULL: no trace; else [nchain][trace_stride] records
+  int64_t trace_stride;
 };
+
+// Index of the calling workgroup among the G workgroups of its chain.
+__device__ __forceinline__ int wg_id(const SweepArgs *__restrict__ A) {
+  return (int)blockIdx.x - A->chain * A->G;
+}
 
 }  // namespace bart

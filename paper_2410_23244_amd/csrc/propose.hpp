@@ -85,7 +85,7 @@ __device__ inline double prob_grow(const SweepArgs *__restrict__ A, int nG, int 
 }
 
 // Proposal for tree j in sweep s from its current structure.
-__device__ __noinline__ void propose_tree(const SweepArgs *__restrict__ A, uint64_t seed, int j,
+__device__ __noinline__ void propose_tree(const SweepArgs *__restrict__ A, Key key, int j,
                                           int64_t s, Prop &P) {
   const int H = A->H;
   const uint16_t *ax = A->axis + (int64_t)j * H;
@@ -112,7 +112,7 @@ __device__ __noinline__ void propose_tree(const SweepArgs *__restrict__ A, uint6
     }
   }
 
-  const Block b = draw(seed, (uint64_t)s, (uint64_t)j, 0, 0);
+  const Block b = draw(key, (uint64_t)s, (uint64_t)j, 0, 0);
   int move = kNone, eta = 0, a = 0, cut = 0;
   if (nG > 0 || nP > 0) {
     move = unit(b.w0) < prob_grow(A, nG, nP) ? kGrow : kPrune;

@@ -187,7 +187,10 @@ __device__ __forceinline__ void build_ranks(const SweepArgs *__restrict__ A, Ctx
     if (h < 2 * A->H && ((c.pr.mask[h >> 6] >> (h & 63)) & 1ull)) {
       int k = 0;
       for (int u = 0; u < (h >> 6); ++u) k += __popcll(c.pr.mask[u]);
-      if (h & 63) k += __popcll(c.pr.mask[h >> 6] & ((1ull << (h & 63)) - 1ull));
+      // leaves below h in its 64-slot word: h & 63 is this thread's lane
+      const uint64_t mw = c.pr.mask[h >> 6];
+      k += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mw >> 32),
+                                          __builtin_amdgcn_mbcnt_lo((uint32_t)mw, 0u));
       r = (uint8_t)k;
       c.heap_of[k] = (uint16_t)h;
     }
@@ -236,13 +239,14 @@ __device__ __forceinline__ void store_tree_data(TreeData &td, const Ctx &c, cons
 // heap slots); each Philox block gives the normals of slots 2u and 2u+1.
 __device__ __noinline__ void gen_normals(const SweepArgs *__restrict__ A, uint64_t seed, int64_t s,
                                          int j0) {
+  const Key key = chain_key(seed, A->chain);
   const int H = A->H;
   double *zb = A->z + (int64_t)(s & 1) * A->m * 2 * H;
   const int64_t gsz = (int64_t)A->G * kBlock;
-  for (int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x; q < (int64_t)A->m * H; q += gsz) {
+  for (int64_t q = (int64_t)wg_id(A) * kBlock + threadIdx.x; q < (int64_t)A->m * H; q += gsz) {
     const int tr = (int)(q / H), u = (int)(q % H);
     if (tr < j0) continue;
-    const Block bl = draw(seed, (uint64_t)s, (uint64_t)tr, 1, (uint64_t)u);
+    const Block bl = draw(key, (uint64_t)s, (uint64_t)tr, 1, (uint64_t)u);
     zb[(int64_t)tr * 2 * H + 2 * u] = gauss(bl.w0, bl.w1);
     zb[(int64_t)tr * 2 * H + 2 * u + 1] = gauss(bl.w2, bl.w3);
   }
@@ -252,22 +256,24 @@ __device__ __noinline__ void gen_normals(const SweepArgs *__restrict__ A, uint64
 // owned by workgroup j mod G), one thread per tree.
 __device__ __noinline__ void gen_proposals(const SweepArgs *__restrict__ A, uint64_t seed, int64_t s,
                                            int j0) {
-  for (int tr = (int)blockIdx.x + A->G * (int)threadIdx.x; tr < A->m; tr += A->G * kBlock)
-    if (tr >= j0) propose_tree(A, seed, tr, s, A->prop[tr]);
+  const Key key = chain_key(seed, A->chain);
+  for (int tr = wg_id(A) + A->G * (int)threadIdx.x; tr < A->m; tr += A->G * kBlock)
+    if (tr >= j0) propose_tree(A, key, tr, s, A->prop[tr]);
 }
 
 // sigma^2 | rest ~ InvGamma((nu+n)/2, (nu lambda + SSR)/2), the conjugate
 // update of the prior lambda nu / sigma^2 ~ chi^2_nu (eq. bartdef).
 __device__ __noinline__ double draw_sigma2(const SweepArgs *__restrict__ A, uint64_t seed, int64_t s,
                                            double ssr) {
+  const Key key = chain_key(seed, A->chain);
   const double shape = 0.5 * (A->nu + (double)A->n);
   const double scale = 0.5 * (A->nu * A->lambda + ssr);
-  return scale / gamma_mt(seed, (uint64_t)s, shape);
+  return scale / gamma_mt(key, (uint64_t)s, shape);
 }
 
 // Post words 0..K-1 (this workgroup's mailbox in buffer par).
 __device__ __forceinline__ uint64_t *mailbox(const SweepArgs *__restrict__ A, int par, int g) {
-  return A->pub + ((int64_t)par * kMaxGrid + g) * kStride;
+  return A->pub + ((int64_t)par * A->G + g) * kStride;
 }
 
 // Poll word k < K of every mailbox of buffer par until all carry step number
@@ -289,7 +295,7 @@ __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH 
   if (t < nseg * K) {
     const int k = t % K, seg = t / K;
     const int g0 = seg * span, g1 = min(G, g0 + span);
-    const uint64_t *base = A->pub + (int64_t)par * kMaxGrid * kStride + k;
+    const uint64_t *base = A->pub + (int64_t)par * A->G * kStride + k;
     double acc = 0.0;
 #pragma unroll 1
     for (int gb = g0; gb < g1; gb += 8) {
@@ -471,7 +477,7 @@ __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Sha
 __device__ __forceinline__ void finish_tree(const SweepArgs *__restrict__ A, const Launch &Lc,
                                             Shared &sh, const Ctx &c, int j, int64_t s,
                                             int step) {
-  const int t = threadIdx.x, w = blockIdx.x, G = A->G, H = A->H;
+  const int t = threadIdx.x, w = wg_id(A), G = A->G, H = A->H;
   const int move = c.pr.move, eta = c.pr.eta, L = c.pr.L;
   const int kl = c.pr.rank_l, kr = c.pr.rank_r;
   const int acc = sh.flags & 1, merged = (sh.flags >> 1) & 1;
@@ -518,7 +524,7 @@ template <class SH>
 __device__ __forceinline__ void sigma2_tail(const SweepArgs *__restrict__ A, const Launch &Lc,
                                             SH &sh, int64_t s, int step, uint32_t seq,
                                             int par) {
-  const int t = threadIdx.x, w = blockIdx.x, m = A->m;
+  const int t = threadIdx.x, w = wg_id(A), m = A->m;
   const uint64_t seed = Lc.seed;
   const bool tracing = Lc.trace != nullptr;
   // the next sweep's proposals (owners) and normals, published by the
@@ -576,7 +582,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
                                            Shared &sh) {
   using IC = IdxChunk<IB>;
   using ChunkT = typename IC::T;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, w = blockIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, w = wg_id(A);
   const int G = A->G, H = A->H, m = A->m;
   const uint64_t seed = Lc.seed;
   const bool tracing = Lc.trace != nullptr;
@@ -896,7 +902,9 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
 template <int V, int IB>
 __global__ void __launch_bounds__(kBlock) sweep_kernel(const SweepArgs *__restrict__ A, Launch Lc) {
   __shared__ Shared sh;
-  sweep_body<V, IB>(A, Lc, sh);
+  const int c = (int)blockIdx.x / A->G;
+  if (Lc.trace) Lc.trace += c * Lc.trace_stride;
+  sweep_body<V, IB>(A + c, Lc, sh);
 }
 
 // ------------------------------------------------------------------ streamed
@@ -916,7 +924,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   using IC = IdxChunk<IB>;
   using ChunkT = typename IC::T;
   constexpr int U = 4;  // chunks of 4 points in flight per thread
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, w = blockIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, w = wg_id(A);
   const int m = A->m, cpt = A->cpt;
   const uint64_t seed = Lc.seed;
   for (int k = t; k < kBinFloats; k += kBlock) sh.bins[k] = 0.f;
@@ -1177,7 +1185,9 @@ template <int IB>
 __global__ void __launch_bounds__(kBlock) sweep_kernel_stream(const SweepArgs *__restrict__ A,
                                                               Launch Lc) {
   __shared__ Shared sh;
-  sweep_body_stream<IB>(A, Lc, sh);
+  const int c = (int)blockIdx.x / A->G;
+  if (Lc.trace) Lc.trace += c * Lc.trace_stride;
+  sweep_body_stream<IB>(A + c, Lc, sh);
 }
 
 }  // namespace bart

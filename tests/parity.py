@@ -42,15 +42,17 @@ class Report:
     notes: list = field(default_factory=list)
 
 
-def oracle_config(inp, fix_sigma2=False):
+def oracle_config(inp, fix_sigma2=False, chain=0):
     h = inp.hyper
     return oracle.make_config(n=inp.n, p=inp.p, m=inp.m, D=inp.D, idx_bytes=inp.idx_bytes,
                               alpha=h.alpha, beta=h.beta, mu_mu=h.mu_mu, sigma_mu=h.sigma_mu,
-                              nu=h.nu, lam=h.lam, p_grow=h.p_grow, fix_sigma2=fix_sigma2)
+                              nu=h.nu, lam=h.lam, p_grow=h.p_grow, fix_sigma2=fix_sigma2,
+                              chain=chain)
 
 
-def chain_from_state(inp, st) -> oracle.Chain:
-    ch = oracle.Chain(oracle_config(inp), inp.X_b, inp.n_cuts, inp.y_c, st["sigma2"])
+def chain_from_state(inp, st, chain=0) -> oracle.Chain:
+    ch = oracle.Chain(oracle_config(inp, chain=chain), inp.X_b, inp.n_cuts, inp.y_c,
+                      st["sigma2"])
     ch.load(st["axis"], st["cut"], st["leaf"], st["idx"], st["resid"], st["sigma2"],
             st["sweep"], st["next"])
     return ch
@@ -159,13 +161,23 @@ def compare_states(inp, gst: dict, ch: oracle.Chain, rep: Report):
 
 def lockstep(inp, gpu, seed: int, warm_sweeps: int, n_steps: int) -> Report:
     """Warm the device chain, then run n_steps in lockstep with the oracle."""
+    return lockstep_chains(inp, gpu, seed, warm_sweeps, n_steps)[0]
+
+
+def lockstep_chains(inp, gpu, seed: int, warm_sweeps: int, n_steps: int) -> list:
+    """lockstep for every chain of the handle: chain c against an oracle chain
+    drawing from stream c."""
+    C = gpu.nchain
     if warm_sweeps:
         gpu.step(warm_sweeps, seed)
-    st = gpu.get_state()
+    chs = [chain_from_state(inp, gpu.get_state(c), chain=c) for c in range(C)]
     assert gpu.status() == 0
-    ch = chain_from_state(inp, st)
     trg = gpu.debug_steps(n_steps, seed)
     assert gpu.status() == 0
-    rep = compare_steps(inp, ch, trg, seed, Report())
-    compare_states(inp, gpu.get_state(), ch, rep)
-    return rep
+    trg = trg.reshape(C, n_steps)
+    reps = []
+    for c in range(C):
+        rep = compare_steps(inp, chs[c], trg[c], seed, Report())
+        compare_states(inp, gpu.get_state(c), chs[c], rep)
+        reps.append(rep)
+    return reps

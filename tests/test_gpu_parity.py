@@ -18,10 +18,10 @@ COOP, ORDINARY = 0, 1  # BART_LAUNCH_COOPERATIVE, BART_LAUNCH_ORDINARY
 AUTO, REGS, STREAM = 0, 1, 2  # BART_RESID_AUTO, BART_RESID_REGISTERS, BART_RESID_STREAMED
 
 
-def _gpu(inp, grid=0, launch=COOP, residency=AUTO):
+def _gpu(inp, grid=0, launch=COOP, residency=AUTO, nchain=1):
     from paper_2410_23244_amd.bart import from_inputs
 
-    return from_inputs(inp, grid=grid, launch=launch, residency=residency)
+    return from_inputs(inp, grid=grid, launch=launch, residency=residency, nchain=nchain)
 
 
 CASES = {
@@ -190,3 +190,56 @@ def test_lockstep_full_size_streamed():
     assert g.launch_info().residency == STREAM
     rep = parity.lockstep(inp, g, seed=inp.seed, warm_sweeps=20, n_steps=inp.m + 1)
     print(f"  {rep}", flush=True)
+
+
+# ---------------------------------------------------------------- several chains
+
+@pytest.mark.parametrize("nchain,grid,residency,launch",
+                         [(3, 0, REGS, COOP), (4, 5, REGS, ORDINARY), (3, 4, STREAM, COOP)])
+def test_chains_lockstep(nchain, grid, residency, launch):
+    inp = make_inputs(2, n=20011, p=30, m=30)
+    print(f"chains={nchain} grid={grid} residency={residency} launch={launch}", flush=True)
+    g = _gpu(inp, grid=grid, launch=launch, residency=residency, nchain=nchain)
+    info = g.launch_info()
+    assert info.nchain == nchain and info.residency == residency
+    reps = parity.lockstep_chains(inp, g, seed=21, warm_sweeps=2, n_steps=31 * 2)
+    for rep in reps:
+        print(f"  {rep}", flush=True)
+        assert rep.tree_steps > 0 and rep.moves > 0
+    # different streams: the chains' trees differ
+    states = [g.get_state(c) for c in range(nchain)]
+    assert not np.array_equal(states[0]["leaf"], states[1]["leaf"])
+
+
+def test_chain0_equals_a_lone_chain():
+    inp = make_inputs(2, n=30011, p=16, m=20)
+    many = _gpu(inp, grid=6, nchain=5)
+    one = _gpu(inp, grid=6)
+    assert many.launch_info().chunks_per_thread == one.launch_info().chunks_per_thread
+    many.step(4, 13)
+    one.step(4, 13)
+    sa, sb = many.get_state(0), one.get_state()
+    for k in ["axis", "cut", "leaf", "idx", "resid"]:
+        np.testing.assert_array_equal(sa[k], sb[k], err_msg=k)
+    assert sa["sigma2"] == sb["sigma2"]
+    assert many.status() == 0 and one.status() == 0
+
+
+def test_chains_predict_and_set_state():
+    inp = make_inputs(1, n=3001, p=10, m=30)
+    g = _gpu(inp, nchain=3)
+    g.step(4, 7)
+    Xt = make_inputs(1, n=1999, p=10, m=30).X_b
+    got = g.predict(Xt, inp.offset).cpu().numpy()
+    assert got.shape == (3, 1999)
+    for c in range(3):
+        ch = parity.chain_from_state(inp, g.get_state(c), chain=c)
+        np.testing.assert_array_equal(got[c], ch.predict(Xt, inp.offset))
+    # set chain 1 to chain 2's state: from then on the two differ only by stream
+    st2 = g.get_state(2)
+    g.set_state(st2, chain=1)
+    s1 = g.get_state(1)
+    for k in ["axis", "cut", "leaf", "idx", "resid"]:
+        np.testing.assert_array_equal(s1[k], st2[k], err_msg=k)
+    assert s1["sigma2"] == st2["sigma2"]
+    assert g.status() == 0

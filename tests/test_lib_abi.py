@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(b):
 
 def _cfg(b, **kw):
     base = dict(n=1000, p=4, ntree=10, max_depth=6, idx_bytes=1, grid=0, launch=0,
-                residency=0, x_stride=1024,
+                residency=0, nchain=1, reserved=0, x_stride=1024,
                 alpha=0.95, beta=2.0, mu_mu=0.0, sigma_mu=0.1, nu=3.0, lam=0.5,
                 sigma2_init=1.0, p_grow=0.5)
     base.update(kw)
@@ -51,7 +51,8 @@ def _cfg(b, **kw):
                                  dict(alpha=1.5), dict(sigma_mu=0.0), dict(nu=-1.0),
                                  dict(p_grow=2.0), dict(grid=300), dict(grid=-1), dict(lam=float("nan")),
                                  dict(launch=2), dict(launch=-1), dict(residency=3),
-                                 dict(residency=-1)])
+                                 dict(residency=-1), dict(nchain=-1), dict(nchain=257),
+                                 dict(nchain=3, grid=100)])
 def test_invalid_configs_are_rejected(b, bad):
     cfg = _cfg(b, **bad)
     assert b.bart_workspace_bytes(cfg) == 0
@@ -80,6 +81,15 @@ def test_workspace_size_and_alignment_checks(b):
                        C.byref(h)) == b.BART_EINVAL
     assert L.bart_init(C.byref(cfg), 0, 4096, nc.ctypes.data, 4096, need, None,
                        C.byref(h)) == b.BART_EINVAL
+
+
+def test_workspace_grows_with_chains(b):
+    one = b.bart_workspace_bytes(_cfg(b, nchain=1))
+    assert b.bart_workspace_bytes(_cfg(b, nchain=0)) == one  # 0 means one chain
+    four = b.bart_workspace_bytes(_cfg(b, nchain=4))
+    # every chain has its own residuals, index cache and trees
+    assert four >= 4 * (1000 * 4 + 10 * 1024 + 10 * 32 * 3)
+    assert four > one
 
 
 def test_null_handle_calls_fail_cleanly(b):

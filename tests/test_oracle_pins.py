@@ -471,3 +471,64 @@ def test_steps_compose_and_are_deterministic():
     for name in ["axis", "cut", "leaf", "idx", "resid"]:
         np.testing.assert_array_equal(getattr(a, name), getattr(b, name))
     assert a.sigma2 == b.sigma2 and a.sweep == b.sweep == 5
+
+
+def _numpy_philox_block(seed, ctr):
+    prev = list(ctr)
+    for k in range(4):
+        prev[k] = (prev[k] - 1) % 2**64
+        if ctr[k] != 0:
+            break
+    bg = np.random.Philox(key=np.array([seed, KEY_TAG], np.uint64),
+                          counter=np.array(prev, np.uint64))
+    return [int(w) for w in bg.random_raw(4)]
+
+
+@pytest.mark.parametrize("chain", [0, 1, 37])
+def test_chain_streams_offset_the_last_counter_word(chain):
+    """Chain c draws block (s, j, q, c 2^32 + t): its accept uniform and leaf
+    normals at sweep 0, tree 0 follow from numpy's Philox at that counter."""
+    from paper_2410_23244_amd.inputs import make_inputs
+
+    inp = make_inputs(1, n=300, p=6, m=3)
+    h = inp.hyper
+    seed = 9
+    cfg = oracle.make_config(n=inp.n, p=inp.p, m=inp.m, D=inp.D, alpha=h.alpha, beta=h.beta,
+                             mu_mu=h.mu_mu, sigma_mu=h.sigma_mu, nu=h.nu, lam=h.lam,
+                             chain=chain)
+    ch = oracle.Chain(cfg, inp.X_b, inp.n_cuts, inp.y_c, h.sigma2_init)
+    tr = ch.step(seed)
+    u01 = lambda w: ((w >> 12) + 0.5) * 2.0**-52
+    w = _numpy_philox_block(seed, (0, 0, 0, chain << 32))
+    assert tr["move"] == 1 and tr["eta"] == 1          # a root-only tree can only grow
+    assert tr["ln_u"] == math.log(u01(w[3]))
+    leaves = [2, 3] if tr["accept"] else [1]
+    s2, sm2 = h.sigma2_init, h.sigma_mu ** 2
+    for leaf in leaves:
+        b = _numpy_philox_block(seed, (0, 0, 1, (chain << 32) + (leaf >> 1)))
+        a, c = (b[2], b[3]) if leaf & 1 else (b[0], b[1])
+        z = math.sqrt(-2.0 * math.log(u01(a))) * math.cos(2.0 * math.pi * u01(c))
+        n_h = float(tr["count"][2] + tr["count"][3]) if leaf == 1 else float(tr["count"][leaf])
+        S_h = float(tr["sum"][2] + tr["sum"][3]) if leaf == 1 else float(tr["sum"][leaf])
+        prec = n_h / s2 + 1.0 / sm2
+        want = (S_h / s2 + h.mu_mu / sm2) / prec + z / math.sqrt(prec)
+        assert abs(tr["leaf_new"][leaf] - want) <= 1e-6 * (abs(want) + 1.0 / math.sqrt(prec))
+
+
+def test_chains_are_independent_streams():
+    from paper_2410_23244_amd.inputs import make_inputs
+
+    inp = make_inputs(1, n=300, p=6, m=5)
+    h = inp.hyper
+    out = []
+    for chain in [0, 1, 2]:
+        cfg = oracle.make_config(n=inp.n, p=inp.p, m=inp.m, D=inp.D, alpha=h.alpha,
+                                 beta=h.beta, mu_mu=h.mu_mu, sigma_mu=h.sigma_mu, nu=h.nu,
+                                 lam=h.lam, chain=chain)
+        ch = oracle.Chain(cfg, inp.X_b, inp.n_cuts, inp.y_c, h.sigma2_init)
+        tr = ch.run(4, 3 * (inp.m + 1), trace=True)
+        out.append((tr["ln_u"].copy(), ch.sigma2))
+    for a in range(3):
+        for b in range(a + 1, 3):
+            assert not np.array_equal(out[a][0], out[b][0])
+            assert out[a][1] != out[b][1]
