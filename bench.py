@@ -8,6 +8,10 @@ and timed sweeps run as bart_step calls of --sweeps-per-launch sweeps each
 the chain's stream, and the whole timed region by device synchronisations.
 Prints one JSON line.
 
+--chains C runs C independent chains in the same launches (multi-chain
+batching); value is then the chain-sweeps per second summed over the chains
+and the roofline counts every chain's bytes.
+
 Roofline: the algorithmic bytes of a tree step are (9 + 2 s_idx) per
 observation (read the index row and the predictor row, read and write the
 residual, write the index row) plus 4 bytes per observation per sweep for
@@ -115,6 +119,8 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=3, help="workload number (3 = headline)")
     ap.add_argument("--cpu-sweeps", type=int, default=20, help="oracle sweeps (0 = skip)")
     ap.add_argument("--seed", type=int, default=3)
+    ap.add_argument("--chains", type=int, default=1, help="independent chains per launch")
+    ap.add_argument("--grid", type=int, default=0, help="workgroups per chain (0 = automatic)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (read MIB, write MIB) three "
                          "times, to calibrate HBM byte counters, and exit")
@@ -144,8 +150,11 @@ def main() -> int:
     print(f"[bench] inputs {inp.workload} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
           flush=True)
     mode = BART_LAUNCH_ORDINARY if args.launch == "ordinary" else BART_LAUNCH_COOPERATIVE
-    g = from_inputs(inp, launch=mode)
+    C = args.chains
+    g = from_inputs(inp, launch=mode, nchain=C, grid=args.grid)
     info = g.launch_info()
+    kernel = (f"bart::sweep_kernel_stream<{inp.idx_bytes}>" if info.residency == 2 else
+              f"bart::sweep_kernel<{info.chunks_per_thread}, {inp.idx_bytes}>")
     stream = g.stream
     for _ in range(args.warmup // S):
         g.step(S, args.seed)
@@ -167,8 +176,8 @@ def main() -> int:
     ms = ev[0].elapsed_time(ev[-1])
     launch_ms = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(L)]
     avg_launch = sum(launch_ms) / L
-    sweeps_per_s = args.steps / (ms / 1e3)
-    per_sweep = model_bytes_per_sweep(inp.n, inp.m, inp.idx_bytes)
+    sweeps_per_s = C * args.steps / (ms / 1e3)
+    per_sweep = C * model_bytes_per_sweep(inp.n, inp.m, inp.idx_bytes)
     achieved = per_sweep * S / (avg_launch / 1e3) / 1e9
     print(f"[bench] {args.steps} sweeps in {L} launches: events {ms:.1f} ms, wall "
           f"{wall * 1e3:.1f} ms, per launch {min(launch_ms):.2f}..{max(launch_ms):.2f} ms",
@@ -180,8 +189,13 @@ def main() -> int:
         cpu = cpu_baseline(inp, st, args.seed, args.cpu_sweeps)
         print(f"[bench] oracle {cpu['value']:.3f} sweeps/s", file=sys.stderr, flush=True)
 
+    metric = METRIC
+    if args.config != 3 or C > 1:
+        metric = (f"full MCMC sweeps/sec (all trees) at n={inp.n},p={inp.p},ntree={inp.m},"
+                  f"D={inp.D}" + (f", summed over {C} chains" if C > 1 else "") +
+                  "; achieved HBM GB/s")
     line = {
-        "metric": METRIC,
+        "metric": metric,
         "value": sweeps_per_s,
         "unit": "sweeps/s",
         "n_gpus": 1,
@@ -195,12 +209,13 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": inp.workload, "n": inp.n, "p": inp.p, "ntree": inp.m,
                    "max_depth": inp.D, "idx_bytes": inp.idx_bytes, "sweeps_per_launch": S,
-                   "launch": args.launch, "grid": info.grid,
+                   "launch": args.launch, "grid": info.grid, "nchain": C,
+                   "residency": "streamed" if info.residency == 2 else "registers",
                    "chunks_per_thread": info.chunks_per_thread, "parallelism": "1 GPU"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": stored_traffic(inp.workload, S),
-                     "kernel": "bart::sweep_kernel<1, 1>", "avg_launch_ms": avg_launch,
+                     "traffic": stored_traffic(inp.workload, S) if C == 1 else None,
+                     "kernel": kernel, "avg_launch_ms": avg_launch,
                      "algorithmic_bytes_per_launch": per_sweep * S},
         "cpu_baseline": cpu,
     }
