@@ -101,9 +101,12 @@ def stored_traffic(workload: str, sweeps_per_launch: int):
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_src_sha256") != kernel_source_digest() or rec.get("workload") != workload:
+    if rec.get("kernel_src_sha256") != kernel_source_digest():
         return None
-    return (rec["fetch_bytes_per_sweep"] + rec["write_bytes_per_sweep"]) * sweeps_per_launch
+    for r in rec.get("records", []):
+        if r.get("workload") == workload:
+            return (r["fetch_bytes_per_sweep"] + r["write_bytes_per_sweep"]) * sweeps_per_launch
+    return None
 
 
 def main() -> int:
