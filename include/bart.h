@@ -173,6 +173,14 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c,
  * calls of k sweeps equal one call of 2k. */
 int bart_step(bart_handle *h, int32_t k_sweeps, uint64_t seed);
 
+/* Add f(x) and f(x)^2, in fp64 before rounding, to sum and sumsq (device
+ * f64 [nchain][n_t]) for every chain: called once per kept sweep it
+ * accumulates the posterior mean and variance of f at the points of Xt
+ * (sec. 2.2: the samples of the chain approximate the posterior).  Xt as
+ * for bart_predict. */
+int bart_predict_accumulate(bart_handle *h, const uint8_t *Xt, int64_t xt_stride, int64_t n_t,
+                            double offset, double *sum, double *sumsq);
+
 /* Sum-of-trees prediction f(x) = offset + sum_j g(x; T_j, M_j) (eq. bartdef),
  * each tree traversed by Algorithm 1, summed in fp64 in tree order and
  * rounded to f32, for every chain.  Xt: device u8 [p][xt_stride] binned like
@@ -181,7 +189,8 @@ int bart_predict(bart_handle *h, const uint8_t *Xt, int64_t xt_stride, int64_t n
                  double offset, float *out);
 
 /* Copy the state of chain dst->chain into caller device buffers and fill
- * the scalars; this synchronises the handle's stream. */
+ * the scalars; this synchronises the handle's stream.  A NULL array pointer
+ * skips that array (all NULL: only sigma^2 and the position). */
 int bart_get_state(bart_handle *h, bart_state *dst);
 
 /* Replace the state of chain src->chain from caller device buffers (index
@@ -201,6 +210,38 @@ int bart_status(bart_handle *h, uint32_t *bits);
 
 /* Launch shape of the sweep kernel. */
 int bart_launch_info(const bart_handle *h, bart_launch *out);
+
+/* ---- Host-side preparation (no device, no handle; sec. 3.2 "Predictors",
+ * sec. 2.1 "Hyperparameters").  Host arrays, row-major by predictor. */
+
+#define BART_GRID_UNIFORM 0  /* K cuts evenly spaced strictly inside [min, max] */
+#define BART_GRID_QUANTILE 1 /* K empirical quantiles at k/(K+1), k = 1..K */
+
+/* Splitting grid of every predictor.  X: host f32 [p][ldx] (finite), K in
+ * [1, 255] cuts per predictor.  UNIFORM: c_k = min + k (max - min)/(K+1).
+ * QUANTILE: linear interpolation between order statistics at position
+ * (n - 1) k/(K+1).  Repeated cuts, and quantile cuts at the minimum, are
+ * dropped, so n_cuts[a] <= K; a constant predictor gets none.  cuts: host
+ * f64 [p][K], increasing in its first n_cuts[a] entries, +inf after. */
+int bart_cutpoints(const float *X, int64_t n, int32_t p, int64_t ldx, int32_t K, int32_t grid,
+                   double *cuts, int32_t *n_cuts);
+
+/* Binned predictors X_b[a][i] = #{k < n_cuts[a] : cuts[a][k] <= X[a][i]}
+ * (0 for NaN), so that "right iff X_b >= s" means "X >= c_s".  X: host f32
+ * [p][ldx]; cuts/n_cuts as from bart_cutpoints (row stride K); X_b: host u8
+ * [p][ldb], columns [0, n) written. */
+int bart_bin(const float *X, int64_t n, int32_t p, int64_t ldx, const double *cuts,
+             const int32_t *n_cuts, int32_t K, uint8_t *X_b, int64_t ldb);
+
+/* Default hyperparameters from the response y (host f64 [n]): offset =
+ * mean(y); y_c = f32(y - offset) (host [n]); in cfg: alpha 0.95, beta 2,
+ * mu_mu 0, sigma_mu = (max - min of y_c) / (4 sqrt(ntree)) (the data range
+ * at +-2 prior sd of the sum of trees), nu 3, lambda = var(y) q / nu with q
+ * the 0.1 quantile of chi^2_nu (the data variance at the 0.9 prior
+ * quantile of sigma^2), sigma2_init = var(y), p_grow 0.5.  Other fields of
+ * cfg are left as they are. */
+int bart_default_hyper(const double *y, int64_t n, int32_t ntree, double *offset, float *y_c,
+                       bart_config *cfg);
 
 /* Release the handle (the caller frees X_b and the workspace). */
 void bart_destroy(bart_handle *h);

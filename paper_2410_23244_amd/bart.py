@@ -29,6 +29,7 @@ class BartError(RuntimeError):
 BART_LAUNCH_COOPERATIVE = 0
 BART_LAUNCH_ORDINARY = 1
 BART_RESID_AUTO, BART_RESID_REGISTERS, BART_RESID_STREAMED = 0, 1, 2
+BART_GRID_UNIFORM, BART_GRID_QUANTILE = 0, 1
 
 
 class Config(C.Structure):
@@ -79,6 +80,12 @@ def lib():
         L.bart_init.argtypes = [P(Config), vp, vp, vp, vp, C.c_size_t, vp, P(vp)]
         L.bart_step.argtypes = [vp, C.c_int32, C.c_uint64]
         L.bart_predict.argtypes = [vp, vp, C.c_int64, C.c_int64, C.c_double, vp]
+        L.bart_predict_accumulate.argtypes = [vp, vp, C.c_int64, C.c_int64, C.c_double, vp, vp]
+        L.bart_cutpoints.argtypes = [vp, C.c_int64, C.c_int32, C.c_int64, C.c_int32, C.c_int32,
+                                     vp, vp]
+        L.bart_bin.argtypes = [vp, C.c_int64, C.c_int32, C.c_int64, vp, vp, C.c_int32, vp,
+                               C.c_int64]
+        L.bart_default_hyper.argtypes = [vp, C.c_int64, C.c_int32, vp, vp, P(Config)]
         L.bart_get_state.argtypes = [vp, P(State)]
         L.bart_set_state.argtypes = [vp, P(State)]
         L.bart_debug_steps.argtypes = [vp, C.c_int32, C.c_uint64, vp]
@@ -88,7 +95,8 @@ def lib():
         L.bart_destroy.restype = None
         L.bart_last_error.restype = C.c_char_p
         for f in ["bart_init", "bart_step", "bart_predict", "bart_get_state", "bart_set_state",
-                  "bart_debug_steps", "bart_status", "bart_launch_info"]:
+                  "bart_debug_steps", "bart_status", "bart_launch_info",
+                  "bart_predict_accumulate", "bart_cutpoints", "bart_bin", "bart_default_hyper"]:
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -121,6 +129,46 @@ def bart_step(h: int, k_sweeps: int, seed: int) -> None:
 def bart_predict(h: int, xt_ptr: int, xt_stride: int, n_t: int, offset: float,
                  out_ptr: int) -> None:
     _check(lib().bart_predict(h, xt_ptr, int(xt_stride), int(n_t), float(offset), out_ptr))
+
+
+def bart_predict_accumulate(h: int, xt_ptr: int, xt_stride: int, n_t: int, offset: float,
+                            sum_ptr: int, sumsq_ptr: int) -> None:
+    _check(lib().bart_predict_accumulate(h, xt_ptr, int(xt_stride), int(n_t), float(offset),
+                                         sum_ptr, sumsq_ptr))
+
+
+def bart_cutpoints(X: np.ndarray, K: int, grid: int) -> tuple[np.ndarray, np.ndarray]:
+    """Host splitting grid of X (f32 [p][n]): cuts f64 [p][K], n_cuts i32 [p]."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    p, n = X.shape
+    cuts = np.empty((p, K), np.float64)
+    nc = np.empty(p, np.int32)
+    _check(lib().bart_cutpoints(X.ctypes.data, n, p, n, int(K), int(grid), cuts.ctypes.data,
+                                nc.ctypes.data))
+    return cuts, nc
+
+
+def bart_bin(X: np.ndarray, cuts: np.ndarray, n_cuts: np.ndarray) -> np.ndarray:
+    """Host binning of X (f32 [p][n]) on a grid from bart_cutpoints: u8 [p][n]."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    cuts = np.ascontiguousarray(cuts, dtype=np.float64)
+    nc = np.ascontiguousarray(n_cuts, dtype=np.int32)
+    p, n = X.shape
+    out = np.empty((p, n), np.uint8)
+    _check(lib().bart_bin(X.ctypes.data, n, p, n, cuts.ctypes.data, nc.ctypes.data,
+                          cuts.shape[1], out.ctypes.data, n))
+    return out
+
+
+def bart_default_hyper(y: np.ndarray, ntree: int) -> tuple[float, np.ndarray, Config]:
+    """offset, y_c (f32) and a Config holding the default hyperparameters."""
+    y = np.ascontiguousarray(y, dtype=np.float64)
+    yc = np.empty(y.size, np.float32)
+    off = C.c_double(0.0)
+    cfg = Config()
+    _check(lib().bart_default_hyper(y.ctypes.data, y.size, int(ntree), C.byref(off),
+                                    yc.ctypes.data, C.byref(cfg)))
+    return off.value, yc, cfg
 
 
 def bart_get_state(h: int, st: State) -> None:
@@ -233,6 +281,22 @@ class Bart:
         self.stream.synchronize()
         return out[0] if self.nchain == 1 else out
 
+    def upload_x(self, Xt):
+        """Binned points (u8 [p][n_t]) on the device with a 256-multiple stride."""
+        torch = self.torch
+        Xn = Xt.cpu().numpy() if hasattr(Xt, "cpu") else np.asarray(Xt)
+        p, nt = Xn.shape
+        assert p == self.p
+        stride = x_stride_for(nt)
+        Xd = torch.zeros((p, stride), dtype=torch.uint8, device=self.device)
+        Xd[:, :nt] = torch.from_numpy(np.ascontiguousarray(Xn, dtype=np.uint8)).to(self.device)
+        return Xd, nt
+
+    def predict_accumulate(self, Xd, nt: int, offset: float, acc_sum, acc_sumsq) -> None:
+        """acc_sum/acc_sumsq: float64 device tensors [nchain][nt]; Xd from upload_x."""
+        bart_predict_accumulate(self.h, Xd.data_ptr(), Xd.shape[1], nt, offset,
+                                acc_sum.data_ptr(), acc_sumsq.data_ptr())
+
     def status(self) -> int:
         return bart_status(self.h)
 
@@ -258,6 +322,12 @@ class Bart:
             out["idx"] = out["idx"].view(np.uint16)
         out.update(sigma2=st.sigma2, sweep=st.sweep, next=st.next)
         return out
+
+    def sigma2(self, chain: int = 0) -> float:
+        """Current sigma^2 of a chain (no array copies)."""
+        st = State(None, None, None, None, None, 0.0, 0, 0, int(chain))
+        bart_get_state(self.h, st)
+        return st.sigma2
 
     def set_state(self, s: dict, chain: int = 0) -> None:
         torch = self.torch
@@ -292,3 +362,50 @@ def from_inputs(inp, grid: int = 0, launch: int = 0, residency: int = 0, nchain:
                 idx_bytes=inp.idx_bytes, alpha=h.alpha, beta=h.beta, mu_mu=h.mu_mu,
                 sigma_mu=h.sigma_mu, nu=h.nu, lam=h.lam, sigma2_init=h.sigma2_init,
                 p_grow=h.p_grow, grid=grid, launch=launch, residency=residency, nchain=nchain)
+
+
+class Regressor:
+    """BART regression with the defaults of sec. 2.1: bins X on the host
+    (bart_cutpoints, bart_bin), sets the hyperparameters from y
+    (bart_default_hyper), runs nchain chains on the device and accumulates the
+    posterior mean and sd of f at the test points over the kept sweeps
+    (bart_predict_accumulate).  X is f32 [n][p] (one row per observation)."""
+
+    def __init__(self, ntree: int = 200, max_depth: int = 6, K: int = 255,
+                 grid: int = BART_GRID_QUANTILE, nchain: int = 1, seed: int = 0):
+        self.ntree, self.max_depth, self.K, self.grid = ntree, max_depth, K, grid
+        self.nchain, self.seed = nchain, seed
+
+    def fit(self, X, y, X_test, n_burn: int = 100, n_keep: int = 1000):
+        import torch
+
+        Xt = np.ascontiguousarray(np.asarray(X, dtype=np.float32).T)
+        Xs = np.ascontiguousarray(np.asarray(X_test, dtype=np.float32).T)
+        self.cuts, self.n_cuts = bart_cutpoints(Xt, self.K, self.grid)
+        Xb = bart_bin(Xt, self.cuts, self.n_cuts)
+        Xsb = bart_bin(Xs, self.cuts, self.n_cuts)
+        self.offset, yc, hc = bart_default_hyper(np.asarray(y, dtype=np.float64), self.ntree)
+        self.chain = Bart(Xb, yc, self.n_cuts, ntree=self.ntree, max_depth=self.max_depth,
+                          alpha=hc.alpha, beta=hc.beta, mu_mu=hc.mu_mu, sigma_mu=hc.sigma_mu,
+                          nu=hc.nu, lam=hc.lam, sigma2_init=hc.sigma2_init, p_grow=hc.p_grow,
+                          nchain=self.nchain)
+        g = self.chain
+        Xd, nt = g.upload_x(Xsb)
+        s = torch.zeros((self.nchain, nt), dtype=torch.float64, device=g.device)
+        s2 = torch.zeros_like(s)
+        g.step(n_burn, self.seed)
+        sig = np.empty((n_keep, self.nchain))
+        for k in range(n_keep):
+            g.step(1, self.seed)
+            g.predict_accumulate(Xd, nt, self.offset, s, s2)
+            for c in range(self.nchain):
+                sig[k, c] = g.sigma2(c)
+        if g.status():
+            raise BartError(BART_EDEVICE, "device error during sampling")
+        mean = (s / n_keep).cpu().numpy()
+        var = (s2 / n_keep).cpu().numpy() - mean ** 2
+        self.chain_mean = mean                       # [nchain][n_test]
+        self.mean = mean.mean(axis=0)                # posterior mean over all chains
+        self.sd = np.sqrt(np.maximum(var.mean(axis=0) + mean.var(axis=0), 0.0))
+        self.sigma2_trace = sig
+        return self

@@ -215,35 +215,77 @@ __global__ void k_recount(const uint8_t *idx, int64_t ldi, int ib, int32_t *coun
     if (hist[k]) atomicAdd(&count[(int64_t)j * 2 * H + k], hist[k]);
 }
 
-// f(x) = offset + sum_j g(x; T_j, M_j): Algorithm 1 per tree, fp64 sum in
-// tree order.  blockIdx.y = chain: its trees sit chain_bytes further on and
-// its predictions nt further on.
-__global__ void k_predict(const uint8_t *Xt, int64_t ldx, int64_t nt, int p,
-                          const uint16_t *axis0, const uint8_t *cut0, const float *leaf0, int m,
-                          int D, int H, double offset, size_t chain_bytes, float *out0) {
-  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  if (i >= nt) return;
+// f(x) = offset + sum_j g(x; T_j, M_j): Algorithm 1 per tree (loop over the
+// levels with a reached-leaf flag), fp64 sum in tree order.  Trees are staged
+// through LDS in tiles of kPredNodes heap slots; every thread follows its
+// point through kPredIlp trees at once so their predictor-byte gathers
+// overlap.  blockIdx.y = chain: its trees sit chain_bytes further on, its
+// outputs nt further on.  ACC: add f and f^2 (fp64) to sum and sumsq instead
+// of writing fp32(f) to out.
+constexpr int kPredBlock = 256;
+constexpr int kPredNodes = 2048;  // heap slots per LDS tile (axis u16 + cut u8 + 2 leaves f32: 22 KB)
+constexpr int kPredIlp = 4;
+
+template <bool ACC>
+__global__ void __launch_bounds__(kPredBlock)
+    k_predict(const uint8_t *Xt, int64_t ldx, int64_t nt, int p, const uint16_t *axis0,
+              const uint8_t *cut0, const float *leaf0, int m, int D, int H, double offset,
+              size_t chain_bytes, float *out0, double *sum0, double *sumsq0) {
+  __shared__ uint16_t s_ax[kPredNodes];
+  __shared__ uint8_t s_ct[kPredNodes];
+  __shared__ float s_lf[2 * kPredNodes];
+  const int t = threadIdx.x;
+  const int64_t i = blockIdx.x * (int64_t)kPredBlock + t;
+  const bool valid = i < nt;
   const size_t cb = blockIdx.y * chain_bytes;
   const uint16_t *axis = (const uint16_t *)((const char *)axis0 + cb);
   const uint8_t *cut = cut0 + cb;
   const float *leaf = (const float *)((const char *)leaf0 + cb);
-  float *out = out0 + blockIdx.y * nt;
+  const int TT = kPredNodes / H;  // trees per tile
+  const uint8_t *xcol = Xt + (valid ? i : 0);
   double acc = 0.0;
-  for (int j = 0; j < m; ++j) {
-    const uint16_t *ax = axis + (int64_t)j * H;
-    const uint8_t *ct = cut + (int64_t)j * H;
-    int index = 1;
-    bool found = false;
-    for (int lvl = 1; lvl <= D - 1; ++lvl) {
-      const int a = ax[index], split = ct[index];
-      found = found || split == 0;
-      const int xa = Xt[(int64_t)(a < p ? a : 0) * ldx + i];
-      const int child = 2 * index + (xa >= split ? 1 : 0);
-      index = found ? index : child;
+  for (int j0 = 0; j0 < m; j0 += TT) {
+    const int nt_ = min(TT, m - j0);
+    __syncthreads();
+    for (int q = t; q < nt_ * H; q += kPredBlock) {
+      s_ax[q] = axis[(int64_t)j0 * H + q];
+      s_ct[q] = cut[(int64_t)j0 * H + q];
     }
-    acc += (double)leaf[(int64_t)j * 2 * H + index];
+    for (int q = t; q < nt_ * 2 * H; q += kPredBlock) s_lf[q] = leaf[(int64_t)j0 * 2 * H + q];
+    __syncthreads();
+    if (!valid) continue;
+    for (int jj = 0; jj < nt_; jj += kPredIlp) {
+      int index[kPredIlp];
+      bool found[kPredIlp];
+#pragma unroll
+      for (int u = 0; u < kPredIlp; ++u) {
+        index[u] = 1;
+        found[u] = jj + u >= nt_;  // past the tile: nothing to do
+      }
+      for (int lvl = 1; lvl <= D - 1; ++lvl) {
+#pragma unroll
+        for (int u = 0; u < kPredIlp; ++u) {
+          const int base = (jj + u < nt_ ? jj + u : 0) * H;
+          const int a = s_ax[base + index[u]], split = s_ct[base + index[u]];
+          found[u] = found[u] || split == 0;
+          const int xa = found[u] ? 0 : xcol[(int64_t)(a < p ? a : 0) * ldx];
+          index[u] = found[u] ? index[u] : 2 * index[u] + (xa >= split ? 1 : 0);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kPredIlp; ++u)  // tree order
+        if (jj + u < nt_) acc += (double)s_lf[(jj + u) * 2 * H + index[u]];
+    }
   }
-  out[i] = (float)(offset + acc);
+  if (!valid) return;
+  const int64_t o = blockIdx.y * nt + i;
+  const double f = offset + acc;
+  if (ACC) {
+    sum0[o] += f;
+    sumsq0[o] += f * f;
+  } else {
+    out0[o] = (float)f;
+  }
 }
 
 int grid_for(int64_t work, int block) {
@@ -526,18 +568,33 @@ int bart_predict(bart_handle *h, const uint8_t *Xt, int64_t xt_stride, int64_t n
   if (!Xt || !out) return fail(BART_EINVAL, "NULL pointer argument");
   if (xt_stride < n_t || xt_stride % 16) return fail(BART_EINVAL, "xt_stride must be >= n_t and a multiple of 16");
   HIP_TRY(hipSetDevice(h->device));
-  k_predict<<<dim3(grid_for(n_t, 256), h->nchain), 256, 0, h->stream>>>(
+  k_predict<false><<<dim3(grid_for(n_t, kPredBlock), h->nchain), kPredBlock, 0, h->stream>>>(
       Xt, xt_stride, n_t, h->cfg.p, atc<uint16_t>(h, 0, h->lay.axis),
       atc<uint8_t>(h, 0, h->lay.cut), atc<float>(h, 0, h->lay.leaf), h->cfg.ntree,
-      h->cfg.max_depth, h->H, offset, h->lay.chain_bytes, out);
+      h->cfg.max_depth, h->H, offset, h->lay.chain_bytes, out, nullptr, nullptr);
+  HIP_TRY(hipGetLastError());
+  return BART_OK;
+}
+
+int bart_predict_accumulate(bart_handle *h, const uint8_t *Xt, int64_t xt_stride, int64_t n_t,
+                            double offset, double *sum, double *sumsq) {
+  if (!h) return fail(BART_EINVAL, "handle is NULL");
+  if (n_t < 0) return fail(BART_EINVAL, "n_t must be >= 0");
+  if (n_t == 0) return BART_OK;
+  if (!Xt || !sum || !sumsq) return fail(BART_EINVAL, "NULL pointer argument");
+  if (xt_stride < n_t || xt_stride % 16) return fail(BART_EINVAL, "xt_stride must be >= n_t and a multiple of 16");
+  if (n_t > ((int64_t)1 << 40)) return fail(BART_ENOTSUP, "n_t too large");
+  HIP_TRY(hipSetDevice(h->device));
+  k_predict<true><<<dim3(grid_for(n_t, kPredBlock), h->nchain), kPredBlock, 0, h->stream>>>(
+      Xt, xt_stride, n_t, h->cfg.p, atc<uint16_t>(h, 0, h->lay.axis),
+      atc<uint8_t>(h, 0, h->lay.cut), atc<float>(h, 0, h->lay.leaf), h->cfg.ntree,
+      h->cfg.max_depth, h->H, offset, h->lay.chain_bytes, nullptr, sum, sumsq);
   HIP_TRY(hipGetLastError());
   return BART_OK;
 }
 
 int bart_get_state(bart_handle *h, bart_state *d) {
   if (!h || !d) return fail(BART_EINVAL, "NULL argument");
-  if (!d->axis || !d->cut || !d->leaf || !d->idx || !d->resid)
-    return fail(BART_EINVAL, "NULL state buffer");
   const int ch = d->chain;
   if (ch < 0 || ch >= h->nchain)
     return fail(BART_EINVAL, "chain %d not in [0, %d)", ch, h->nchain);
@@ -546,15 +603,21 @@ int bart_get_state(bart_handle *h, bart_state *d) {
   const size_t m = c.ntree, H = h->H;
   hipStream_t st = h->stream;
   const Layout &L = h->lay;
-  HIP_TRY(hipMemcpyAsync(d->axis, atc<void>(h, ch, L.axis), 2 * m * H, hipMemcpyDeviceToDevice, st));
-  HIP_TRY(hipMemcpyAsync(d->cut, atc<void>(h, ch, L.cut), m * H, hipMemcpyDeviceToDevice, st));
-  HIP_TRY(hipMemcpyAsync(d->leaf, atc<void>(h, ch, L.leaf), 4 * m * 2 * H, hipMemcpyDeviceToDevice,
-                         st));
-  HIP_TRY(hipMemcpy2DAsync(d->idx, (size_t)c.n * c.idx_bytes, atc<void>(h, ch, L.idx),
-                           (size_t)L.n_pad * c.idx_bytes, (size_t)c.n * c.idx_bytes, m,
+  if (d->axis)
+    HIP_TRY(hipMemcpyAsync(d->axis, atc<void>(h, ch, L.axis), 2 * m * H, hipMemcpyDeviceToDevice,
+                           st));
+  if (d->cut)
+    HIP_TRY(hipMemcpyAsync(d->cut, atc<void>(h, ch, L.cut), m * H, hipMemcpyDeviceToDevice, st));
+  if (d->leaf)
+    HIP_TRY(hipMemcpyAsync(d->leaf, atc<void>(h, ch, L.leaf), 4 * m * 2 * H,
                            hipMemcpyDeviceToDevice, st));
-  HIP_TRY(hipMemcpyAsync(d->resid, atc<void>(h, ch, L.resid), 4 * (size_t)c.n,
-                         hipMemcpyDeviceToDevice, st));
+  if (d->idx)
+    HIP_TRY(hipMemcpy2DAsync(d->idx, (size_t)c.n * c.idx_bytes, atc<void>(h, ch, L.idx),
+                             (size_t)L.n_pad * c.idx_bytes, (size_t)c.n * c.idx_bytes, m,
+                             hipMemcpyDeviceToDevice, st));
+  if (d->resid)
+    HIP_TRY(hipMemcpyAsync(d->resid, atc<void>(h, ch, L.resid), 4 * (size_t)c.n,
+                           hipMemcpyDeviceToDevice, st));
   Ctl ctl;
   HIP_TRY(hipMemcpyAsync(&ctl, atc<void>(h, ch, L.ctl), sizeof(Ctl), hipMemcpyDeviceToHost, st));
   HIP_TRY(hipStreamSynchronize(st));
@@ -634,3 +697,6 @@ int bart_launch_info(const bart_handle *h, bart_launch *o) {
 void bart_destroy(bart_handle *h) { delete h; }
 
 }  // extern "C"
+
+// host-side input preparation (bart_cutpoints, bart_bin, bart_default_hyper)
+#include "prep.hpp"

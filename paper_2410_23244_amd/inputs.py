@@ -183,3 +183,27 @@ def timing_dgp(n: int, p: int) -> tuple[np.ndarray, np.ndarray]:
         X_b[j - 1] = ((i + (p + 1) * j) % 256).astype(np.uint8)
     y = np.cos(2.0 * n * np.pi / 32.0 * (i - 1) / max(n - 1, 1))
     return X_b, y
+
+
+def rmse_dgp(n_train: int, n_test: int, p: int, seed: int = 0):
+    """The paper's predictive-accuracy data (sec. 4.2, eq. rmsedgp): a dense
+    linear term and a sparse quadratic term, each standardised to unit
+    sample variance over train and test together, plus N(0, 1) noise.
+    X ~ U(0,1), beta_j ~ N(0,1), A_jk ~ N(0,1) when the circular distance
+    min(|j-k|, p-|j-k|) < 5, else 0.  Returns (X_train [p][n_train] f32,
+    y_train, X_test [p][n_test] f32, y_test, f_test) with y and f in fp64."""
+    rng = np.random.default_rng([*SEED_BASE, 42, seed])
+    n = n_train + n_test
+    X = rng.random((n, p))
+    beta = rng.standard_normal(p)
+    j = np.arange(p)
+    dist = np.abs(j[:, None] - j[None, :])
+    near = np.minimum(dist, p - dist) < 5
+    A = np.where(near, rng.standard_normal((p, p)), 0.0)
+    lin = X @ beta
+    quad = np.einsum("ij,jk,ik->i", X, A, X)
+    f = lin / lin.std() + quad / quad.std()
+    y = f + rng.standard_normal(n)
+    Xf = X.astype(np.float32).T.copy()
+    return (Xf[:, :n_train].copy(), y[:n_train], Xf[:, n_train:].copy(), y[n_train:],
+            f[n_train:])
