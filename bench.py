@@ -79,16 +79,19 @@ def copy_probe(mib: int) -> int:
     return 0
 
 
+SWEEP_SOURCES = ("common.hpp", "propose.hpp", "rng.hpp", "sweep.hpp")
+
+
 def kernel_source_digest() -> str:
-    """sha256 over the HIP sources of the sweep (to tell whether stored counters are stale)."""
+    """sha256 over the sources of the sweep kernels (to tell whether stored
+    counters are stale); host code and the predict kernel do not enter."""
     import hashlib
 
     d = os.path.join(ROOT, "paper_2410_23244_amd", "csrc")
     h = hashlib.sha256()
-    for name in sorted(os.listdir(d)):
-        if name.endswith((".hip", ".hpp")):
-            with open(os.path.join(d, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+    for name in SWEEP_SOURCES:
+        with open(os.path.join(d, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()
 
 
@@ -109,6 +112,45 @@ def stored_traffic(workload: str, sweeps_per_launch: int):
     return None
 
 
+def bench_predict(args, inp, g) -> int:
+    """Time bart_predict of the warmed-up chains on NT points of the same generator."""
+    import torch
+
+    from paper_2410_23244_amd.inputs import make_inputs
+
+    nt = args.predict
+    Xt = make_inputs(args.config, n=nt).X_b
+    Xd, _ = g.upload_x(Xt)
+    out = torch.empty((args.chains, nt), dtype=torch.float32, device=g.device)
+    from paper_2410_23244_amd.bart import bart_predict
+
+    def once():
+        bart_predict(g.h, Xd.data_ptr(), Xd.shape[1], nt, inp.offset, out.data_ptr())
+
+    for _ in range(3):
+        once()
+    torch.cuda.synchronize()
+    reps = max(1, args.steps // 100)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(g.stream)
+    for _ in range(reps):
+        once()
+    e1.record(g.stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    trav = args.chains * nt * inp.m
+    line = {"metric": f"sum-of-trees predictions/sec at n_t={nt}, ntree={inp.m}, D={inp.D}, "
+                      f"p={inp.p}",
+            "value": args.chains * nt / (ms / 1e3), "unit": "points/s", "n_gpus": 1,
+            "steps": reps, "warmup": 3, "ms_per_step": ms, "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "f64 sum, u8 route",
+            "data": "synthetic", "tree_traversals_per_s": trav / (ms / 1e3),
+            "config": {"workload": f"bart_predict_nt{nt}_" + inp.workload, "nchain": args.chains,
+                       "trees_after_warmup_sweeps": args.warmup}}
+    print(json.dumps(line), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -124,6 +166,8 @@ def main() -> int:
     ap.add_argument("--seed", type=int, default=3)
     ap.add_argument("--chains", type=int, default=1, help="independent chains per launch")
     ap.add_argument("--grid", type=int, default=0, help="workgroups per chain (0 = automatic)")
+    ap.add_argument("--predict", type=int, default=0, metavar="NT",
+                    help="after the warm-up, time bart_predict on NT points instead of sweeps")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (read MIB, write MIB) three "
                          "times, to calibrate HBM byte counters, and exit")
@@ -164,6 +208,8 @@ def main() -> int:
     torch.cuda.synchronize()
     assert g.status() == 0, "device error during warm-up"
     print(f"[bench] warm-up {args.warmup} sweeps done", file=sys.stderr, flush=True)
+    if args.predict:
+        return bench_predict(args, inp, g)
 
     L = args.steps // S
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * L)]
