@@ -146,6 +146,12 @@ struct Shared {
   double wave_part[kWaves];
   double sigma2;
   double dec_logr;
+  // constants of tree j's decision that do not depend on its sums, computed
+  // while the mailboxes fill: per rank of a leaf whose count is known, the new
+  // value is S la + lb and S = R + lnm; the merged leaf likewise (ma, mb);
+  // for a PRUNE, the count-only parts of the likelihood ratio
+  double la[kMaxLeaves], lb[kMaxLeaves], lnm[kMaxLeaves];
+  double ma, mb, pdet, pdL, pdR, pdP;
   uint64_t stats[6];  // workgroup 0: move statistics of this launch
   int nr[2];  // GROW right-counts of the trees being routed, by tree parity
   int flags;  // bit0 accept, bit1 merged
@@ -393,26 +399,60 @@ __device__ __noinline__ void trace_tree_step(bart_trace *R, Shared &sh, const Ct
 // leaves; each wave sums the segments of the words it needs with the
 // fixed-order DPP tree (nseg <= 32).  Writes sh.flags, dec_logr, and per
 // rank cntd, S, newv, dlt, plus newv_m and dlt_m for a merged move.
+// The parts of tree j's decision that need only counts (sec. 3.3 items 4,
+// 5, 9, 10): for every leaf of known count (all but the children of a GROW)
+// prec = n / s2 + 1 / v2 and the draw mean + z / sqrt(prec) written as
+// S la + lb; the merged leaf of eta; for a PRUNE, the determinant term and
+// the denominators of the likelihood ratio.  Waves 4..7, before the gather.
+__device__ __forceinline__ void pre_decide(const SweepArgs *__restrict__ A, Shared &sh,
+                                           const Ctx &c, const TreeData &td) {
+  const int u = (int)threadIdx.x - 4 * 64;
+  if (u < 0) return;
+  const int move = c.pr.move, eta = c.pr.eta, L = c.pr.L;
+  const int kl = c.pr.rank_l, kr = c.pr.rank_r;
+  const double s2 = sh.sigma2, v2 = A->sigma_mu * A->sigma_mu;
+  const double iv2 = 1.0 / v2, mm = A->mu_mu * iv2;
+  auto consts = [&](double n, double z, double &la, double &lb) {
+    const double prec = n / s2 + iv2;
+    la = 1.0 / (s2 * prec);
+    lb = mm / prec + z / sqrt(prec);
+  };
+  if (u < L) {
+    const int h = c.heap_of[u];
+    const bool child = (move == kGrow) && ((h >> 1) == eta);
+    if (!child) {
+      const double n = (double)td.cnt[u];
+      consts(n, td.z[u], sh.la[u], sh.lb[u]);
+      sh.lnm[u] = n * (double)td.mu[u];
+    }
+  } else if (u == L && move != kNone) {
+    const double n = move == kGrow ? (double)td.eta_cnt : (double)td.cnt[kl] + (double)td.cnt[kr];
+    consts(n, td.eta_z, sh.ma, sh.mb);
+  } else if (u == L + 1 && move == kPrune) {
+    const double nl = (double)td.cnt[kl], nr = (double)td.cnt[kr], np = nl + nr;
+    const double eL = s2 + nl * v2, eR = s2 + nr * v2, eP = s2 + np * v2;
+    sh.pdL = 1.0 / eL;
+    sh.pdR = 1.0 / eR;
+    sh.pdP = 1.0 / eP;
+    sh.pdet = 0.5 * log(s2 * eP / (eL * eR));
+  }
+}
+
+// Tree j's decision once the sums are in (sec. 3.3 items 8-10): wave 0 the
+// MH ratio and accept, waves 1-2 the draws of the two move leaves, wave 3
+// the merged draw, waves 4-7 every other leaf.  Every workgroup runs this on
+// identical totals.
 __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Shared &sh,
                                             const Ctx &c, const TreeData &td, int nseg) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int move = c.pr.move, eta = c.pr.eta, L = c.pr.L;
+  const int move = c.pr.move, L = c.pr.L;
   const int kl = c.pr.rank_l, kr = c.pr.rank_r;
   const int K = L + 1;
   const double s2 = sh.sigma2, v2 = A->sigma_mu * A->sigma_mu;
   auto total = [&](int k) {
     return wave_total63(lane < nseg ? sh.part[lane * K + k] : 0.0);  // valid in lane 63
   };
-  // count and partial sum S_h = R_h + n_h * (old value) of rank k (sec. 3.3
-  // item 8); nR is the GROW right-count
-  auto leaf_stats = [&](int k, double R, double nR, double &nk, float &mo) {
-    const int h = c.heap_of[k];
-    const bool child = (move == kGrow) && ((h >> 1) == eta);
-    nk = child ? ((h & 1) ? nR : (double)td.eta_cnt - nR) : (double)td.cnt[k];
-    mo = child ? td.eta_mu : td.mu[k];
-    return R + nk * (double)mo;
-  };
-  // conditional draw of a leaf value (items 4, 5, 10)
+  // conditional draw of a GROW child, whose count comes with the sums
   auto draw_leaf = [&](double nf, double Sf, double z) {
     const double prec = nf / s2 + 1.0 / v2;
     const double mean = (Sf / s2 + A->mu_mu / v2) / prec;
@@ -422,28 +462,49 @@ __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Sha
     const double nR = move == kGrow ? total(L) : 0.0;
     const double Rl = total(kl), Rr = total(kr);
     if (lane == 63) {
-      double nl, nr;
+      // counts and partial sums S_h = R_h + n_h (old value) of the two leaves
+      double nl = 0.0, nr = 0.0, Sl, Sr;
       float mol, mor;
-      const double Sl = leaf_stats(kl, Rl, nR, nl, mol);
-      const double Sr = leaf_stats(kr, Rr, nR, nr, mor);
+      if (move == kGrow) {
+        nr = nR;
+        nl = (double)td.eta_cnt - nR;
+        mol = mor = td.eta_mu;
+        Sl = Rl + nl * (double)mol;
+        Sr = Rr + nr * (double)mor;
+      } else {
+        mol = td.mu[kl];
+        mor = td.mu[kr];
+        Sl = Rl + sh.lnm[kl];
+        Sr = Rr + sh.lnm[kr];
+      }
       if (wave == 0) {
-        const double llr = split_llr(s2, A->mu_mu, v2, nl, Sl, nr, Sr);
+        double llr;
+        if (move == kGrow) {
+          llr = split_llr(s2, A->mu_mu, v2, nl, Sl, nr, Sr);
+        } else {
+          const double nlp = (double)td.cnt[kl], nrp = (double)td.cnt[kr];
+          const double tL = Sl - nlp * A->mu_mu, tR = Sr - nrp * A->mu_mu;
+          const double tP = (Sl + Sr) - (nlp + nrp) * A->mu_mu;
+          llr = sh.pdet + v2 / (2.0 * s2) *
+                              (tL * tL * sh.pdL + tR * tR * sh.pdR - tP * tP * sh.pdP);
+        }
         const double logr = c.pr.c_prior + (move == kGrow ? llr : -llr);
         const int acc = c.pr.ln_u < logr ? 1 : 0;
         const int merged = (move == kGrow && !acc) || (move == kPrune && acc);
         sh.dec_logr = logr;
         sh.flags = acc | (merged << 1);
       } else if (wave == 3) {
-        const float vm = draw_leaf(nl + nr, Sl + Sr, td.eta_z);
+        const float vm = (float)((Sl + Sr) * sh.ma + sh.mb);
         sh.newv_m = vm;
         sh.dlt_m[0] = mol - vm;
         sh.dlt_m[1] = mor - vm;
       } else {
         const int k = wave == 1 ? kl : kr;
-        const double nk = wave == 1 ? nl : nr, Sk = wave == 1 ? Sl : Sr;
+        const double Sk = wave == 1 ? Sl : Sr;
         const float mo = wave == 1 ? mol : mor;
-        const float v = draw_leaf(nk, Sk, td.z[k]);
-        sh.cntd[k] = nk;
+        const float v = move == kGrow ? draw_leaf(wave == 1 ? nl : nr, Sk, td.z[k])
+                                      : (float)(Sk * sh.la[k] + sh.lb[k]);
+        sh.cntd[k] = move == kGrow ? (wave == 1 ? nl : nr) : (double)td.cnt[k];
         sh.S[k] = Sk;
         sh.newv[k] = v;
         sh.dlt[k] = mo - v;
@@ -456,17 +517,15 @@ __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Sha
   }
   const int first = move != kNone ? wave - 4 : wave, stride = move != kNone ? 4 : kWaves;
   for (int k = first < 0 ? L : first; k < L; k += stride) {
-    if (k == kl || k == kr) continue;
+    if (move != kNone && (k == kl || k == kr)) continue;
     const double R = total(k);
     if (lane == 63) {
-      double nk;
-      float mo;
-      const double Sk = leaf_stats(k, R, 0.0, nk, mo);
-      const float v = draw_leaf(nk, Sk, td.z[k]);
-      sh.cntd[k] = nk;
+      const double Sk = R + sh.lnm[k];
+      const float v = (float)(Sk * sh.la[k] + sh.lb[k]);
+      sh.cntd[k] = (double)td.cnt[k];
       sh.S[k] = Sk;
       sh.newv[k] = v;
-      sh.dlt[k] = mo - v;
+      sh.dlt[k] = td.mu[k] - v;
     }
   }
 }
@@ -810,6 +869,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       //    per-segment partials, then one wave reduces a word over the
       //    segments with the fixed-order DPP tree (nseg <= 32 lanes)
       const int K = L + 1;
+      pre_decide(A, sh, c, sh.td[j & 1]);
       const int nseg = gather_polls(A, sh, par, seq, K, L);
       decide_step(A, sh, c, sh.td[j & 1], nseg);
       // stage what later trees need
@@ -1155,6 +1215,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       const uint32_t pw3 = load_prop_word(A, j3);
       lds_barrier();
       if (t == L) sh.nr[j & 1] = 0;
+      pre_decide(A, sh, c, sh.td[j & 1]);
       const int nseg = gather_polls(A, sh, par, seq, L + 1, L);
       decide_step(A, sh, c, sh.td[j & 1], nseg);
       if (more3 && t < kPropWords) ((uint32_t *)&sh.ctx[(j + 3) & (kRing - 1)].pr)[t] = pw3;
