@@ -96,6 +96,22 @@ __device__ __forceinline__ double wave_total63(double v) {
   return v;
 }
 
+// wave_total63 of three values at once, the steps interleaved so that the
+// three DPP chains overlap.
+__device__ __forceinline__ void wave_totals3(double &a, double &b, double &c) {
+#define BART_STEP3(ctrl, mask)        \
+  a += dpp_f64<ctrl, mask>(a);        \
+  b += dpp_f64<ctrl, mask>(b);        \
+  c += dpp_f64<ctrl, mask>(c);
+  BART_STEP3(0x111, 0xF)
+  BART_STEP3(0x112, 0xF)
+  BART_STEP3(0x114, 0xF)
+  BART_STEP3(0x118, 0xF)
+  BART_STEP3(0x142, 0xA)
+  BART_STEP3(0x143, 0xC)
+#undef BART_STEP3
+}
+
 // Log marginal-likelihood ratio of splitting a leaf into (L, R): the
 // partial residuals of a leaf with n points, its N(mu_mu, sigma_mu^2) value
 // integrated out (sec. 2.1), are N(mu_mu 1, sigma^2 I + sigma_mu^2 1 1^T).
@@ -449,9 +465,13 @@ __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Sha
   const int kl = c.pr.rank_l, kr = c.pr.rank_r;
   const int K = L + 1;
   const double s2 = sh.sigma2, v2 = A->sigma_mu * A->sigma_mu;
-  auto total = [&](int k) {
-    return wave_total63(lane < nseg ? sh.part[lane * K + k] : 0.0);  // valid in lane 63
+  // this lane's segment partial of word k (0 past the segments); the read
+  // index is clamped so every lane reads in bounds without a branch
+  auto seg_part = [&](int k) {
+    const double x = sh.part[(lane < nseg ? lane : 0) * K + k];
+    return lane < nseg ? x : 0.0;
   };
+  auto total = [&](int k) { return wave_total63(seg_part(k)); };  // valid in lane 63
   // conditional draw of a GROW child, whose count comes with the sums
   auto draw_leaf = [&](double nf, double Sf, double z) {
     const double prec = nf / s2 + 1.0 / v2;
@@ -459,8 +479,8 @@ __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Sha
     return (float)(mean + z / sqrt(prec));
   };
   if (move != kNone && wave < 4) {
-    const double nR = move == kGrow ? total(L) : 0.0;
-    const double Rl = total(kl), Rr = total(kr);
+    double nR = move == kGrow ? seg_part(L) : 0.0, Rl = seg_part(kl), Rr = seg_part(kr);
+    wave_totals3(nR, Rl, Rr);
     if (lane == 63) {
       // counts and partial sums S_h = R_h + n_h (old value) of the two leaves
       double nl = 0.0, nr = 0.0, Sl, Sr;
