@@ -112,20 +112,6 @@ __device__ __forceinline__ void wave_totals3(double &a, double &b, double &c) {
 #undef BART_STEP3
 }
 
-// Log marginal-likelihood ratio of splitting a leaf into (L, R): the
-// partial residuals of a leaf with n points, its N(mu_mu, sigma_mu^2) value
-// integrated out (sec. 2.1), are N(mu_mu 1, sigma^2 I + sigma_mu^2 1 1^T).
-__device__ inline double split_llr(double s2, double mu_mu, double v, double nL, double SL,
-                                   double nR, double SR) {
-  const double nP = nL + nR, SP = SL + SR;
-  const double tL = SL - nL * mu_mu, tR = SR - nR * mu_mu, tP = SP - nP * mu_mu;
-  const double qL = tL * tL / (s2 + nL * v);
-  const double qR = tR * tR / (s2 + nR * v);
-  const double qP = tP * tP / (s2 + nP * v);
-  const double det = 0.5 * log(s2 * (s2 + nP * v) / ((s2 + nL * v) * (s2 + nR * v)));
-  return det + v / (2.0 * s2) * (qL + qR - qP);
-}
-
 // Per-workgroup view of one tree's proposal.
 struct Ctx {
   Prop pr;
@@ -167,7 +153,7 @@ struct Shared {
   // value is S la + lb and S = R + lnm; the merged leaf likewise (ma, mb);
   // for a PRUNE, the count-only parts of the likelihood ratio
   double la[kMaxLeaves], lb[kMaxLeaves], lnm[kMaxLeaves];
-  double ma, mb, pdet, pdL, pdR, pdP;
+  double ma, mb, pdet, pdL, pdR, pdP, gs2eP;
   uint64_t stats[6];  // workgroup 0: move statistics of this launch
   int nr[2];  // GROW right-counts of the trees being routed, by tree parity
   int flags;  // bit0 accept, bit1 merged
@@ -451,6 +437,11 @@ __device__ __forceinline__ void pre_decide(const SweepArgs *__restrict__ A, Shar
     sh.pdR = 1.0 / eR;
     sh.pdP = 1.0 / eP;
     sh.pdet = 0.5 * log(s2 * eP / (eL * eR));
+  } else if (u == L + 1 && move == kGrow) {
+    // the parent eta of a GROW keeps its count: its denominator is known
+    const double eP = s2 + (double)td.eta_cnt * v2;
+    sh.pdP = 1.0 / eP;
+    sh.gs2eP = s2 * eP;
   }
 }
 
@@ -472,59 +463,69 @@ __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Sha
     return lane < nseg ? x : 0.0;
   };
   auto total = [&](int k) { return wave_total63(seg_part(k)); };  // valid in lane 63
-  // conditional draw of a GROW child, whose count comes with the sums
-  auto draw_leaf = [&](double nf, double Sf, double z) {
-    const double prec = nf / s2 + 1.0 / v2;
-    const double mean = (Sf / s2 + A->mu_mu / v2) / prec;
-    return (float)(mean + z / sqrt(prec));
+  // conditional draw of a GROW child, whose count n comes with the sums:
+  // with e = s2 + n v2, prec = e / (s2 v2), the mean is (S v2 + mu_mu s2) / e
+  // and the sd sqrt(s2 v2 / e)
+  auto draw_child = [&](double e, double Sf, double z) {
+    const double ie = 1.0 / e;
+    return (float)((Sf * v2 + A->mu_mu * s2) * ie + z * sqrt(s2 * v2 * ie));
   };
   if (move != kNone && wave < 4) {
+    // everything this part reads from LDS besides the sums, read up front
+    const double eta_cnt = (double)td.eta_cnt;
+    const float eta_mu = td.eta_mu, mul = td.mu[kl], mur = td.mu[kr];
+    const double cl = (double)td.cnt[kl], cr = (double)td.cnt[kr];
+    const double lnml = sh.lnm[kl], lnmr = sh.lnm[kr];
+    const double lal = sh.la[kl], lar = sh.la[kr], lbl = sh.lb[kl], lbr = sh.lb[kr];
+    const double zl = td.z[kl], zr = td.z[kr];
+    const double ma = sh.ma, mb = sh.mb, pdP = sh.pdP;
+    const double pdet = sh.pdet, pdL = sh.pdL, pdR = sh.pdR, gs2eP = sh.gs2eP;
+    const double c_prior = c.pr.c_prior, ln_u = c.pr.ln_u;
     double nR = move == kGrow ? seg_part(L) : 0.0, Rl = seg_part(kl), Rr = seg_part(kr);
     wave_totals3(nR, Rl, Rr);
     if (lane == 63) {
       // counts and partial sums S_h = R_h + n_h (old value) of the two leaves
-      double nl = 0.0, nr = 0.0, Sl, Sr;
-      float mol, mor;
-      if (move == kGrow) {
-        nr = nR;
-        nl = (double)td.eta_cnt - nR;
-        mol = mor = td.eta_mu;
-        Sl = Rl + nl * (double)mol;
-        Sr = Rr + nr * (double)mor;
-      } else {
-        mol = td.mu[kl];
-        mor = td.mu[kr];
-        Sl = Rl + sh.lnm[kl];
-        Sr = Rr + sh.lnm[kr];
-      }
+      const bool grow = move == kGrow;
+      const double nl = grow ? eta_cnt - nR : cl, nr = grow ? nR : cr;
+      const float mol = grow ? eta_mu : mul, mor = grow ? eta_mu : mur;
+      const double Sl = grow ? Rl + nl * (double)mol : Rl + lnml;
+      const double Sr = grow ? Rr + nr * (double)mor : Rr + lnmr;
+      const double mm = A->mu_mu;
+      const double tL = Sl - nl * mm, tR = Sr - nr * mm, tP = (Sl + Sr) - (nl + nr) * mm;
       if (wave == 0) {
+        // log marginal-likelihood ratio of splitting a leaf into (L, R): the
+        // partial residuals of a leaf with n points, its N(mu_mu, v2) value
+        // integrated out (sec. 2.1), are N(mu_mu 1, s2 I + v2 1 1^T), so
+        // LLR = 1/2 ln(s2 eP / (eL eR)) + v2 / (2 s2) (tL^2/eL + tR^2/eR -
+        // tP^2/eP) with e = s2 + n v2 and t = S - n mu_mu; the count-only
+        // parts come from pre_decide
         double llr;
-        if (move == kGrow) {
-          llr = split_llr(s2, A->mu_mu, v2, nl, Sl, nr, Sr);
+        if (grow) {
+          const double eL = s2 + nl * v2, eR = s2 + nr * v2;
+          const double r = 1.0 / (eL * eR);
+          llr = 0.5 * log(gs2eP * r) +
+                v2 / (2.0 * s2) * (tL * tL * (eR * r) + tR * tR * (eL * r) - tP * tP * pdP);
         } else {
-          const double nlp = (double)td.cnt[kl], nrp = (double)td.cnt[kr];
-          const double tL = Sl - nlp * A->mu_mu, tR = Sr - nrp * A->mu_mu;
-          const double tP = (Sl + Sr) - (nlp + nrp) * A->mu_mu;
-          llr = sh.pdet + v2 / (2.0 * s2) *
-                              (tL * tL * sh.pdL + tR * tR * sh.pdR - tP * tP * sh.pdP);
+          llr = pdet + v2 / (2.0 * s2) * (tL * tL * pdL + tR * tR * pdR - tP * tP * pdP);
         }
-        const double logr = c.pr.c_prior + (move == kGrow ? llr : -llr);
-        const int acc = c.pr.ln_u < logr ? 1 : 0;
-        const int merged = (move == kGrow && !acc) || (move == kPrune && acc);
+        const double logr = c_prior + (grow ? llr : -llr);
+        const int acc = ln_u < logr ? 1 : 0;
+        const int merged = (grow && !acc) || (move == kPrune && acc);
         sh.dec_logr = logr;
         sh.flags = acc | (merged << 1);
       } else if (wave == 3) {
-        const float vm = (float)((Sl + Sr) * sh.ma + sh.mb);
+        const float vm = (float)((Sl + Sr) * ma + mb);
         sh.newv_m = vm;
         sh.dlt_m[0] = mol - vm;
         sh.dlt_m[1] = mor - vm;
       } else {
-        const int k = wave == 1 ? kl : kr;
-        const double Sk = wave == 1 ? Sl : Sr;
-        const float mo = wave == 1 ? mol : mor;
-        const float v = move == kGrow ? draw_leaf(wave == 1 ? nl : nr, Sk, td.z[k])
-                                      : (float)(Sk * sh.la[k] + sh.lb[k]);
-        sh.cntd[k] = move == kGrow ? (wave == 1 ? nl : nr) : (double)td.cnt[k];
+        const bool left = wave == 1;
+        const int k = left ? kl : kr;
+        const double Sk = left ? Sl : Sr, nk = left ? nl : nr;
+        const float mo = left ? mol : mor;
+        const float v = grow ? draw_child(s2 + nk * v2, Sk, left ? zl : zr)
+                             : (float)(Sk * (left ? lal : lar) + (left ? lbl : lbr));
+        sh.cntd[k] = nk;
         sh.S[k] = Sk;
         sh.newv[k] = v;
         sh.dlt[k] = mo - v;
