@@ -208,6 +208,13 @@ int bart_debug_steps(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace 
  * error bits of all chains (or-ed) in *bits (may be NULL). */
 int bart_status(bart_handle *h, uint32_t *bits);
 
+/* Move statistics of one chain since bart_init (sec. 2.2, "Behavior of the
+ * BART MCMC": acceptance is typically 10-30 %, trees stay small): out[0]
+ * GROW proposed, out[1] PRUNE proposed, out[2] GROW accepted, out[3] PRUNE
+ * accepted, out[4] tree steps, out[5] the sum over tree steps of the leaves
+ * of the tree after the step.  Synchronises the handle's stream. */
+int bart_move_stats(bart_handle *h, int32_t chain, uint64_t *out);
+
 /* Launch shape of the sweep kernel. */
 int bart_launch_info(const bart_handle *h, bart_launch *out);
 

@@ -91,12 +91,14 @@ def lib():
         L.bart_debug_steps.argtypes = [vp, C.c_int32, C.c_uint64, vp]
         L.bart_status.argtypes = [vp, P(C.c_uint32)]
         L.bart_launch_info.argtypes = [vp, P(LaunchInfo)]
+        L.bart_move_stats.argtypes = [vp, C.c_int32, vp]
         L.bart_destroy.argtypes = [vp]
         L.bart_destroy.restype = None
         L.bart_last_error.restype = C.c_char_p
         for f in ["bart_init", "bart_step", "bart_predict", "bart_get_state", "bart_set_state",
                   "bart_debug_steps", "bart_status", "bart_launch_info",
-                  "bart_predict_accumulate", "bart_cutpoints", "bart_bin", "bart_default_hyper"]:
+                  "bart_predict_accumulate", "bart_cutpoints", "bart_bin", "bart_default_hyper",
+                  "bart_move_stats"]:
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -195,6 +197,14 @@ def bart_launch_info(h: int) -> LaunchInfo:
     info = LaunchInfo()
     _check(lib().bart_launch_info(h, C.byref(info)))
     return info
+
+
+def bart_move_stats(h: int, chain: int = 0) -> dict:
+    out = np.zeros(6, np.uint64)
+    _check(lib().bart_move_stats(h, int(chain), out.ctypes.data))
+    keys = ["grow_proposed", "prune_proposed", "grow_accepted", "prune_accepted", "tree_steps",
+            "leaves"]
+    return {k: int(v) for k, v in zip(keys, out)}
 
 
 def bart_destroy(h: int) -> None:
@@ -302,6 +312,9 @@ class Bart:
 
     def launch_info(self) -> LaunchInfo:
         return bart_launch_info(self.h)
+
+    def move_stats(self, chain: int = 0) -> dict:
+        return bart_move_stats(self.h, chain)
 
     # -- state
     def get_state(self, chain: int = 0) -> dict:

@@ -679,6 +679,19 @@ int bart_status(bart_handle *h, uint32_t *bits) {
   return BART_OK;
 }
 
+int bart_move_stats(bart_handle *h, int32_t chain, uint64_t *out) {
+  if (!h || !out) return fail(BART_EINVAL, "NULL argument");
+  if (chain < 0 || chain >= h->nchain)
+    return fail(BART_EINVAL, "chain %d not in [0, %d)", chain, h->nchain);
+  HIP_TRY(hipSetDevice(h->device));
+  Ctl ctl;
+  HIP_TRY(hipMemcpyAsync(&ctl, atc<void>(h, chain, h->lay.ctl), sizeof(Ctl), hipMemcpyDeviceToHost,
+                         h->stream));
+  HIP_TRY(hipStreamSynchronize(h->stream));
+  for (int k = 0; k < 6; ++k) out[k] = ctl.stats[k];
+  return BART_OK;
+}
+
 int bart_launch_info(const bart_handle *h, bart_launch *o) {
   if (!h || !o) return fail(BART_EINVAL, "NULL argument");
   memset(o, 0, sizeof *o);

@@ -401,15 +401,33 @@ __device__ __noinline__ void trace_tree_step(bart_trace *R, Shared &sh, const Ct
 // leaves; each wave sums the segments of the words it needs with the
 // fixed-order DPP tree (nseg <= 32).  Writes sh.flags, dec_logr, and per
 // rank cntd, S, newv, dlt, plus newv_m and dlt_m for a merged move.
+// Move statistics of workgroup 0 (GROW proposed, PRUNE proposed, GROW
+// accepted, PRUNE accepted, tree steps, leaves after the step) for the tree
+// step whose proposal is c and whose decision flags are still in sh.flags.
+// One thread; called where its wave would otherwise wait (the gather of the
+// next tree step, the sigma^2 step, the end of the launch).
+__device__ __forceinline__ void count_move(Shared &sh, const Ctx &c) {
+  const int move = c.pr.move, L = c.pr.L;
+  const int acc = sh.flags & 1, merged = (sh.flags >> 1) & 1;
+  sh.stats[0] += move == kGrow;
+  sh.stats[1] += move == kPrune;
+  sh.stats[2] += move == kGrow && acc;
+  sh.stats[3] += move == kPrune && acc;
+  sh.stats[4] += 1;
+  sh.stats[5] += (uint64_t)(L - merged);
+}
+
 // The parts of tree j's decision that need only counts (sec. 3.3 items 4,
 // 5, 9, 10): for every leaf of known count (all but the children of a GROW)
 // prec = n / s2 + 1 / v2 and the draw mean + z / sqrt(prec) written as
 // S la + lb; the merged leaf of eta; for a PRUNE, the determinant term and
 // the denominators of the likelihood ratio.  Waves 4..7, before the gather.
 __device__ __forceinline__ void pre_decide(const SweepArgs *__restrict__ A, Shared &sh,
-                                           const Ctx &c, const TreeData &td) {
+                                           const Ctx &c, const TreeData &td, int uncounted) {
   const int u = (int)threadIdx.x - 4 * 64;
   if (u < 0) return;
+  // the previous tree step's statistics (its flags are still in sh.flags)
+  if (uncounted >= 0 && threadIdx.x == kBlock - 1) count_move(sh, sh.ctx[uncounted & (kRing - 1)]);
   const int move = c.pr.move, eta = c.pr.eta, L = c.pr.L;
   const int kl = c.pr.rank_l, kr = c.pr.rank_r;
   const double s2 = sh.sigma2, v2 = A->sigma_mu * A->sigma_mu;
@@ -553,7 +571,7 @@ __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Sha
 
 // After the decision of tree j: its owner workgroup (j mod G) stores the
 // final tree (values and counts of its leaves, structure change) and the
-// trace record; workgroup 0 counts the move.
+// trace record.
 __device__ __forceinline__ void finish_tree(const SweepArgs *__restrict__ A, const Launch &Lc,
                                             Shared &sh, const Ctx &c, int j, int64_t s,
                                             int step) {
@@ -586,15 +604,8 @@ __device__ __forceinline__ void finish_tree(const SweepArgs *__restrict__ A, con
     }
     if (Lc.trace) trace_tree_step(Lc.trace + step, sh, c, j, s, H);
   }
-  if (w == 0 && t == 0) {
-    sh.stats[0] += move == kGrow;
-    sh.stats[1] += move == kPrune;
-    sh.stats[2] += move == kGrow && acc;
-    sh.stats[3] += move == kPrune && acc;
-    sh.stats[4] += 1;
-    sh.stats[5] += (uint64_t)(L - merged);
-  }
 }
+
 
 // The sigma^2 step after this workgroup's per-wave sums of squared
 // residuals are in sh.wave_part: the next sweep's proposals (owners) and
@@ -699,6 +710,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     sh.sigma2 = A->ctl->sigma2;
   }
   if (t < 6) sh.stats[t] = 0;
+  int uncounted = -1;  // tree step whose move statistics workgroup 0 has yet to count
 
   // ---- helpers over the pipeline ----
   // issue the index-row and predictor-row loads of tree `tree` (its proposal in ctx)
@@ -890,7 +902,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       //    per-segment partials, then one wave reduces a word over the
       //    segments with the fixed-order DPP tree (nseg <= 32 lanes)
       const int K = L + 1;
-      pre_decide(A, sh, c, sh.td[j & 1]);
+      pre_decide(A, sh, c, sh.td[j & 1], w == 0 ? uncounted : -1);
       const int nseg = gather_polls(A, sh, par, seq, K, L);
       decide_step(A, sh, c, sh.td[j & 1], nseg);
       // stage what later trees need
@@ -933,6 +945,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
         }
       }
       finish_tree(A, Lc, sh, c, j, s, step);
+      uncounted = j;
       // 5. tree j+1: rank table of j+3, partial sums from the updated residuals
       if (more3) build_ranks(A, sh.ctx[(j + 3) & (kRing - 1)]);
       if (more1) {
@@ -945,6 +958,9 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       ++j;
     } else {
       // ================= sigma^2 step (sec. 3.3, "Sampling the error variance")
+      if (w == 0 && t == kBlock - 1 && uncounted >= 0)
+        count_move(sh, sh.ctx[uncounted & (kRing - 1)]);
+      uncounted = -1;
       __syncthreads();  // this workgroup's tree writes are visible to all its threads
       double ssr = 0.0;
 #pragma unroll
@@ -974,6 +990,9 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       q[2] = r[v][2];
       q[3] = r[v][3];
     }
+  if (w == 0 && t == kBlock - 1 && uncounted >= 0)
+    count_move(sh, sh.ctx[uncounted & (kRing - 1)]);
+  __syncthreads();
   if (w == 0 && t < 6) A->ctl->stats[t] += sh.stats[t];
   if (t == 0 && (sh.abort_flag || sh.dev_err))
     atomicOr(&A->ctl->error, (sh.abort_flag ? BART_DEVERR_TIMEOUT : 0u) |
@@ -1016,6 +1035,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     sh.sigma2 = A->ctl->sigma2;
   }
   if (t < 6) sh.stats[t] = 0;
+  int uncounted = -1;  // tree step whose move statistics workgroup 0 has yet to count
 
   // leaf ranks in tree c's larger tree of the 4 points of a chunk (0 for
   // padding); GROW right-count into nr
@@ -1236,18 +1256,22 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       const uint32_t pw3 = load_prop_word(A, j3);
       lds_barrier();
       if (t == L) sh.nr[j & 1] = 0;
-      pre_decide(A, sh, c, sh.td[j & 1]);
+      pre_decide(A, sh, c, sh.td[j & 1], w == 0 ? uncounted : -1);
       const int nseg = gather_polls(A, sh, par, seq, L + 1, L);
       decide_step(A, sh, c, sh.td[j & 1], nseg);
       if (more3 && t < kPropWords) ((uint32_t *)&sh.ctx[(j + 3) & (kRing - 1)].pr)[t] = pw3;
       if (more1) store_tree_data(sh.td[(j + 1) & 1], sh.ctx[(j + 1) & (kRing - 1)], tdn);
       lds_barrier();
       finish_tree(A, Lc, sh, c, j, s, step);
+      uncounted = j;
       if (more3) build_ranks(A, sh.ctx[(j + 3) & (kRing - 1)]);
       have_ssr = j == m - 1;
       pass_all(j, more1 ? j + 1 : -1, have_ssr);
       ++j;
     } else {
+      if (w == 0 && t == kBlock - 1 && uncounted >= 0)
+        count_move(sh, sh.ctx[uncounted & (kRing - 1)]);
+      uncounted = -1;
       __syncthreads();
       if (!have_ssr) pass(-1, -1, true, 0);
       have_ssr = false;
@@ -1257,6 +1281,9 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s);
     }
   }
+  if (w == 0 && t == kBlock - 1 && uncounted >= 0)
+    count_move(sh, sh.ctx[uncounted & (kRing - 1)]);
+  __syncthreads();
   if (w == 0 && t < 6) A->ctl->stats[t] += sh.stats[t];
   if (t == 0 && (sh.abort_flag || sh.dev_err))
     atomicOr(&A->ctl->error, (sh.abort_flag ? BART_DEVERR_TIMEOUT : 0u) |

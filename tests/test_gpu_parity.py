@@ -243,3 +243,29 @@ def test_chains_predict_and_set_state():
         np.testing.assert_array_equal(s1[k], st2[k], err_msg=k)
     assert s1["sigma2"] == st2["sigma2"]
     assert g.status() == 0
+
+
+def test_move_statistics_count_every_step():
+    """bart_move_stats against the per-step records of the same steps: runs
+    that start and end inside a sweep, several launches, several chains."""
+    inp = make_inputs(2, n=8009, p=20, m=25)
+    g = _gpu(inp, nchain=2, launch=ORDINARY)
+    g.step(3, 17)
+    before = [g.move_stats(c) for c in range(2)]
+    assert all(b["tree_steps"] == 3 * inp.m for b in before)
+    n_steps = 2 * (inp.m + 1) + 7
+    tr = g.debug_steps(n_steps, 17)                    # ends inside a sweep
+    tr2 = g.debug_steps(inp.m + 1, 17)                 # starts inside one
+    for c in range(2):
+        recs = np.concatenate([tr[c], tr2[c]])
+        t = recs[recs["kind"] == 0]
+        after = g.move_stats(c)
+        d = {k: after[k] - before[c][k] for k in after}
+        assert d["tree_steps"] == len(t)
+        assert d["grow_proposed"] == int((t["move"] == 1).sum())
+        assert d["prune_proposed"] == int((t["move"] == 2).sum())
+        assert d["grow_accepted"] == int(((t["move"] == 1) & (t["accept"] == 1)).sum())
+        assert d["prune_accepted"] == int(((t["move"] == 2) & (t["accept"] == 1)).sum())
+        merged = ((t["move"] == 1) & (t["accept"] == 0)) | ((t["move"] == 2) & (t["accept"] == 1))
+        assert d["leaves"] == int((t["n_leaves"] - merged).sum())
+    assert g.status() == 0
