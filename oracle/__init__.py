@@ -35,13 +35,15 @@ class Config(C.Structure):
                 ("idx_bytes", C.c_int32), ("fix_sigma2", C.c_int32),
                 ("chain", C.c_int32), ("pad", C.c_int32), ("alpha", C.c_double), ("beta", C.c_double), ("mu_mu", C.c_double),
                 ("sigma_mu", C.c_double), ("nu", C.c_double), ("lam", C.c_double),
-                ("p_grow", C.c_double)]
+                ("p_grow", C.c_double), ("probit", C.c_int32), ("pad2", C.c_int32),
+                ("probit_offset", C.c_double)]
 
 
 class _State(C.Structure):
     _fields_ = [("axis", C.c_void_p), ("cut", C.c_void_p), ("leaf", C.c_void_p),
                 ("idx", C.c_void_p), ("resid", C.c_void_p), ("sigma2", C.c_double),
-                ("sweep", C.c_int64), ("next", C.c_int32)]
+                ("sweep", C.c_int64), ("next", C.c_int32), ("latent", C.c_void_p),
+                ("ybin", C.c_void_p)]
 
 
 TRACE_DTYPE = np.dtype([
@@ -66,6 +68,12 @@ def lib():
         L.oc_philox4x64_10.argtypes = [vp, vp, vp]
         L.oc_normal.argtypes = [u64, u64, u64, u64]
         L.oc_normal.restype = f64
+        L.oc_norm_cdf.argtypes = [f64]
+        L.oc_norm_cdf.restype = f64
+        L.oc_norm_ppf.argtypes = [f64]
+        L.oc_norm_ppf.restype = f64
+        L.oc_latent_draw.argtypes = [f64, i32, f64]
+        L.oc_latent_draw.restype = f64
         L.oc_gamma_draw.argtypes = [u64, u64, f64]
         L.oc_gamma_draw.restype = f64
         L.oc_sigma2_draw.argtypes = [u64, u64, f64, f64, i64, f64]
@@ -97,11 +105,13 @@ def _ptr(a: np.ndarray) -> int:
 
 
 def make_config(n, p, m, D, idx_bytes=1, alpha=0.95, beta=2.0, mu_mu=0.0, sigma_mu=1.0,
-                nu=3.0, lam=1.0, p_grow=0.5, fix_sigma2=False, chain=0) -> Config:
-    """chain selects the random stream: counter word 3 offset by chain * 2^32."""
+                nu=3.0, lam=1.0, p_grow=0.5, fix_sigma2=False, chain=0, probit=False,
+                probit_offset=0.0) -> Config:
+    """chain selects the random stream: counter word 3 offset by chain * 2^32.
+    probit: binary y, latent normals, sigma^2 held at its initial value 1."""
     return Config(int(n), int(p), int(m), int(D), int(idx_bytes), int(bool(fix_sigma2)),
                   int(chain), 0, float(alpha), float(beta), float(mu_mu), float(sigma_mu), float(nu),
-                  float(lam), float(p_grow))
+                  float(lam), float(p_grow), int(bool(probit)), 0, float(probit_offset))
 
 
 def philox(counter, key) -> np.ndarray:
@@ -110,6 +120,18 @@ def philox(counter, key) -> np.ndarray:
     out = np.zeros(4, dtype=np.uint64)
     lib().oc_philox4x64_10(_ptr(ctr), _ptr(k), _ptr(out))
     return out
+
+
+def norm_cdf(x) -> float:
+    return lib().oc_norm_cdf(float(x))
+
+
+def norm_ppf(p) -> float:
+    return lib().oc_norm_ppf(float(p))
+
+
+def latent_draw(f, y, u) -> float:
+    return lib().oc_latent_draw(float(f), int(y), float(u))
 
 
 def normal(seed, s, j, slot) -> float:
@@ -213,8 +235,18 @@ class Chain:
         self.sigma2 = float(sigma2)
         self.sweep = 0
         self.next = 0
+        self.latent = self.ybin = None
+        if cfg.probit:
+            # binary y = [y_c > 0]; latents start at +-1 on their side of 0,
+            # residuals at z - offset (the trees are all zero); sigma^2 = 1
+            self.ybin = (np.asarray(y_c[:n]) > 0).astype(np.uint8)
+            self.latent = np.where(self.ybin == 1, 1.0, -1.0).astype(np.float32)
+            self.resid = (self.latent.astype(np.float64) - cfg.probit_offset).astype(np.float32)
+            self.sigma2 = 1.0
 
-    def load(self, axis, cut, leaf, idx, resid, sigma2, sweep, next_step=0):
+    def load(self, axis, cut, leaf, idx, resid, sigma2, sweep, next_step=0, latent=None):
+        if latent is not None:
+            self.latent[...] = latent
         self.axis[...] = axis
         self.cut[...] = cut
         self.leaf[...] = leaf
@@ -226,7 +258,9 @@ class Chain:
 
     def _state(self) -> _State:
         return _State(_ptr(self.axis), _ptr(self.cut), _ptr(self.leaf), _ptr(self.idx),
-                      _ptr(self.resid), self.sigma2, self.sweep, self.next)
+                      _ptr(self.resid), self.sigma2, self.sweep, self.next,
+                      None if self.latent is None else _ptr(self.latent),
+                      None if self.ybin is None else _ptr(self.ybin))
 
     def _pull(self, st: _State):
         self.sigma2 = st.sigma2

@@ -21,12 +21,16 @@
  */
 #include "bart_oracle.h"
 
+#include <float.h>
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
 
 #ifndef M_PI
 #define M_PI 3.14159265358979323846
+#endif
+#ifndef M_SQRT1_2
+#define M_SQRT1_2 0.70710678118654752440
 #endif
 
 /* ------------------------------------------------------------------ */
@@ -138,6 +142,45 @@ static double sigma2_of(uint64_t seed, uint32_t chain, uint64_t s, double nu, do
 double oc_sigma2_draw(uint64_t seed, uint64_t s, double nu, double lambda, int64_t n,
                       double ssr) {
   return sigma2_of(seed, 0, s, nu, lambda, n, ssr);
+}
+
+/* ------------------------------------------------------------------ */
+/* Probit model for binary y (sec. 5, "Mild limitations": binary outcomes
+ * follow the BART literature), by the latent-variable augmentation of
+ * Albert and Chib (1993): z_i ~ N(f(x_i), 1), y_i = 1 iff z_i > 0, so given
+ * the trees z_i is a normal truncated to the side its y_i fixes, and given
+ * the z_i the trees are fitted to z with sigma^2 = 1.                   */
+
+double oc_norm_cdf(double x) { return 0.5 * erfc(-x * M_SQRT1_2); }
+
+/* Inverse of oc_norm_cdf.  Solved in the lower tail, where the cdf is
+ * accurate, for q = min(p, 1 - p) (1 - p is exact for p >= 1/2) and
+ * reflected: a start from the rational approximation of Abramowitz and
+ * Stegun 26.2.23 (|error| < 4.5e-4), then Newton steps on oc_norm_cdf until
+ * they stop moving the root. */
+double oc_norm_ppf(double p) {
+  if (!(p > 0.0)) return -INFINITY;
+  if (!(p < 1.0)) return INFINITY;
+  double q = p < 0.5 ? p : 1.0 - p;
+  double t = sqrt(-2.0 * log(q));
+  double x = -(t - (2.515517 + 0.802853 * t + 0.010328 * t * t) /
+                       (1.0 + 1.432788 * t + 0.189269 * t * t + 0.001308 * t * t * t));
+  for (int it = 0; it < 50; it++) {
+    double dens = exp(-0.5 * x * x) / sqrt(2.0 * M_PI);
+    double dx = (oc_norm_cdf(x) - q) / dens;
+    x -= dx;
+    if (fabs(dx) <= 1e-15 * (1.0 + fabs(x))) break;
+  }
+  return p < 0.5 ? x : -x;
+}
+
+/* z | f, y ~ N(f, 1) truncated to z > 0 (y = 1) or z <= 0 (y = 0), by
+ * inversion on the allowed side: with e = z - f, P(e < -f) = Phi(-f), so
+ * y = 0 takes e = Phi^-1(u Phi(-f)) and y = 1 takes e = -Phi^-1(u Phi(f)). */
+double oc_latent_draw(double f, int32_t y, double u) {
+  double p = u * oc_norm_cdf(y ? f : -f);
+  if (p < 1e-300) p = 1e-300;
+  return y ? f - oc_norm_ppf(p) : f + oc_norm_ppf(p);
 }
 
 /* ------------------------------------------------------------------ */
@@ -603,10 +646,31 @@ static void tree_step(const oc_config *c, const int32_t *n_cuts, const uint8_t *
   free(fresh);
 }
 
+/* Probit: new latents given the trees, f_i = z_i - r_i (offset included),
+ * one uniform per observation from block (s, 2^64 - 2, 3, c 2^32 + i/4),
+ * word i mod 4.  The latent is stored in f32 on its side of 0 and the
+ * residual follows it: r_i = z_i - f_i. */
+static void latent_step(const oc_config *c, oc_state *st, uint64_t seed) {
+  uint64_t w[4];
+  for (int64_t i = 0; i < c->n; i++) {
+    if ((i & 3) == 0) block(seed, (uint32_t)c->chain, (uint64_t)st->sweep, ~1ULL, 3, (uint64_t)(i >> 2), w);
+    double u = u01(w[i & 3]);
+    double f = (double)st->latent[i] - (double)st->resid[i];
+    int y = st->ybin[i] != 0;
+    float z = (float)oc_latent_draw(f, y, u);
+    if (y && !(z > 0.0f)) z = FLT_MIN;
+    if (!y && z > 0.0f) z = 0.0f;
+    st->latent[i] = z;
+    st->resid[i] = (float)((double)z - f);
+  }
+}
+
 static void sigma_step(const oc_config *c, oc_state *st, uint64_t seed, oc_trace *tr) {
   double ssr = 0.0;
   for (int64_t i = 0; i < c->n; i++) ssr += (double)st->resid[i] * (double)st->resid[i];
-  if (!c->fix_sigma2)
+  if (c->probit)
+    latent_step(c, st, seed);
+  else if (!c->fix_sigma2)
     st->sigma2 = sigma2_of(seed, (uint32_t)c->chain, (uint64_t)st->sweep, c->nu, c->lambda, c->n,
                            ssr);
   if (tr) {

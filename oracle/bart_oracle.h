@@ -37,6 +37,9 @@ typedef struct {
   double mu_mu, sigma_mu;         /* leaf prior N(mu_mu, sigma_mu^2) (sec. 2.1) */
   double nu, lambda;              /* lambda*nu/sigma^2 ~ chi^2_nu (eq. bartdef) */
   double p_grow;                  /* P(GROW) when both moves are possible */
+  int32_t probit;                 /* 1: binary y, latent-variable probit model */
+  int32_t pad2;
+  double probit_offset;           /* probit: f(x) = offset + sum of trees */
 } oc_config;
 
 /* Mutable chain state.  All arrays are caller-owned. */
@@ -49,6 +52,8 @@ typedef struct {
   double sigma2;
   int64_t sweep;    /* index s of the sweep in progress */
   int32_t next;     /* next step of sweep s: 0..m-1 tree steps, m = sigma^2 step */
+  float *latent;    /* probit: [n] latent z_i (y_i = 1 iff z_i > 0) */
+  const uint8_t *ybin; /* probit: [n] binary response */
 } oc_state;
 
 /* Per-step trace record (4224 bytes). */
@@ -71,6 +76,9 @@ typedef struct {
 } oc_trace;
 
 void oc_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]);
+double oc_norm_cdf(double x);
+double oc_norm_ppf(double p);
+double oc_latent_draw(double f, int32_t y, double u);
 double oc_normal(uint64_t seed, uint64_t s, uint64_t j, uint64_t slot);
 double oc_sigma2_draw(uint64_t seed, uint64_t s, double nu, double lambda, int64_t n,
                       double ssr);

@@ -532,3 +532,93 @@ def test_chains_are_independent_streams():
         for b in range(a + 1, 3):
             assert not np.array_equal(out[a][0], out[b][0])
             assert out[a][1] != out[b][1]
+
+
+# --------------------------------------------------------------------------
+# probit model (binary y by latent normals)
+
+def test_normal_cdf_and_inverse():
+    # the tail is conditioned like x^2 eps in the argument of erfc
+    x = np.concatenate([np.linspace(-37, 8, 400), [0.0]])
+    np.testing.assert_allclose([oracle.norm_cdf(v) for v in x], stats.norm.cdf(x),
+                               rtol=2e-16 * (1 + 37.0**2), atol=0)
+    p = np.concatenate([np.logspace(-300, -1, 150), np.linspace(0.01, 0.99, 99),
+                        [1 - 1e-12, 1 - 2**-53]])
+    got = np.array([oracle.norm_ppf(v) for v in p])
+    np.testing.assert_allclose(got, stats.norm.ppf(p), rtol=2e-15, atol=2e-15)
+
+
+@pytest.mark.parametrize("f", [-3.0, -0.4, 0.0, 1.7, 6.0])
+def test_latent_draw_is_the_truncated_normal_quantile(f):
+    """z | f, y is N(f, 1) truncated to z <= 0 (y = 0) or z > 0 (y = 1); the
+    draw at uniform u is that law's quantile (at u for y = 0, at 1 - u for
+    y = 1, the reflected inversion)."""
+    u = np.linspace(0.001, 0.999, 57)
+    lo = stats.truncnorm(-np.inf, -f, loc=f)
+    hi = stats.truncnorm(-f, np.inf, loc=f)
+    z0 = np.array([oracle.latent_draw(f, 0, v) for v in u])
+    z1 = np.array([oracle.latent_draw(f, 1, v) for v in u])
+    assert (z0 <= 0).all() and (z1 > 0).all()
+    np.testing.assert_allclose(z0, lo.ppf(u), rtol=1e-9, atol=1e-9)
+    np.testing.assert_allclose(z1, hi.ppf(1 - u), rtol=1e-9, atol=1e-9)
+
+
+@pytest.mark.parametrize("m", [1, 3])
+def test_probit_no_split_model_matches_quadrature(m):
+    """alpha = 0: y_i ~ Bernoulli(Phi(offset + sum_j mu_j)).  The latent Gibbs
+    chain over the m root leaves must reproduce the posterior of
+    f = sum mu_j under f ~ N(m mu_mu, m sigma_mu^2), by quadrature."""
+    rng = np.random.default_rng(5)
+    n = 30
+    yb = (rng.random(n) < 0.7).astype(np.float32)
+    mu_mu, sigma_mu, off = 0.05, 0.6, 0.2
+    X = np.zeros((1, n), np.uint8)
+    cfg = oracle.make_config(n=n, p=1, m=m, D=3, alpha=0.0, beta=2.0, mu_mu=mu_mu,
+                             sigma_mu=sigma_mu, probit=True, probit_offset=off)
+    ch = oracle.Chain(cfg, X, [3], yb, 1.0)
+    assert ch.sigma2 == 1.0
+    ch.sweeps(23, 200)
+    fs = []
+    for _ in range(40000):
+        ch.run(23, m + 1)
+        fs.append(float(ch.leaf[:, 1].astype(np.float64).sum()))
+        assert ((ch.latent > 0) == (yb > 0)).all()
+    fs = np.array(fs)
+    assert ch.sigma2 == 1.0
+    fg = np.linspace(-4.0, 4.0, 4001)
+    k = int(yb.sum())
+    L = (stats.norm(m * mu_mu, math.sqrt(m) * sigma_mu).logpdf(fg)
+         + k * stats.norm.logcdf(off + fg) + (n - k) * stats.norm.logcdf(-(off + fg)))
+    W = np.exp(L - L.max())
+    W /= W.sum()
+    Ef = (W * fg).sum()
+    sdf = math.sqrt((W * (fg - Ef) ** 2).sum())
+    assert abs(fs.mean() - Ef) < 6 * sdf / math.sqrt(4000), (fs.mean(), Ef)
+    assert abs(fs.std() / sdf - 1) < 0.1, (fs.std(), sdf)
+
+
+def test_probit_chain_recovers_class_probabilities():
+    """Binary data from P(y = 1 | x) = Phi(g(x)); the posterior mean of
+    Phi(f) tracks the true probabilities."""
+    from paper_2410_23244_amd.inputs import bin_column, cutpoints
+
+    rng = np.random.default_rng(8)
+    n, p, m = 3000, 4, 50
+    X = rng.random((p, n)).astype(np.float32)
+    g = 1.5 * np.sin(2 * np.pi * X[0]) + 2.0 * (X[1] - 0.5)
+    yb = (rng.random(n) < stats.norm.cdf(g)).astype(np.float32)
+    Xb = np.stack([bin_column(X[a], cutpoints(X[a], 63, "quantile")) for a in range(p)])
+    off = float(stats.norm.ppf(yb.mean()))
+    cfg = oracle.make_config(n=n, p=p, m=m, D=6, mu_mu=0.0, sigma_mu=3.0 / (2 * math.sqrt(m)),
+                             probit=True, probit_offset=off)
+    ch = oracle.Chain(cfg, Xb, np.full(p, 63, np.int32), yb, 1.0)
+    ch.sweeps(4, 200)
+    acc = np.zeros(n)
+    for _ in range(200):
+        ch.sweeps(4, 1)
+        acc += stats.norm.cdf(ch.predict(Xb, off).astype(np.float64))
+    prob = acc / 200
+    err = np.abs(prob - stats.norm.cdf(g))
+    assert err.mean() < 0.06, err.mean()
+    # beats the constant predictor by far
+    assert err.mean() < 0.3 * np.abs(yb.mean() - stats.norm.cdf(g)).mean()
