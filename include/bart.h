@@ -94,7 +94,7 @@ typedef struct {
   int32_t residency;  /* BART_RESID_AUTO, BART_RESID_REGISTERS or BART_RESID_STREAMED */
   int32_t nchain;     /* independent chains: 0 or 1 = one, else in [1, 256] (at most
                          one per compute unit) */
-  int32_t reserved;   /* set to 0 */
+  int32_t probit;     /* 0: regression; 1: binary y by the probit model (below) */
   int64_t x_stride;   /* elements between predictor rows of X_b: >= n, multiple of 16 */
   double alpha, beta; /* tree prior P_d = alpha (1+d)^-beta, alpha in [0,1], beta >= 0 */
   double mu_mu;       /* leaf prior mean (sec. 2.1 "Prior over leaf values") */
@@ -102,7 +102,18 @@ typedef struct {
   double nu, lambda;  /* error-variance prior lambda nu / sigma^2 ~ chi^2_nu, > 0 */
   double sigma2_init; /* initial sigma^2, > 0 */
   double p_grow;      /* P(GROW) when both GROW and PRUNE are possible, in [0,1] */
+  double probit_offset; /* probit: f(x) = probit_offset + sum of trees, finite */
 } bart_config;
+
+/* Probit model (binary outcomes, which the paper leaves to the BART
+ * literature in sec. 5, "Mild limitations"): P(y = 1 | x) = Phi(f(x)), fitted
+ * with latent z_i ~ N(f(x_i), 1), y_i = 1 iff z_i > 0 (Albert and Chib,
+ * 1993).  bart_init reads y_i = [y_c[i] > 0], starts every latent at +-1 on
+ * its side of 0 and the residuals at z_i - probit_offset; sigma^2 stays 1
+ * (sigma2_init, nu and lambda are not used).  The step that ends a sweep
+ * draws every z_i from N(f_i, 1) truncated to its side of 0, by inversion
+ * of the normal cdf with one uniform per observation, and moves the residual
+ * with it.  bart_predict gives f, to be passed through Phi. */
 
 /* State of one chain, in the layouts above.  For bart_get_state the array
  * pointers are caller-owned device buffers that receive copies; for
@@ -118,6 +129,7 @@ typedef struct {
   int64_t sweep;  /* index of the sweep in progress */
   int32_t next;   /* next step of that sweep: 0..ntree-1 trees, ntree = sigma^2 */
   int32_t chain;  /* in [0, nchain) */
+  float *latent;  /* probit: [n] latents z_i (NULL: not copied); ignored otherwise */
 } bart_state;
 
 /* Per-step record written by bart_debug_steps (4224 bytes).  Slots are heap

@@ -36,16 +36,18 @@ class Config(C.Structure):
     _fields_ = [("n", C.c_int32), ("p", C.c_int32), ("ntree", C.c_int32),
                 ("max_depth", C.c_int32), ("idx_bytes", C.c_int32), ("grid", C.c_int32),
                 ("launch", C.c_int32), ("residency", C.c_int32), ("nchain", C.c_int32),
-                ("reserved", C.c_int32), ("x_stride", C.c_int64),
+                ("probit", C.c_int32), ("x_stride", C.c_int64),
                 ("alpha", C.c_double), ("beta", C.c_double),
                 ("mu_mu", C.c_double), ("sigma_mu", C.c_double), ("nu", C.c_double),
-                ("lam", C.c_double), ("sigma2_init", C.c_double), ("p_grow", C.c_double)]
+                ("lam", C.c_double), ("sigma2_init", C.c_double), ("p_grow", C.c_double),
+                ("probit_offset", C.c_double)]
 
 
 class State(C.Structure):
     _fields_ = [("axis", C.c_void_p), ("cut", C.c_void_p), ("leaf", C.c_void_p),
                 ("idx", C.c_void_p), ("resid", C.c_void_p), ("sigma2", C.c_double),
-                ("sweep", C.c_int64), ("next", C.c_int32), ("chain", C.c_int32)]
+                ("sweep", C.c_int64), ("next", C.c_int32), ("chain", C.c_int32),
+                ("latent", C.c_void_p)]
 
 
 class LaunchInfo(C.Structure):
@@ -231,7 +233,7 @@ class Bart:
                  mu_mu: float = 0.0, sigma_mu: float = 1.0, nu: float = 3.0,
                  lam: float = 1.0, sigma2_init: float = 1.0, p_grow: float = 0.5,
                  grid: int = 0, launch: int = 0, residency: int = 0, nchain: int = 1,
-                 device: str = "cuda"):
+                 probit: bool = False, probit_offset: float = 0.0, device: str = "cuda"):
         import torch
 
         if not torch.cuda.is_available():
@@ -250,9 +252,10 @@ class Bart:
         self.y = torch.from_numpy(np.ascontiguousarray(yn, dtype=np.float32)).to(self.device)
         self.n_cuts = np.ascontiguousarray(n_cuts, dtype=np.int32)
         self.nchain = nchain
-        self.cfg = Config(n, p, ntree, max_depth, idx_bytes, grid, launch, residency, nchain, 0,
-                          self.x_stride, alpha, beta, mu_mu, sigma_mu, nu, lam, sigma2_init,
-                          p_grow)
+        self.probit = bool(probit)
+        self.cfg = Config(n, p, ntree, max_depth, idx_bytes, grid, launch, residency, nchain,
+                          int(self.probit), self.x_stride, alpha, beta, mu_mu, sigma_mu, nu, lam,
+                          sigma2_init, p_grow, probit_offset)
         nbytes = bart_workspace_bytes(self.cfg)
         if nbytes == 0:
             raise BartError(BART_EINVAL, "invalid configuration")
@@ -326,8 +329,11 @@ class Bart:
                     leaf=torch.empty((m, 2 * H), dtype=torch.float32, device=self.device),
                     idx=torch.empty((m, n), dtype=it, device=self.device),
                     resid=torch.empty(n, dtype=torch.float32, device=self.device))
+        if self.probit:
+            bufs["latent"] = torch.empty(n, dtype=torch.float32, device=self.device)
         st = State(bufs["axis"].data_ptr(), bufs["cut"].data_ptr(), bufs["leaf"].data_ptr(),
-                   bufs["idx"].data_ptr(), bufs["resid"].data_ptr(), 0.0, 0, 0, int(chain))
+                   bufs["idx"].data_ptr(), bufs["resid"].data_ptr(), 0.0, 0, 0, int(chain),
+                   bufs["latent"].data_ptr() if self.probit else None)
         bart_get_state(self.h, st)
         out = {k: v.cpu().numpy() for k, v in bufs.items()}
         out["axis"] = out["axis"].view(np.uint16)
@@ -338,21 +344,23 @@ class Bart:
 
     def sigma2(self, chain: int = 0) -> float:
         """Current sigma^2 of a chain (no array copies)."""
-        st = State(None, None, None, None, None, 0.0, 0, 0, int(chain))
+        st = State(None, None, None, None, None, 0.0, 0, 0, int(chain), None)
         bart_get_state(self.h, st)
         return st.sigma2
 
     def set_state(self, s: dict, chain: int = 0) -> None:
         torch = self.torch
         dev = {}
-        for k in ["axis", "cut", "leaf", "idx", "resid"]:
+        keys = ["axis", "cut", "leaf", "idx", "resid"] + (["latent"] if self.probit else [])
+        for k in keys:
             a = np.ascontiguousarray(s[k])
             if a.dtype == np.uint16:
                 a = a.view(np.int16)
             dev[k] = torch.from_numpy(a).to(self.device)
         st = State(dev["axis"].data_ptr(), dev["cut"].data_ptr(), dev["leaf"].data_ptr(),
                    dev["idx"].data_ptr(), dev["resid"].data_ptr(), float(s["sigma2"]),
-                   int(s["sweep"]), int(s.get("next", 0)), int(chain))
+                   int(s["sweep"]), int(s.get("next", 0)), int(chain),
+                   dev["latent"].data_ptr() if self.probit else None)
         bart_set_state(self.h, st)
         self.stream.synchronize()
 
@@ -369,12 +377,15 @@ class Bart:
 
 
 def from_inputs(inp, grid: int = 0, launch: int = 0, residency: int = 0, nchain: int = 1) -> Bart:
-    """Chains for a generated workload (paper_2410_23244_amd.inputs.Inputs)."""
+    """Chains for a generated workload (paper_2410_23244_amd.inputs.Inputs);
+    a probit workload gives probit chains with its offset."""
     h = inp.hyper
     return Bart(inp.X_b, inp.y_c, inp.n_cuts, ntree=inp.m, max_depth=inp.D,
                 idx_bytes=inp.idx_bytes, alpha=h.alpha, beta=h.beta, mu_mu=h.mu_mu,
                 sigma_mu=h.sigma_mu, nu=h.nu, lam=h.lam, sigma2_init=h.sigma2_init,
-                p_grow=h.p_grow, grid=grid, launch=launch, residency=residency, nchain=nchain)
+                p_grow=h.p_grow, grid=grid, launch=launch, residency=residency, nchain=nchain,
+                probit=getattr(inp, "probit", False),
+                probit_offset=inp.offset if getattr(inp, "probit", False) else 0.0)
 
 
 class Regressor:

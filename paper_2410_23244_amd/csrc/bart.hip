@@ -45,8 +45,8 @@ struct Layout {
   int64_t n_pad;
   int32_t nchain;
   int32_t gcap;  // workgroups per chain the mailboxes are sized for
-  size_t resid, idx, axis, cut, leaf, count, prop, z, ctl, pub, chain_bytes;
-  size_t n_cuts, nz_list, nz_rank, args, total;
+  size_t resid, idx, axis, cut, leaf, count, prop, z, ctl, pub, latent, chain_bytes;
+  size_t n_cuts, nz_list, nz_rank, ybin, args, total;
 };
 
 int nchain_of(const bart_config &c) { return c.nchain > 0 ? c.nchain : 1; }
@@ -76,6 +76,8 @@ const char *check_config(const bart_config *c) {
   if (!(c->sigma2_init > 0.0 && std::isfinite(c->sigma2_init))) return "sigma2_init must be > 0";
   if (!(c->p_grow >= 0.0 && c->p_grow <= 1.0)) return "p_grow must be in [0, 1]";
   if (c->nu + (double)c->n < 2.0) return "nu + n must be >= 2 (gamma shape >= 1)";
+  if (c->probit != 0 && c->probit != 1) return "probit must be 0 or 1";
+  if (c->probit && !std::isfinite(c->probit_offset)) return "probit_offset must be finite";
   return nullptr;
 }
 
@@ -102,11 +104,13 @@ Layout make_layout(const bart_config &c) {
   L.z = take(sizeof(double) * 2 * m * 2 * H);
   L.ctl = take(sizeof(Ctl));
   L.pub = take(sizeof(uint64_t) * 2 * L.gcap * kStride);
+  L.latent = take(c.probit ? sizeof(float) * L.n_pad : 0);
   L.chain_bytes = o;
   o = L.chain_bytes * L.nchain;
   L.n_cuts = take(sizeof(int32_t) * c.p);
   L.nz_list = take(sizeof(int32_t) * c.p);
   L.nz_rank = take(sizeof(int32_t) * c.p);
+  L.ybin = take(c.probit ? L.n_pad : 0);
   L.args = take(sizeof(SweepArgs) * L.nchain);
   L.total = o;
   return L;
@@ -138,6 +142,21 @@ __global__ void k_init_resid(float *resid, const float *y, int64_t n, int64_t n_
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n_pad;
        i += (int64_t)gridDim.x * blockDim.x)
     resid[i] = i < n ? y[i] : 0.f;
+}
+
+// Probit start: y_i = [y_c[i] > 0], latent z_i = +-1 on its side of 0,
+// residual z_i - offset (every tree is zero); padding gets y = 0, z = r = 0.
+__global__ void k_init_probit(const float *y, uint8_t *ybin, float *latent, float *resid,
+                              double offset, int64_t n, int64_t n_pad) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n_pad;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const bool valid = i < n;
+    const int yb = valid && y[i] > 0.f;
+    const float z = valid ? (yb ? 1.f : -1.f) : 0.f;
+    if (ybin) ybin[i] = (uint8_t)yb;
+    latent[i] = z;
+    resid[i] = valid ? (float)((double)z - offset) : 0.f;
+  }
 }
 
 __global__ void k_fill_idx(uint8_t *idx, int64_t entries, int ib) {
@@ -346,6 +365,10 @@ SweepArgs make_args(bart_handle *h, int ch) {
   A.ctl = atc<Ctl>(h, ch, h->lay.ctl);
   A.pub = atc<uint64_t>(h, ch, h->lay.pub);
   A.chain = ch;
+  A.probit = c.probit;
+  A.probit_offset = c.probit_offset;
+  A.latent = c.probit ? atc<float>(h, ch, h->lay.latent) : nullptr;
+  A.ybin = c.probit ? at<uint8_t>(h, h->lay.ybin) : nullptr;
   A.n = c.n;
   A.p = c.p;
   A.m = c.ntree;
@@ -525,7 +548,12 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
       k_init_trees<<<grid_for((int64_t)cfg->ntree * 2 * h->H, 256), 256, 0, st>>>(
           atc<uint16_t>(h, c, lay.axis), atc<uint8_t>(h, c, lay.cut), atc<float>(h, c, lay.leaf),
           atc<int32_t>(h, c, lay.count), cfg->ntree, h->H, cfg->n);
-      k_set_ctl<<<1, 64, 0, st>>>(atc<Ctl>(h, c, lay.ctl), cfg->sigma2_init, 0, 1);
+      if (cfg->probit)
+        k_init_probit<<<grid_for(lay.n_pad, 256), 256, 0, st>>>(
+            y_c, c == 0 ? at<uint8_t>(h, lay.ybin) : nullptr, atc<float>(h, c, lay.latent),
+            atc<float>(h, c, lay.resid), cfg->probit_offset, cfg->n, lay.n_pad);
+      k_set_ctl<<<1, 64, 0, st>>>(atc<Ctl>(h, c, lay.ctl), cfg->probit ? 1.0 : cfg->sigma2_init,
+                                  0, 1);
       HIP_TRY(hipGetLastError());
       args[c] = make_args(h, c);
     }
@@ -618,6 +646,9 @@ int bart_get_state(bart_handle *h, bart_state *d) {
   if (d->resid)
     HIP_TRY(hipMemcpyAsync(d->resid, atc<void>(h, ch, L.resid), 4 * (size_t)c.n,
                            hipMemcpyDeviceToDevice, st));
+  if (d->latent && c.probit)
+    HIP_TRY(hipMemcpyAsync(d->latent, atc<void>(h, ch, L.latent), 4 * (size_t)c.n,
+                           hipMemcpyDeviceToDevice, st));
   Ctl ctl;
   HIP_TRY(hipMemcpyAsync(&ctl, atc<void>(h, ch, L.ctl), sizeof(Ctl), hipMemcpyDeviceToHost, st));
   HIP_TRY(hipStreamSynchronize(st));
@@ -637,6 +668,7 @@ int bart_set_state(bart_handle *h, const bart_state *s) {
     return fail(BART_EINVAL, "chain %d not in [0, %d)", ch, h->nchain);
   if (!(s->sigma2 > 0.0 && std::isfinite(s->sigma2))) return fail(BART_EINVAL, "sigma2 must be > 0");
   if (s->sweep < 0 || s->next < 0 || s->next > c.ntree) return fail(BART_EINVAL, "bad position");
+  if (c.probit && !s->latent) return fail(BART_EINVAL, "a probit state needs its latents");
   HIP_TRY(hipSetDevice(h->device));
   const size_t m = c.ntree, H = h->H;
   hipStream_t st = h->stream;
@@ -650,6 +682,9 @@ int bart_set_state(bart_handle *h, const bart_state *s) {
                            hipMemcpyDeviceToDevice, st));
   HIP_TRY(hipMemcpyAsync(atc<void>(h, ch, L.resid), s->resid, 4 * (size_t)c.n,
                          hipMemcpyDeviceToDevice, st));
+  if (c.probit)
+    HIP_TRY(hipMemcpyAsync(atc<void>(h, ch, L.latent), s->latent, 4 * (size_t)c.n,
+                           hipMemcpyDeviceToDevice, st));
   const int64_t cells = (int64_t)m * 2 * H;
   k_zero_i32<<<grid_for(cells, 256), 256, 0, st>>>(atc<int32_t>(h, ch, L.count), cells);
   dim3 g(std::min<int64_t>(((int64_t)c.n + 1023) / 1024, 64), (unsigned)m);

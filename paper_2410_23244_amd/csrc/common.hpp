@@ -73,6 +73,10 @@ struct SweepArgs {
   int32_t n, p, m, D, H, p_nz, G, chunks;
   int32_t cpt;    // chunks of 4 observations per thread
   int32_t chain;  // index of this chain in the launch
+  float *latent;        // probit: [n_pad] latents of this chain
+  const uint8_t *ybin;  // probit: [n_pad] binary response (shared)
+  int32_t probit, pad2_;
+  double probit_offset;
   double alpha, beta, mu_mu, sigma_mu, nu, lambda, p_grow;
 };
 

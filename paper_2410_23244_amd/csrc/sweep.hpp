@@ -279,6 +279,41 @@ __device__ __noinline__ double draw_sigma2(const SweepArgs *__restrict__ A, uint
   return scale / gamma_mt(key, (uint64_t)s, shape);
 }
 
+// Probit latent of one observation (sec. 5 "Mild limitations"; Albert and
+// Chib 1993): z ~ N(f, 1) truncated to z > 0 (y = 1) or z <= 0 (y = 0), by
+// inversion on the allowed side, stored in f32 on that side; the residual
+// moves with it, r = z - f.  Returns (new z, new r).  Not inlined: the
+// normal cdf and its inverse are long, and this runs once per sweep.
+__device__ __noinline__ float2 latent_update(double u, uint32_t y, float z, float r) {
+  const double f = (double)z - (double)r;
+  double p = u * normcdf(y ? f : -f);
+  p = p < 1e-300 ? 1e-300 : p;
+  float zn = (float)(y ? f - normcdfinv(p) : f + normcdfinv(p));
+  if (y && !(zn > 0.f)) zn = 1.17549435e-38f;  // smallest normal f32
+  if (!y && zn > 0.f) zn = 0.f;
+  return make_float2(zn, (float)((double)zn - f));
+}
+
+// Latents of the 4 observations of chunk ch (those set in ok) after sweep s:
+// one Philox block (s, 2^64 - 2, 3, chunk) per chunk, word b for point b.
+__device__ __forceinline__ void latent_chunk(const SweepArgs *__restrict__ A, uint64_t seed,
+                                             int64_t s, int32_t ch, uint32_t ok, float (&r)[4]) {
+  const gptr<float> zp = gbl(A->latent) + 4 * (int64_t)ch;
+  const uint32_t yb = gbl((const uint32_t *)A->ybin)[ch];
+  const Block bl = draw(chain_key(seed, A->chain), (uint64_t)s, ~1ull, 3, (uint64_t)ch);
+  const uint64_t wd[4] = {bl.w0, bl.w1, bl.w2, bl.w3};
+  float z[4] = {zp[0], zp[1], zp[2], zp[3]};
+#pragma unroll
+  for (int b = 0; b < 4; ++b)
+    if ((ok >> b) & 1u) {
+      const float2 zr = latent_update(unit(wd[b]), (yb >> (8 * b)) & 1u, z[b], r[b]);
+      z[b] = zr.x;
+      r[b] = zr.y;
+    }
+#pragma unroll
+  for (int b = 0; b < 4; ++b) zp[b] = z[b];
+}
+
 // Post words 0..K-1 (this workgroup's mailbox in buffer par).
 __device__ __forceinline__ uint64_t *mailbox(const SweepArgs *__restrict__ A, int par, int g) {
   return A->pub + ((int64_t)par * A->G + g) * kStride;
@@ -633,7 +668,8 @@ __device__ __forceinline__ void sigma2_tail(const SweepArgs *__restrict__ A, con
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   if (t == 0) {
     const double ssr_all = sh.tot[0];
-    const double s2 = draw_sigma2(A, seed, s, ssr_all);
+    // the probit model holds sigma^2 at 1 and draws latents instead
+    const double s2 = A->probit ? sh.sigma2 : draw_sigma2(A, seed, s, ssr_all);
     sh.sigma2 = s2;
     if (w == 0) {
       A->ctl->sigma2 = s2;
@@ -973,6 +1009,10 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       ssr = wave_total63(ssr);
       if (lane == 63) sh.wave_part[wave] = ssr;
       sigma2_tail(A, Lc, sh, s, step, seq, par);
+      if (A->probit)
+#pragma unroll
+        for (int v = 0; v < V; ++v)
+          if (okm[v]) latent_chunk(A, seed, s, (w * V + v) * kBlock + t, okm[v], r[v]);
       j = 0;
       ++s;
       if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s);
@@ -1276,6 +1316,19 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       if (!have_ssr) pass(-1, -1, true, 0);
       have_ssr = false;
       sigma2_tail(A, Lc, sh, s, step, seq, par);
+      if (A->probit) {
+        const gptr<f32x4> res = gbl((f32x4 *)A->resid);
+        for (int i0 = 0; i0 < cpt; ++i0) {
+          const int32_t ch = (w * cpt + i0) * kBlock + t;
+          if (ch >= A->chunks) break;
+          const int32_t rem = A->n - 4 * ch;
+          const uint32_t ok = rem >= 4 ? 15u : ((1u << rem) - 1u);
+          const f32x4 rv = res[ch];
+          float r4[4] = {rv[0], rv[1], rv[2], rv[3]};
+          latent_chunk(A, seed, s, ch, ok, r4);
+          res[ch] = f32x4{r4[0], r4[1], r4[2], r4[3]};
+        }
+      }
       j = 0;
       ++s;
       if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s);

@@ -74,6 +74,7 @@ class Inputs:
     offset: float              # mean of y (fp64), added back by predict
     hyper: Hyper = field(default_factory=Hyper)
     seed: int = 0
+    probit: bool = False       # y_c holds binary y (0/1); offset is the probit offset
 
     @property
     def workload(self) -> str:
@@ -207,3 +208,34 @@ def rmse_dgp(n_train: int, n_test: int, p: int, seed: int = 0):
     Xf = X.astype(np.float32).T.copy()
     return (Xf[:, :n_train].copy(), y[:n_train], Xf[:, n_train:].copy(), y[n_train:],
             f[n_train:])
+
+
+def make_probit_inputs(n: int, p: int, m: int, D: int = 6, K: int = 255, seed: int = 0,
+                       idx_bytes: int = 1) -> Inputs:
+    """Binary-response workload for the probit model: X ~ U[0,1) columns of
+    workload 2's generator, P(y = 1 | x) = Phi(g(x)) with
+    g = 1.5 sin(2 pi x_0) + 2 (x_1 - 1/2) + x_2 x_3 - 1/4, K quantile cuts.
+    y_c holds y in {0, 1}; offset = Phi^-1(mean y); sigma_mu = 3 / (2 sqrt m)
+    puts +-3 (probabilities 0.1 % and 99.9 %) at 2 prior sd of the sum of
+    trees; sigma^2 = 1."""
+    from scipy.stats import norm
+
+    X_b = np.empty((p, n), np.uint8)
+    cols = {}
+    for a in range(max(p, 4)):
+        x = column(2, a, n)
+        if a < 4:
+            cols[a] = x.astype(np.float64)
+        if a < p:
+            X_b[a] = bin_column(x, cutpoints(x, K, "quantile"))
+    g = (1.5 * np.sin(2.0 * np.pi * cols[0]) + 2.0 * (cols[1] - 0.5) + cols[2] * cols[3]
+         - 0.25)
+    u = np.random.default_rng([*SEED_BASE, 77, seed]).random(n)
+    y = (u < norm.cdf(g)).astype(np.float32)
+    ybar = float(y.mean()) if n else 0.5
+    offset = float(norm.ppf(min(max(ybar, 1e-6), 1 - 1e-6)))
+    hyper = Hyper(sigma_mu=3.0 / (2.0 * math.sqrt(m)), sigma2_init=1.0)
+    inp = Inputs(config=2, n=n, p=p, m=m, D=D, idx_bytes=idx_bytes, sweeps=0, X_b=X_b,
+                 n_cuts=np.full(p, K, np.int32), y_c=y, offset=offset, hyper=hyper,
+                 seed=seed, probit=True)
+    return inp

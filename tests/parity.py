@@ -47,14 +47,15 @@ def oracle_config(inp, fix_sigma2=False, chain=0):
     return oracle.make_config(n=inp.n, p=inp.p, m=inp.m, D=inp.D, idx_bytes=inp.idx_bytes,
                               alpha=h.alpha, beta=h.beta, mu_mu=h.mu_mu, sigma_mu=h.sigma_mu,
                               nu=h.nu, lam=h.lam, p_grow=h.p_grow, fix_sigma2=fix_sigma2,
-                              chain=chain)
+                              chain=chain, probit=getattr(inp, "probit", False),
+                              probit_offset=inp.offset if getattr(inp, "probit", False) else 0.0)
 
 
 def chain_from_state(inp, st, chain=0) -> oracle.Chain:
     ch = oracle.Chain(oracle_config(inp, chain=chain), inp.X_b, inp.n_cuts, inp.y_c,
                       st["sigma2"])
     ch.load(st["axis"], st["cut"], st["leaf"], st["idx"], st["resid"], st["sigma2"],
-            st["sweep"], st["next"])
+            st["sweep"], st["next"], latent=st.get("latent"))
     return ch
 
 
@@ -153,7 +154,16 @@ def compare_states(inp, gst: dict, ch: oracle.Chain, rep: Report):
     # the oracle adopted the device's leaf draws, so the fp32 residual updates
     # r + (old - new) were the same operations on the same values on both sides
     rep.max_resid_err = float(np.abs(gst["resid"].astype(np.float64) - ch.resid).max())
-    np.testing.assert_array_equal(gst["resid"], ch.resid, err_msg="residual cache")
+    if getattr(inp, "probit", False):
+        # the latent draws invert the normal cdf with each side's own
+        # implementation (fp64, a few ulps apart) before rounding to f32
+        tol = 1e-6 * (1.0 + np.abs(ch.latent.astype(np.float64)))
+        assert (np.abs(gst["latent"].astype(np.float64) - ch.latent) <= tol).all(), "latents"
+        assert ((gst["latent"] > 0) == (ch.ybin > 0)).all()
+        tol = 1e-6 * (1.0 + np.abs(ch.resid.astype(np.float64)))
+        assert (np.abs(gst["resid"].astype(np.float64) - ch.resid) <= tol).all(), "residuals"
+    else:
+        np.testing.assert_array_equal(gst["resid"], ch.resid, err_msg="residual cache")
     np.testing.assert_array_equal(gst["leaf"], ch.leaf, err_msg="leaf values")
     assert gst["sweep"] == ch.sweep and gst["next"] == ch.next
     assert abs(gst["sigma2"] - ch.sigma2) <= 1e-5 * ch.sigma2

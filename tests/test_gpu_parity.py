@@ -269,3 +269,49 @@ def test_move_statistics_count_every_step():
         merged = ((t["move"] == 1) & (t["accept"] == 0)) | ((t["move"] == 2) & (t["accept"] == 1))
         assert d["leaves"] == int((t["n_leaves"] - merged).sum())
     assert g.status() == 0
+
+
+# ---------------------------------------------------------------- probit
+
+@pytest.mark.parametrize("residency,nchain", [(REGS, 1), (STREAM, 1), (REGS, 2)])
+def test_probit_lockstep(residency, nchain):
+    """Binary y: tree steps as in regression (sigma^2 = 1), and the step that
+    ends a sweep draws the latents; two whole sweeps in lockstep."""
+    from paper_2410_23244_amd.inputs import make_probit_inputs
+
+    inp = make_probit_inputs(n=20011, p=10, m=30)
+    print(f"probit residency={residency} nchain={nchain}", flush=True)
+    g = _gpu(inp, residency=residency, nchain=nchain)
+    assert g.launch_info().residency == residency
+    st = g.get_state()
+    ybin = inp.y_c > 0
+    assert ((st["latent"] > 0) == ybin).all() and st["sigma2"] == 1.0
+    reps = parity.lockstep_chains(inp, g, seed=31, warm_sweeps=3, n_steps=2 * (inp.m + 1))
+    for c, rep in enumerate(reps):
+        print(f"  {rep}", flush=True)
+        assert rep.tree_steps > 0 and rep.moves > 0
+        s = g.get_state(c)
+        assert s["sigma2"] == 1.0 and ((s["latent"] > 0) == ybin).all()
+
+
+def test_probit_recovers_class_probabilities():
+    from scipy import stats
+
+    from paper_2410_23244_amd.inputs import column, make_probit_inputs
+
+    inp = make_probit_inputs(n=50000, p=10, m=50)
+    g = _gpu(inp, nchain=2)
+    g.step(100, 3)
+    cols = [column(2, a, inp.n).astype(np.float64) for a in range(4)]
+    gtrue = (1.5 * np.sin(2 * np.pi * cols[0]) + 2.0 * (cols[1] - 0.5) + cols[2] * cols[3]
+             - 0.25)
+    prob = np.zeros(inp.n)
+    for _ in range(50):
+        g.step(1, 3)
+        f = g.predict(inp.X_b, inp.offset).cpu().numpy().astype(np.float64)
+        prob += stats.norm.cdf(f).mean(axis=0)
+    prob /= 50
+    err = np.abs(prob - stats.norm.cdf(gtrue)).mean()
+    print(f"probit mean |p - p_true| = {err:.4f}", flush=True)
+    assert err < 0.05
+    assert g.status() == 0

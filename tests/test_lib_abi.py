@@ -39,9 +39,9 @@ def test_exports_every_declared_symbol(b):
 
 def _cfg(b, **kw):
     base = dict(n=1000, p=4, ntree=10, max_depth=6, idx_bytes=1, grid=0, launch=0,
-                residency=0, nchain=1, reserved=0, x_stride=1024,
+                residency=0, nchain=1, probit=0, x_stride=1024,
                 alpha=0.95, beta=2.0, mu_mu=0.0, sigma_mu=0.1, nu=3.0, lam=0.5,
-                sigma2_init=1.0, p_grow=0.5)
+                sigma2_init=1.0, p_grow=0.5, probit_offset=0.0)
     base.update(kw)
     return b.Config(*[base[f] for f, _ in b.Config._fields_])
 
@@ -52,7 +52,8 @@ def _cfg(b, **kw):
                                  dict(p_grow=2.0), dict(grid=300), dict(grid=-1), dict(lam=float("nan")),
                                  dict(launch=2), dict(launch=-1), dict(residency=3),
                                  dict(residency=-1), dict(nchain=-1), dict(nchain=257),
-                                 dict(nchain=3, grid=100)])
+                                 dict(nchain=3, grid=100), dict(probit=2),
+                                 dict(probit=1, probit_offset=float("inf"))])
 def test_invalid_configs_are_rejected(b, bad):
     cfg = _cfg(b, **bad)
     assert b.bart_workspace_bytes(cfg) == 0
