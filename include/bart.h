@@ -86,7 +86,12 @@ typedef struct {
   int32_t p;          /* predictors, >= 1 */
   int32_t ntree;      /* trees m (sec. 2.1 "Hyperparameters"), >= 1 */
   int32_t max_depth;  /* D in [2, 8]; nodes at depth D-1 are leaves */
-  int32_t idx_bytes;  /* 1 or 2: width of the index cache entries */
+  int32_t idx_bytes;  /* 1 or 2: width of the index cache entries; 0: no [ntree][n]
+                         index cache (sec. 5, "Deeper limitations": it can be
+                         dropped at some speed): every tree step routes the
+                         observations by Algorithm 1 and two rolling u8 rows carry
+                         a tree's leaves from the step that sums it to the step
+                         that applies it; needs streamed residuals */
   int32_t grid;       /* workgroups of the sweep kernel per chain, each owning a
                          slice of the observations: 0 = automatic, else in
                          [1, 256] with grid x nchain <= compute units */
@@ -118,7 +123,9 @@ typedef struct {
 /* State of one chain, in the layouts above.  For bart_get_state the array
  * pointers are caller-owned device buffers that receive copies; for
  * bart_set_state they are read.  idx is dense [ntree][n] of idx_bytes-wide
- * entries.  chain selects the chain (input of both calls). */
+ * entries (u8 when idx_bytes = 0: bart_get_state computes it by Algorithm 1
+ * and bart_set_state ignores it).  chain selects the chain (input of both
+ * calls). */
 typedef struct {
   uint16_t *axis;
   uint8_t *cut;

@@ -323,7 +323,7 @@ class Bart:
     def get_state(self, chain: int = 0) -> dict:
         torch = self.torch
         m, H, n = self.m, self.H, self.n
-        it = torch.uint8 if self.idx_bytes == 1 else torch.int16
+        it = torch.int16 if self.idx_bytes == 2 else torch.uint8  # 0: no cache, u8 leaves
         bufs = dict(axis=torch.empty((m, H), dtype=torch.int16, device=self.device),
                     cut=torch.empty((m, H), dtype=torch.uint8, device=self.device),
                     leaf=torch.empty((m, 2 * H), dtype=torch.float32, device=self.device),

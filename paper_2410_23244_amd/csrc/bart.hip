@@ -57,7 +57,9 @@ const char *check_config(const bart_config *c) {
   if (c->p < 1 || c->p > 65535) return "p must be in [1, 65535]";
   if (c->ntree < 1) return "ntree must be >= 1";
   if (c->max_depth < 2 || c->max_depth > 8) return "max_depth must be in [2, 8]";
-  if (c->idx_bytes != 1 && c->idx_bytes != 2) return "idx_bytes must be 1 or 2";
+  if (c->idx_bytes < 0 || c->idx_bytes > 2) return "idx_bytes must be 0, 1 or 2";
+  if (c->idx_bytes == 0 && c->residency == BART_RESID_REGISTERS)
+    return "idx_bytes = 0 (no index cache) needs streamed residuals";
   if (c->grid < 0 || c->grid > kMaxGrid) return "grid must be 0 or in [1, 256]";
   if (c->nchain < 0 || c->nchain > kMaxGrid) return "nchain must be 0 or in [1, 256]";
   if (c->grid > 0 && (int64_t)c->grid * nchain_of(*c) > kMaxGrid)
@@ -95,7 +97,8 @@ Layout make_layout(const bart_config &c) {
   L.nchain = nchain_of(c);
   L.gcap = kMaxGrid / L.nchain;
   L.resid = take(sizeof(float) * L.n_pad);
-  L.idx = take((size_t)m * L.n_pad * c.idx_bytes);
+  // without an index cache: two rolling rows of u8 leaf indices
+  L.idx = take(c.idx_bytes ? (size_t)m * L.n_pad * c.idx_bytes : 2 * (size_t)L.n_pad);
   L.axis = take(sizeof(uint16_t) * m * H);
   L.cut = take(m * H);
   L.leaf = take(sizeof(float) * m * 2 * H);
@@ -132,8 +135,10 @@ SweepFn regs_fn(int V) {
 
 SweepFn sweep_fn(int V, int IB) { return IB == 1 ? regs_fn<1>(V) : regs_fn<2>(V); }
 
+// IB = 0: no index cache (rolling u8 rows and Algorithm 1 per tree step)
 SweepFn stream_fn(int IB) {
-  return IB == 1 ? sweep_kernel_stream<1> : sweep_kernel_stream<2>;
+  return IB == 0 ? sweep_kernel_stream<1, true>
+                 : (IB == 1 ? sweep_kernel_stream<1, false> : sweep_kernel_stream<2, false>);
 }
 
 // ---------------------------------------------------------------- kernels
@@ -215,6 +220,35 @@ __global__ void k_zero_i32(int32_t *p, int64_t count) {
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count;
        i += (int64_t)gridDim.x * blockDim.x)
     p[i] = 0;
+}
+
+// Leaf of every observation in every tree (blockIdx.y) by Algorithm 1: into
+// out [m][n] u8 and/or as per-leaf counts (an LDS histogram per block).
+__global__ void k_leaf_index(const uint8_t *X, int64_t ldx, int64_t n, int p, const uint16_t *axis,
+                             const uint8_t *cut, int D, int H, uint8_t *out, int32_t *count) {
+  __shared__ int hist[256];
+  const int j = blockIdx.y;
+  for (int k = threadIdx.x; k < 256; k += blockDim.x) hist[k] = 0;
+  __syncthreads();
+  const uint16_t *ax = axis + (int64_t)j * H;
+  const uint8_t *ct = cut + (int64_t)j * H;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    int h = 1;
+    for (int lvl = 1; lvl < D; ++lvl) {
+      const int cv = ct[h];
+      if (cv == 0) break;
+      const int a = ax[h] < p ? ax[h] : 0;
+      h = 2 * h + (X[(int64_t)a * ldx + i] >= cv ? 1 : 0);
+      if (h >= H) break;
+    }
+    if (out) out[(int64_t)j * n + i] = (uint8_t)h;
+    if (count) atomicAdd(&hist[h], 1);
+  }
+  __syncthreads();
+  if (count)
+    for (int k = threadIdx.x; k < 2 * H; k += blockDim.x)
+      if (hist[k]) atomicAdd(&count[(int64_t)j * 2 * H + k], hist[k]);
 }
 
 // Per-leaf counts of every tree from the index cache (after a state load).
@@ -478,7 +512,7 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
     return fail(BART_ENOTSUP, "grid=%d x nchain=%d exceeds the %d compute units", cfg->grid,
                 nchain, prop.multiProcessorCount);
   int V = 0, G = 0;
-  if (cfg->residency != BART_RESID_STREAMED) {
+  if (cfg->residency != BART_RESID_STREAMED && cfg->idx_bytes != 0) {
     for (int v : kVs) {
       const int64_t need = (chunks + (int64_t)v * kBlock - 1) / ((int64_t)v * kBlock);
       const int g = cfg->grid > 0 ? cfg->grid : (int)std::max<int64_t>(need, 1);
@@ -538,13 +572,13 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
                            hipMemcpyHostToDevice, st));
     HIP_TRY(hipMemcpyAsync(at<int32_t>(h, lay.nz_rank), h->nz_rank.data(), sizeof(int32_t) * cfg->p,
                            hipMemcpyHostToDevice, st));
-    const int64_t entries = (int64_t)cfg->ntree * lay.n_pad;
+    const int64_t entries = cfg->idx_bytes ? (int64_t)cfg->ntree * lay.n_pad : 2 * lay.n_pad;
     std::vector<SweepArgs> args(nchain);
     for (int c = 0; c < nchain; ++c) {
       k_init_resid<<<grid_for(lay.n_pad, 256), 256, 0, st>>>(atc<float>(h, c, lay.resid), y_c,
                                                                cfg->n, lay.n_pad);
       k_fill_idx<<<grid_for(entries, 256), 256, 0, st>>>(atc<uint8_t>(h, c, lay.idx), entries,
-                                                           cfg->idx_bytes);
+                                                           cfg->idx_bytes ? cfg->idx_bytes : 1);
       k_init_trees<<<grid_for((int64_t)cfg->ntree * 2 * h->H, 256), 256, 0, st>>>(
           atc<uint16_t>(h, c, lay.axis), atc<uint8_t>(h, c, lay.cut), atc<float>(h, c, lay.leaf),
           atc<int32_t>(h, c, lay.count), cfg->ntree, h->H, cfg->n);
@@ -639,10 +673,18 @@ int bart_get_state(bart_handle *h, bart_state *d) {
   if (d->leaf)
     HIP_TRY(hipMemcpyAsync(d->leaf, atc<void>(h, ch, L.leaf), 4 * m * 2 * H,
                            hipMemcpyDeviceToDevice, st));
-  if (d->idx)
+  if (d->idx && c.idx_bytes)
     HIP_TRY(hipMemcpy2DAsync(d->idx, (size_t)c.n * c.idx_bytes, atc<void>(h, ch, L.idx),
                              (size_t)L.n_pad * c.idx_bytes, (size_t)c.n * c.idx_bytes, m,
                              hipMemcpyDeviceToDevice, st));
+  if (d->idx && !c.idx_bytes) {
+    // no cache: the leaves by Algorithm 1 on the current trees
+    dim3 g(grid_for(c.n, 256), (unsigned)m);
+    k_leaf_index<<<g, 256, 0, st>>>(h->X, c.x_stride, c.n, c.p, atc<uint16_t>(h, ch, L.axis),
+                                    atc<uint8_t>(h, ch, L.cut), c.max_depth, h->H,
+                                    (uint8_t *)d->idx, nullptr);
+    HIP_TRY(hipGetLastError());
+  }
   if (d->resid)
     HIP_TRY(hipMemcpyAsync(d->resid, atc<void>(h, ch, L.resid), 4 * (size_t)c.n,
                            hipMemcpyDeviceToDevice, st));
@@ -677,9 +719,10 @@ int bart_set_state(bart_handle *h, const bart_state *s) {
   HIP_TRY(hipMemcpyAsync(atc<void>(h, ch, L.cut), s->cut, m * H, hipMemcpyDeviceToDevice, st));
   HIP_TRY(hipMemcpyAsync(atc<void>(h, ch, L.leaf), s->leaf, 4 * m * 2 * H, hipMemcpyDeviceToDevice,
                          st));
-  HIP_TRY(hipMemcpy2DAsync(atc<void>(h, ch, L.idx), (size_t)L.n_pad * c.idx_bytes, s->idx,
-                           (size_t)c.n * c.idx_bytes, (size_t)c.n * c.idx_bytes, m,
-                           hipMemcpyDeviceToDevice, st));
+  if (c.idx_bytes)
+    HIP_TRY(hipMemcpy2DAsync(atc<void>(h, ch, L.idx), (size_t)L.n_pad * c.idx_bytes, s->idx,
+                             (size_t)c.n * c.idx_bytes, (size_t)c.n * c.idx_bytes, m,
+                             hipMemcpyDeviceToDevice, st));
   HIP_TRY(hipMemcpyAsync(atc<void>(h, ch, L.resid), s->resid, 4 * (size_t)c.n,
                          hipMemcpyDeviceToDevice, st));
   if (c.probit)
@@ -687,9 +730,16 @@ int bart_set_state(bart_handle *h, const bart_state *s) {
                            hipMemcpyDeviceToDevice, st));
   const int64_t cells = (int64_t)m * 2 * H;
   k_zero_i32<<<grid_for(cells, 256), 256, 0, st>>>(atc<int32_t>(h, ch, L.count), cells);
-  dim3 g(std::min<int64_t>(((int64_t)c.n + 1023) / 1024, 64), (unsigned)m);
-  k_recount<<<g, 1024, 0, st>>>(atc<uint8_t>(h, ch, L.idx), L.n_pad, c.idx_bytes,
-                                atc<int32_t>(h, ch, L.count), c.n, h->H);
+  if (c.idx_bytes) {
+    dim3 g(std::min<int64_t>(((int64_t)c.n + 1023) / 1024, 64), (unsigned)m);
+    k_recount<<<g, 1024, 0, st>>>(atc<uint8_t>(h, ch, L.idx), L.n_pad, c.idx_bytes,
+                                  atc<int32_t>(h, ch, L.count), c.n, h->H);
+  } else {
+    dim3 g(grid_for(c.n, 256), (unsigned)m);
+    k_leaf_index<<<g, 256, 0, st>>>(h->X, c.x_stride, c.n, c.p, atc<uint16_t>(h, ch, L.axis),
+                                    atc<uint8_t>(h, ch, L.cut), c.max_depth, h->H, nullptr,
+                                    atc<int32_t>(h, ch, L.count));
+  }
   // the position is shared by all chains
   for (int k = 0; k < h->nchain; ++k)
     k_set_ctl<<<1, 64, 0, st>>>(atc<Ctl>(h, k, L.ctl), k == ch ? s->sigma2 : -1.0, s->sweep, 0);

@@ -117,6 +117,8 @@ struct Ctx {
   Prop pr;
   uint8_t rank_of[256];          // heap slot -> rank among larger-tree leaves (0xFF: none)
   uint16_t heap_of[kMaxLeaves];  // rank -> heap slot
+  uint16_t ax[kMaxLeaves];       // without an index cache: the tree's axis and cut per
+  uint8_t ct[kMaxLeaves];        // internal heap slot, for Algorithm 1
 };
 
 // What the decision of one tree needs besides the sums: per rank of the
@@ -1058,7 +1060,7 @@ __global__ void __launch_bounds__(kBlock) sweep_kernel(const SweepArgs *__restri
 // value (route of j+1 from its rows).  Partial sums are fp64 per lane.
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-template <int IB>
+template <int IB, bool CF>
 __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ A, const Launch &Lc,
                                                   Shared &sh) {
   using IC = IdxChunk<IB>;
@@ -1114,10 +1116,16 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     const bool xa = do_a && ca.pr.move == kGrow, xn = do_n && cn.pr.move == kGrow;
     const int Ln = do_n ? cn.pr.L : 0;
     const bool regs = Ln <= kRegLeaves;
-    const gptr<ChunkT> rowa =
-        gbl((ChunkT *)((char *)A->idx + (int64_t)(do_a ? ja : 0) * A->ldi * IB));
-    const gptr<const ChunkT> rown =
-        gbl((const ChunkT *)((const char *)A->idx + (int64_t)(do_n ? jn : 0) * A->ldi * IB));
+    // index rows of trees ja and jn: rows of the cache, or without one the
+    // two rolling rows (by tree parity) that carry a tree's leaves from the
+    // step that accumulates it to the step that applies it
+    auto row_of = [&](int tree) {
+      const int64_t r = CF ? (tree & 1) : tree;
+      return gbl((ChunkT *)((char *)A->idx + r * A->ldi * IB));
+    };
+    const gptr<ChunkT> rowa = row_of(do_a ? ja : 0);
+    const gptr<ChunkT> rown = row_of(do_n ? jn : 0);
+    const bool trav = CF && do_n && lo == 0;  // Algorithm 1 for tree jn
     const gptr<const uint32_t> xra = gbl((const uint32_t *)(A->X + (int64_t)ca.pr.axis * A->ldx));
     const gptr<const uint32_t> xrn = gbl((const uint32_t *)(A->X + (int64_t)cn.pr.axis * A->ldx));
     const gptr<f32x4> res = gbl((f32x4 *)A->resid);
@@ -1149,8 +1157,47 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           rv[u] = res[ch[u]];
           if (do_a) ra[u] = rowa[ch[u]];
           if (xa) xa4[u] = xra[ch[u]];
-          if (do_n) rn[u] = rown[ch[u]];
+          if (do_n && !trav) rn[u] = rown[ch[u]];
           if (xn) xn4[u] = xrn[ch[u]];
+        }
+      }
+      if (trav) {
+        // leaves of tree jn by Algorithm 1 on its structure snapshot, level
+        // by level with the predictor bytes of all 4 U points in flight
+        int hh[U][4];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) hh[u][b] = 1;
+        const int H = A->H;
+        for (int lvl = 1; lvl < A->D; ++lvl) {
+          int xb[U][4];
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              const int h = hh[u][b];
+              const int cv = h < H ? cn.ct[h] : 0;
+              xb[u][b] = 0;
+              if (((ok[u] >> b) & 1u) && cv)
+                xb[u][b] = A->X[(int64_t)cn.ax[h] * A->ldx + 4 * (int64_t)ch[u] + b];
+            }
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              const int h = hh[u][b];
+              const int cv = h < H ? cn.ct[h] : 0;
+              if (cv) hh[u][b] = 2 * h + (xb[u][b] >= cv ? 1 : 0);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          ChunkT pk = 0;
+#pragma unroll
+          for (int b = 0; b < 4; ++b) pk = IC::put(pk, b, hh[u][b]);
+          rn[u] = pk;
+          if (ok[u]) rown[ch[u]] = pk;
         }
       }
 #pragma unroll
@@ -1173,7 +1220,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
             if (changed) out = IC::put(out, b, (merged && pair) ? eta_a : (int)ca.heap_of[rnk]);
           }
           if (ok[u]) res[ch[u]] = rv[u];
-          if (changed && touch && ok[u]) rowa[ch[u]] = out;
+          if (!CF && changed && touch && ok[u]) rowa[ch[u]] = out;
         }
         if (want_ssr) {
 #pragma unroll
@@ -1244,13 +1291,26 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     for (int u = 0; u < kWaves; ++u) a += sh.red_w[k][u];
     return a;
   };
-  // proposals of trees j0..j0+2, their rank tables, the decision data of j0
-  // and tree j0's partial sums
+  // axis and cut of one heap slot of tree j (thread t < H), packed
+  auto struct_word = [&](int tree) -> uint32_t {
+    const int H = A->H, h = t < H ? t : 0;
+    const int64_t o = (int64_t)tree * H + h;
+    return (uint32_t)gbl(A->axis)[o] | ((uint32_t)gbl(A->cut)[o] << 16);
+  };
+  auto store_struct = [&](Ctx &c, uint32_t wv) {
+    if (t < A->H) {
+      c.ax[t] = (uint16_t)(wv & 0xffffu);
+      c.ct[t] = (uint8_t)(wv >> 16);
+    }
+  };
+  // proposals of trees j0..j0+2, their rank tables (and structures, without
+  // an index cache), the decision data of j0 and tree j0's partial sums
   auto refill = [&](int j0, int64_t s) {
     for (int q = 0; q < 3; ++q)
       if (j0 + q < m) {
         const uint32_t wd = load_prop_word(A, j0 + q);
         if (t < kPropWords) ((uint32_t *)&sh.ctx[(j0 + q) & (kRing - 1)].pr)[t] = wd;
+        if (CF) store_struct(sh.ctx[(j0 + q) & (kRing - 1)], struct_word(j0 + q));
       }
     lds_barrier();
     for (int q = 0; q < 3; ++q)
@@ -1294,12 +1354,14 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       const int j1 = more1 ? j + 1 : j, j3 = more3 ? j + 3 : j;
       const TdRegs tdn = load_tree_data(A, sh.ctx[j1 & (kRing - 1)], j1, s);
       const uint32_t pw3 = load_prop_word(A, j3);
+      const uint32_t sw3 = CF ? struct_word(j3) : 0u;
       lds_barrier();
       if (t == L) sh.nr[j & 1] = 0;
       pre_decide(A, sh, c, sh.td[j & 1], w == 0 ? uncounted : -1);
       const int nseg = gather_polls(A, sh, par, seq, L + 1, L);
       decide_step(A, sh, c, sh.td[j & 1], nseg);
       if (more3 && t < kPropWords) ((uint32_t *)&sh.ctx[(j + 3) & (kRing - 1)].pr)[t] = pw3;
+      if (CF && more3) store_struct(sh.ctx[(j + 3) & (kRing - 1)], sw3);
       if (more1) store_tree_data(sh.td[(j + 1) & 1], sh.ctx[(j + 1) & (kRing - 1)], tdn);
       lds_barrier();
       finish_tree(A, Lc, sh, c, j, s, step);
@@ -1343,13 +1405,13 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
                                  (sh.dev_err ? BART_DEVERR_CACHE : 0u));
 }
 
-template <int IB>
+template <int IB, bool CF>
 __global__ void __launch_bounds__(kBlock) sweep_kernel_stream(const SweepArgs *__restrict__ A,
                                                               Launch Lc) {
   __shared__ Shared sh;
   const int c = (int)blockIdx.x / A->G;
   if (Lc.trace) Lc.trace += c * Lc.trace_stride;
-  sweep_body_stream<IB>(A + c, Lc, sh);
+  sweep_body_stream<IB, CF>(A + c, Lc, sh);
 }
 
 }  // namespace bart

@@ -44,7 +44,8 @@ class Report:
 
 def oracle_config(inp, fix_sigma2=False, chain=0):
     h = inp.hyper
-    return oracle.make_config(n=inp.n, p=inp.p, m=inp.m, D=inp.D, idx_bytes=inp.idx_bytes,
+    # the oracle always keeps an index cache (u8 when the device has none)
+    return oracle.make_config(n=inp.n, p=inp.p, m=inp.m, D=inp.D, idx_bytes=inp.idx_bytes or 1,
                               alpha=h.alpha, beta=h.beta, mu_mu=h.mu_mu, sigma_mu=h.sigma_mu,
                               nu=h.nu, lam=h.lam, p_grow=h.p_grow, fix_sigma2=fix_sigma2,
                               chain=chain, probit=getattr(inp, "probit", False),

@@ -315,3 +315,49 @@ def test_probit_recovers_class_probabilities():
     print(f"probit mean |p - p_true| = {err:.4f}", flush=True)
     assert err < 0.05
     assert g.status() == 0
+
+
+# ---------------------------------------------------------------- no index cache
+
+@pytest.mark.parametrize("cfg,over", [(2, dict(n=40003, p=30, m=40)),
+                                      (5, dict(n=25003, p=1000, m=120))])
+def test_no_index_cache_lockstep(cfg, over):
+    """idx_bytes = 0: the trees route the observations by Algorithm 1 every
+    step; lockstep against the oracle, whose cache the device exports."""
+    inp = make_inputs(cfg, **over, idx_bytes=0)
+    g = _gpu(inp, grid=4, launch=ORDINARY)
+    assert g.launch_info().residency == STREAM
+    rep = parity.lockstep(inp, g, seed=inp.seed + 7, warm_sweeps=2, n_steps=inp.m + 1 + 9)
+    print(f"  {rep}", flush=True)
+    assert rep.tree_steps > 0 and rep.moves > 0
+
+
+def test_no_index_cache_equals_the_cached_kernel():
+    """Same partition, same sums: the chain without an index cache is the
+    chain with one, bit for bit, across launches that split sweeps."""
+    inp8 = make_inputs(2, n=30011, p=16, m=25)
+    inp0 = make_inputs(2, n=30011, p=16, m=25, idx_bytes=0)
+    a = _gpu(inp8, grid=5, residency=STREAM, nchain=2)
+    b = _gpu(inp0, grid=5, nchain=2)
+    for k in (3, 1, 2):
+        a.step(k, 29)
+        b.step(k, 29)
+    a.debug_steps(13, 29)
+    b.debug_steps(13, 29)
+    for c in range(2):
+        sa, sb = a.get_state(c), b.get_state(c)
+        for key in ["axis", "cut", "leaf", "idx", "resid"]:
+            np.testing.assert_array_equal(sa[key], sb[key], err_msg=key)
+        assert sa["sigma2"] == sb["sigma2"]
+    # a state loaded into a chain without a cache continues identically
+    st = a.get_state(0)
+    c0 = _gpu(inp0, grid=5)
+    c8 = _gpu(inp8, grid=5, residency=STREAM)
+    c0.set_state(st)
+    c8.set_state(st)
+    c0.debug_steps(20, 5)
+    c8.debug_steps(20, 5)
+    s0, s8 = c0.get_state(), c8.get_state()
+    for key in ["axis", "cut", "leaf", "idx", "resid"]:
+        np.testing.assert_array_equal(s0[key], s8[key], err_msg=key)
+    assert a.status() == 0 and b.status() == 0 and c0.status() == 0
