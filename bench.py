@@ -166,6 +166,8 @@ def main() -> int:
     ap.add_argument("--seed", type=int, default=3)
     ap.add_argument("--chains", type=int, default=1, help="independent chains per launch")
     ap.add_argument("--grid", type=int, default=0, help="workgroups per chain (0 = automatic)")
+    ap.add_argument("--no-index-cache", action="store_true",
+                    help="run without the [ntree][n] index cache (Algorithm 1 every tree step)")
     ap.add_argument("--predict", type=int, default=0, metavar="NT",
                     help="after the warm-up, time bart_predict on NT points instead of sweeps")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -193,7 +195,7 @@ def main() -> int:
     if args.copy_probe:
         return copy_probe(args.copy_probe)
     t0 = time.perf_counter()
-    inp = make_inputs(args.config)
+    inp = make_inputs(args.config, idx_bytes=0 if args.no_index_cache else None)
     print(f"[bench] inputs {inp.workload} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
           flush=True)
     mode = BART_LAUNCH_ORDINARY if args.launch == "ordinary" else BART_LAUNCH_COOPERATIVE
@@ -226,7 +228,8 @@ def main() -> int:
     launch_ms = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(L)]
     avg_launch = sum(launch_ms) / L
     sweeps_per_s = C * args.steps / (ms / 1e3)
-    per_sweep = C * model_bytes_per_sweep(inp.n, inp.m, inp.idx_bytes)
+    # without an index cache the same model bytes as the u8 cache are counted
+    per_sweep = C * model_bytes_per_sweep(inp.n, inp.m, max(1, inp.idx_bytes))
     achieved = per_sweep * S / (avg_launch / 1e3) / 1e9
     print(f"[bench] {args.steps} sweeps in {L} launches: events {ms:.1f} ms, wall "
           f"{wall * 1e3:.1f} ms, per launch {min(launch_ms):.2f}..{max(launch_ms):.2f} ms",
@@ -239,9 +242,10 @@ def main() -> int:
         print(f"[bench] oracle {cpu['value']:.3f} sweeps/s", file=sys.stderr, flush=True)
 
     metric = METRIC
-    if args.config != 3 or C > 1:
+    if args.config != 3 or C > 1 or args.no_index_cache:
         metric = (f"full MCMC sweeps/sec (all trees) at n={inp.n},p={inp.p},ntree={inp.m},"
                   f"D={inp.D}" + (f", summed over {C} chains" if C > 1 else "") +
+                  (", no index cache" if args.no_index_cache else "") +
                   "; achieved HBM GB/s")
     line = {
         "metric": metric,
