@@ -1142,25 +1142,27 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       f32x4 rv[U];
       ChunkT ra[U], rn[U];
       uint32_t xa4[U], xn4[U];
+      // every lane loads (chunk 0 stands in for chunks past the end) and
+      // only workgroup-uniform conditions select loads, so all of them are in
+      // flight at once; padding points are masked by ok in the arithmetic
+      int32_t cu[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         ch[u] = (w * cpt + i0 + u) * kBlock + t;
-        ok[u] = 0;
-        if (i0 + u < cpt && ch[u] < A->chunks) {
-          const int32_t rem = A->n - 4 * ch[u];
-          ok[u] = rem >= 4 ? 15u : ((1u << rem) - 1u);
-        }
-        rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-        ra[u] = rn[u] = 0;
-        xa4[u] = xn4[u] = 0;
-        if (ok[u]) {
-          rv[u] = res[ch[u]];
-          if (do_a) ra[u] = rowa[ch[u]];
-          if (xa) xa4[u] = xra[ch[u]];
-          if (do_n && !trav) rn[u] = rown[ch[u]];
-          if (xn) xn4[u] = xrn[ch[u]];
-        }
+        const bool valid = i0 + u < cpt && ch[u] < A->chunks;
+        const int32_t rem = A->n - 4 * ch[u];
+        ok[u] = !valid ? 0u : (rem >= 4 ? 15u : ((1u << rem) - 1u));
+        cu[u] = valid ? ch[u] : 0;
+        rv[u] = res[cu[u]];
       }
+#pragma unroll
+      for (int u = 0; u < U; ++u) ra[u] = do_a ? rowa[cu[u]] : (ChunkT)0;
+#pragma unroll
+      for (int u = 0; u < U; ++u) xa4[u] = xa ? xra[cu[u]] : 0u;
+#pragma unroll
+      for (int u = 0; u < U; ++u) rn[u] = do_n && !trav ? rown[cu[u]] : (ChunkT)0;
+#pragma unroll
+      for (int u = 0; u < U; ++u) xn4[u] = xn ? xrn[cu[u]] : 0u;
       if (trav) {
         // leaves of tree jn by Algorithm 1 on its structure snapshot, level
         // by level with the predictor bytes of all 4 U points in flight
