@@ -39,6 +39,7 @@ namespace bart {
 constexpr uint32_t kSpinLimit = 1u << 21;
 constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
 constexpr int kRegLeaves = 8;  // trees with at most this many leaves are reduced in registers
+constexpr int kStreamRegLeaves = 0;  // the streamed pass sums every tree in LDS bins
 constexpr int kRegPath = 0;
 constexpr int kBinRanks = kBinFloats / (kWaves * 64);  // ranks per pass of the LDS bins (64)
 
@@ -1115,7 +1116,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     const float dml = sh.dlt_m[0], dmr = sh.dlt_m[1];
     const bool xa = do_a && ca.pr.move == kGrow, xn = do_n && cn.pr.move == kGrow;
     const int Ln = do_n ? cn.pr.L : 0;
-    const bool regs = Ln <= kRegLeaves;
+    const bool regs = Ln <= kStreamRegLeaves;
     // index rows of trees ja and jn: rows of the cache, or without one the
     // two rolling rows (by tree parity) that carry a tree's leaves from the
     // step that accumulates it to the step that applies it
@@ -1283,11 +1284,11 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   auto pass_all = [&](int ja, int jn, bool want_ssr) {
     pass(ja, jn, want_ssr, 0);
     const int Ln = jn >= 0 ? sh.ctx[jn & (kRing - 1)].pr.L : 0;
-    if (Ln > kRegLeaves)
+    if (Ln > kStreamRegLeaves)
       for (int lo = kBinRanks; lo < Ln; lo += kBinRanks) pass(-1, jn, false, lo);
   };
   auto partial = [&](int L, int k) {
-    if (L > kRegLeaves) return sh.red[k];
+    if (L > kStreamRegLeaves) return sh.red[k];
     double a = 0.0;
 #pragma unroll
     for (int u = 0; u < kWaves; ++u) a += sh.red_w[k][u];
