@@ -39,9 +39,9 @@ namespace bart {
 constexpr uint32_t kSpinLimit = 1u << 21;
 constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
 constexpr int kRegLeaves = 8;  // trees with at most this many leaves are reduced in registers
-constexpr int kStreamRegLeaves = 0;  // the streamed pass sums every tree in LDS bins
 constexpr int kRegPath = 0;
 constexpr int kBinRanks = kBinFloats / (kWaves * 64);  // ranks per pass of the LDS bins (64)
+constexpr int kSlotRanks = kBinRanks / 4;  // the same with a bin per chunk position (16)
 
 __device__ __forceinline__ uint64_t ld_dev(const uint64_t *p) {
   return __hip_atomic_load(gbl(const_cast<uint64_t *>(p)), __ATOMIC_RELAXED,
@@ -1102,10 +1102,10 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     return pk;
   };
 
-  // one pass: apply tree ja (-1: none), accumulate tree jn (-1: none) into
-  // sh.red_w (<= kRegLeaves leaves; fp64 per lane) or, for ranks in
-  // [lo, lo + kBinRanks), into sh.red (private fp32 bins per lane), sum of
-  // squares into sh.wave_part if want_ssr.  Ends with an LDS barrier.
+  // one pass: apply tree ja (-1: none), accumulate the ranks [lo, lo +
+  // kSlotRanks) of tree jn (-1: none) into sh.red (private fp32 bins per lane
+  // and chunk position, then a fixed-order fp64 reduction), sum of squares
+  // into sh.wave_part if want_ssr.  Ends with an LDS barrier.
   auto pass = [&](int ja, int jn, bool want_ssr, int lo) {
     const Ctx &ca = sh.ctx[(ja < 0 ? 0 : ja) & (kRing - 1)];
     const Ctx &cn = sh.ctx[(jn < 0 ? 0 : jn) & (kRing - 1)];
@@ -1116,7 +1116,6 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     const float dml = sh.dlt_m[0], dmr = sh.dlt_m[1];
     const bool xa = do_a && ca.pr.move == kGrow, xn = do_n && cn.pr.move == kGrow;
     const int Ln = do_n ? cn.pr.L : 0;
-    const bool regs = Ln <= kStreamRegLeaves;
     // index rows of trees ja and jn: rows of the cache, or without one the
     // two rolling rows (by tree parity) that carry a tree's leaves from the
     // step that accumulates it to the step that applies it
@@ -1130,9 +1129,6 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     const gptr<const uint32_t> xra = gbl((const uint32_t *)(A->X + (int64_t)ca.pr.axis * A->ldx));
     const gptr<const uint32_t> xrn = gbl((const uint32_t *)(A->X + (int64_t)cn.pr.axis * A->ldx));
     const gptr<f32x4> res = gbl((f32x4 *)A->resid);
-    double accd[kRegLeaves];
-#pragma unroll
-    for (int k = 0; k < kRegLeaves; ++k) accd[k] = 0.0;
     double ssr = 0.0;
     int nr = 0;
     uint32_t bad = 0;
@@ -1233,19 +1229,24 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           }
         }
         if (do_n) {
+          // a private bin per lane and chunk position: the 4 points of a
+          // chunk never share one, so the chunk is one batch of independent
+          // read-modify-writes (chunks follow in LDS order); points that are
+          // padding or outside the pass add 0 to a bin of the pass
           const uint32_t rk = ranks4(cn, rn[u], xn4[u], ok[u], nr, bad);
+          int q[4];
+          float add[4], cur[4];
 #pragma unroll
           for (int b = 0; b < 4; ++b) {
-            const int rnk = (rk >> (8 * b)) & 0xff;
-            const double add = ((ok[u] >> b) & 1u) ? (double)rv[u][b] : 0.0;
-            if (regs) {
-#pragma unroll
-              for (int k = 0; k < kRegLeaves; ++k)
-                if (k < Ln && rnk == k) accd[k] += add;
-            } else if (rnk >= lo && rnk < lo + kBinRanks && ((ok[u] >> b) & 1u)) {
-              sh.bins[(((rnk - lo) * kWaves + wave) << 6) | lane] += rv[u][b];
-            }
+            const int rl = (int)((rk >> (8 * b)) & 0xff) - lo;
+            const bool in = rl >= 0 && rl < kSlotRanks && ((ok[u] >> b) & 1u);
+            q[b] = ((((in ? rl : 0) * 4 + b) * kWaves + wave) << 6) | lane;
+            add[b] = in ? rv[u][b] : 0.f;
           }
+#pragma unroll
+          for (int b = 0; b < 4; ++b) cur[b] = sh.bins[q[b]];
+#pragma unroll
+          for (int b = 0; b < 4; ++b) sh.bins[q[b]] = cur[b] + add[b];
         }
       }
     }
@@ -1255,24 +1256,18 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       const double tot = wave_total63(ssr);
       if (lane == 63) sh.wave_part[wave] = tot;
     }
-    if (do_n && regs) {
-#pragma unroll
-      for (int k = 0; k < kRegLeaves; ++k)
-        if (k < Ln) {
-          const double tot = wave_total63(accd[k]);
-          if (lane == 63) sh.red_w[k][wave] = tot;
-        }
-    }
     lds_barrier();
-    if (do_n && !regs) {
-      for (int k = lo + wave; k < min(Ln, lo + kBinRanks); k += kWaves) {
+    if (do_n) {
+      for (int k = lo + wave; k < min(Ln, lo + kSlotRanks); k += kWaves) {
         double a = 0.0;
 #pragma unroll
-        for (int u = 0; u < kWaves; ++u) {
-          const int q = (((k - lo) * kWaves + u) << 6) | lane;
-          a += (double)sh.bins[q];
-          sh.bins[q] = 0.f;
-        }
+        for (int u = 0; u < kWaves; ++u)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const int q = ((((k - lo) * 4 + b) * kWaves + u) << 6) | lane;
+            a += (double)sh.bins[q];
+            sh.bins[q] = 0.f;
+          }
         const double tot = wave_total63(a);
         if (lane == 63) sh.red[k] = tot;
       }
@@ -1284,16 +1279,9 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   auto pass_all = [&](int ja, int jn, bool want_ssr) {
     pass(ja, jn, want_ssr, 0);
     const int Ln = jn >= 0 ? sh.ctx[jn & (kRing - 1)].pr.L : 0;
-    if (Ln > kStreamRegLeaves)
-      for (int lo = kBinRanks; lo < Ln; lo += kBinRanks) pass(-1, jn, false, lo);
+    for (int lo = kSlotRanks; lo < Ln; lo += kSlotRanks) pass(-1, jn, false, lo);
   };
-  auto partial = [&](int L, int k) {
-    if (L > kStreamRegLeaves) return sh.red[k];
-    double a = 0.0;
-#pragma unroll
-    for (int u = 0; u < kWaves; ++u) a += sh.red_w[k][u];
-    return a;
-  };
+  auto partial = [&](int, int k) { return sh.red[k]; };
   // axis and cut of one heap slot of tree j (thread t < H), packed
   auto struct_word = [&](int tree) -> uint32_t {
     const int H = A->H, h = t < H ? t : 0;
