@@ -712,7 +712,11 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
                                            Shared &sh) {
   using IC = IdxChunk<IB>;
   using ChunkT = typename IC::T;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, w = wg_id(A);
+  // the thread index is re-read opaquely at every step (see the loop), so
+  // addresses derived from it are recomputed rather than kept in registers
+  // (or spilled) across the whole loop
+  int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int w = wg_id(A);
   const int G = A->G, H = A->H, m = A->m;
   const uint64_t seed = Lc.seed;
   const bool tracing = Lc.trace != nullptr;
@@ -912,6 +916,9 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
 #pragma unroll 1
   for (int step = 0; step < Lc.n_steps; ++step) {
     if (sh.abort_flag) break;
+    asm volatile("" : "+v"(t));
+    lane = t & 63;
+    wave = t >> 6;
     const uint32_t seq = (uint32_t)step + 2;
     const int par = step & 1;
     if (j < m) {
