@@ -938,10 +938,11 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       }
       // 2. while the mailboxes fill: load rows of j+2, the decision data of
       //    j+1 and the proposal of j+3
-      if (more2) issue_rows(j + 2);
+      // (the small loads first: nothing waits behind the row loads)
       const int j1 = more1 ? j + 1 : j, j3 = more3 ? j + 3 : j;
       const TdRegs tdn = load_tree_data(A, sh.ctx[j1 & (kRing - 1)], j1, s);
       const uint32_t pw3 = load_prop_word(A, j3);
+      if (more2) issue_rows(j + 2);
       lds_barrier();  // nr[j&1] read by the poster before it is cleared
       if (t == L) sh.nr[j & 1] = 0;
       // 3. totals of tree j, in the same order in every workgroup: polls into
