@@ -38,8 +38,6 @@ namespace bart {
 
 constexpr uint32_t kSpinLimit = 1u << 21;
 constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
-constexpr int kRegLeaves = 8;  // trees with at most this many leaves are reduced in registers
-constexpr int kRegPath = 0;
 constexpr int kBinRanks = kBinFloats / (kWaves * 64);  // ranks per pass of the LDS bins (64)
 constexpr int kSlotRanks = kBinRanks / 4;  // the same with a bin per chunk position (16)
 
@@ -139,7 +137,6 @@ struct Shared {
   Ctx ctx[kRing];
   TreeData td[2];
   double red[kMaxLeaves + 1];  // this workgroup's partial sums of the tree to post next
-  double red_w[kRegLeaves][kWaves];  // the same per wave, for small trees
   double part[kBlock];
   double tot[kMaxLeaves + 1];
   double S[kMaxLeaves];
@@ -813,47 +810,22 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     if (bad) sh.dev_err = 1;
     if (lane == 0 && nr) atomicAdd(&sh.nr[tree & 1], nr);
   };
-  // partial sums of tree `tree` from the current residuals.  Up to kRegLeaves
-  // leaves: per-lane fp32 sums in registers, a fixed-order fp64 DPP sum per
-  // wave into sh.red_w[k][wave] (the poster adds the waves); more leaves:
-  // per-lane private LDS bins and a fixed-order fp64 reduction into sh.red.
-  // Ends with an LDS barrier.
+  // partial sums of tree `tree` from the current residuals: per-lane private
+  // LDS bins for up to kBinRanks ranks at a time (a plain read-modify-write:
+  // LDS float atomics are many times slower; padding points and ranks outside
+  // the pass add 0 to a bin of the pass, so there is no branch per point),
+  // then a fixed-order fp64 reduction into sh.red; larger trees take several
+  // passes.  Ends with an LDS barrier.
   auto reduce = [&](int tree, const uint32_t (&rks)[V]) {
     const int L = sh.ctx[tree & (kRing - 1)].pr.L;
-    if (L <= kRegPath) {
-      float acc[kRegLeaves];
-#pragma unroll
-      for (int k = 0; k < kRegLeaves; ++k) acc[k] = 0.f;
-#pragma unroll
-      for (int v = 0; v < V; ++v)
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const int rnk = (rks[v] >> (8 * b)) & 0xff;
-          const float add = ((okm[v] >> b) & 1u) ? r[v][b] : 0.f;
-#pragma unroll
-          for (int k = 0; k < kRegLeaves; ++k)
-            if (k < L && rnk == k) acc[k] += add;
-        }
-#pragma unroll
-      for (int k = 0; k < kRegLeaves; ++k)
-        if (k < L) {
-          const double tot = wave_total63((double)acc[k]);
-          if (lane == 63) sh.red_w[k][wave] = tot;
-        }
-      lds_barrier();
-      return;
-    }
-    // private bins of every lane for up to kBinRanks ranks at a time: a plain
-    // read-modify-write (LDS float atomics serialise across lanes and are
-    // many times slower); larger trees take several passes
     for (int base = 0; base < L; base += kBinRanks) {
 #pragma unroll
       for (int v = 0; v < V; ++v)
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
           const int rnk = ((rks[v] >> (8 * b)) & 0xff) - base;
-          if (rnk >= 0 && rnk < kBinRanks && ((okm[v] >> b) & 1u))
-            sh.bins[((rnk * kWaves + wave) << 6) | lane] += r[v][b];
+          const bool in = rnk >= 0 && rnk < kBinRanks && ((okm[v] >> b) & 1u);
+          sh.bins[(((in ? rnk : 0) * kWaves + wave) << 6) | lane] += in ? r[v][b] : 0.f;
         }
       lds_barrier();
       for (int k = base + wave; k < min(L, base + kBinRanks); k += kWaves) {
@@ -870,14 +842,8 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       lds_barrier();
     }
   };
-  // this workgroup's partial sum of rank k of a tree with L leaves (after reduce)
-  auto partial = [&](int L, int k) {
-    if (L > kRegPath) return sh.red[k];
-    double acc = 0.0;
-#pragma unroll
-    for (int u = 0; u < kWaves; ++u) acc += sh.red_w[k][u];
-    return acc;
-  };
+  // this workgroup's partial sum of rank k (after reduce)
+  auto partial = [&](int, int k) { return sh.red[k]; };
   // proposals of trees j0.. j0+2 into the ring, rank tables, rows of j0,
   // route of j0, rows of j0+1, decision data of j0, partial sums of j0
   auto refill = [&](int j0, int64_t s) {
