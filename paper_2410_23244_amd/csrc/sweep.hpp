@@ -95,6 +95,17 @@ __device__ __forceinline__ double wave_total63(double v) {
   return v;
 }
 
+// Sum of an int over the wave into lane 63, with the steps of wave_total63.
+__device__ __forceinline__ int wave_sum63_i32(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, true);
+  return v;
+}
+
 // wave_total63 of three values at once, the steps interleaved so that the
 // three DPP chains overlap.
 __device__ __forceinline__ void wave_totals3(double &a, double &b, double &c) {
@@ -786,7 +797,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
         const int in = ci == grow_eta;
         const int right = xi >= cutv;
         cp[v][b] = (in ? 2 * eta + right : ci) & 255;
-        nr += __popcll(__ballot(ok && in && right));
+        nr += (ok && in && right) ? 1 : 0;
       }
     int r0[V][4];
 #pragma unroll
@@ -808,7 +819,8 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       out[v] = pk;
     }
     if (bad) sh.dev_err = 1;
-    if (lane == 0 && nr) atomicAdd(&sh.nr[tree & 1], nr);
+    nr = wave_sum63_i32(nr);
+    if (lane == 63 && nr) atomicAdd(&sh.nr[tree & 1], nr);
   };
   // partial sums of tree `tree` from the current residuals: per-lane private
   // LDS bins for up to kBinRanks ranks at a time (a plain read-modify-write:
@@ -1040,7 +1052,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
                                                   Shared &sh) {
   using IC = IdxChunk<IB>;
   using ChunkT = typename IC::T;
-  constexpr int U = 4;  // chunks of 4 points in flight per thread
+  constexpr int U = 1;  // chunks of 4 points per batch (two batches in flight)
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6, w = wg_id(A);
   const int m = A->m, cpt = A->cpt;
   const uint64_t seed = Lc.seed;
@@ -1106,34 +1118,46 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     double ssr = 0.0;
     int nr = 0;
     uint32_t bad = 0;
-#pragma unroll 1
-    for (int i0 = 0; i0 < cpt; i0 += U) {
+    // a batch of U chunks per thread: its loads, then its arithmetic; the
+    // loop keeps the next batch's loads in flight while one is computed
+    struct Batch {
       int32_t ch[U];
       uint32_t ok[U];
       f32x4 rv[U];
       ChunkT ra[U], rn[U];
       uint32_t xa4[U], xn4[U];
-      // every lane loads (chunk 0 stands in for chunks past the end) and
-      // only workgroup-uniform conditions select loads, so all of them are in
-      // flight at once; padding points are masked by ok in the arithmetic
+    };
+    // every lane loads (chunk 0 stands in for chunks past the end) and only
+    // workgroup-uniform conditions select loads, so all of them are in
+    // flight at once; padding points are masked by ok in the arithmetic
+    auto load_batch = [&](int i0, Batch &B) {
       int32_t cu[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        ch[u] = (w * cpt + i0 + u) * kBlock + t;
-        const bool valid = i0 + u < cpt && ch[u] < A->chunks;
-        const int32_t rem = A->n - 4 * ch[u];
-        ok[u] = !valid ? 0u : (rem >= 4 ? 15u : ((1u << rem) - 1u));
-        cu[u] = valid ? ch[u] : 0;
-        rv[u] = res[cu[u]];
+        B.ch[u] = (w * cpt + i0 + u) * kBlock + t;
+        const bool valid = i0 + u < cpt && B.ch[u] < A->chunks;
+        const int32_t rem = A->n - 4 * B.ch[u];
+        B.ok[u] = !valid ? 0u : (rem >= 4 ? 15u : ((1u << rem) - 1u));
+        cu[u] = valid ? B.ch[u] : 0;
+        B.rv[u] = res[cu[u]];
       }
 #pragma unroll
-      for (int u = 0; u < U; ++u) ra[u] = do_a ? rowa[cu[u]] : (ChunkT)0;
+      for (int u = 0; u < U; ++u) B.ra[u] = do_a ? rowa[cu[u]] : (ChunkT)0;
 #pragma unroll
-      for (int u = 0; u < U; ++u) xa4[u] = xa ? xra[cu[u]] : 0u;
+      for (int u = 0; u < U; ++u) B.xa4[u] = xa ? xra[cu[u]] : 0u;
 #pragma unroll
-      for (int u = 0; u < U; ++u) rn[u] = do_n && !trav ? rown[cu[u]] : (ChunkT)0;
+      for (int u = 0; u < U; ++u) B.rn[u] = do_n && !trav ? rown[cu[u]] : (ChunkT)0;
 #pragma unroll
-      for (int u = 0; u < U; ++u) xn4[u] = xn ? xrn[cu[u]] : 0u;
+      for (int u = 0; u < U; ++u) B.xn4[u] = xn ? xrn[cu[u]] : 0u;
+    };
+    auto compute_batch = [&](Batch &B) {
+      int32_t (&ch)[U] = B.ch;
+      uint32_t (&ok)[U] = B.ok;
+      f32x4 (&rv)[U] = B.rv;
+      ChunkT (&ra)[U] = B.ra;
+      ChunkT (&rn)[U] = B.rn;
+      uint32_t (&xa4)[U] = B.xa4;
+      uint32_t (&xn4)[U] = B.xn4;
       if (trav) {
         // leaves of tree jn by Algorithm 1 on its structure snapshot, level
         // by level with the predictor bytes of all 4 U points in flight
@@ -1223,6 +1247,16 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           for (int b = 0; b < 4; ++b) sh.bins[q[b]] = cur[b] + add[b];
         }
       }
+    };
+    Batch B0, B1;
+    load_batch(0, B0);
+#pragma unroll 1
+    for (int i0 = 0; i0 < cpt; i0 += 2 * U) {
+      if (i0 + U < cpt) load_batch(i0 + U, B1);
+      compute_batch(B0);
+      if (i0 + U >= cpt) break;
+      if (i0 + 2 * U < cpt) load_batch(i0 + 2 * U, B0);
+      compute_batch(B1);
     }
     if (bad) sh.dev_err = 1;
     if (do_n && lo == 0 && lane == 0 && nr) atomicAdd(&sh.nr[jn & 1], nr);
