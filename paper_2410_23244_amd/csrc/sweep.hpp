@@ -1052,7 +1052,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
                                                   Shared &sh) {
   using IC = IdxChunk<IB>;
   using ChunkT = typename IC::T;
-  constexpr int U = 1;  // chunks of 4 points per batch (two batches in flight)
+  constexpr int U = 1;  // chunks of 4 points per batch (three batches in flight)
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6, w = wg_id(A);
   const int m = A->m, cpt = A->cpt;
   const uint64_t seed = Lc.seed;
@@ -1119,7 +1119,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     int nr = 0;
     uint32_t bad = 0;
     // a batch of U chunks per thread: its loads, then its arithmetic; the
-    // loop keeps the next batch's loads in flight while one is computed
+    // loop keeps the next two batches' loads in flight while one is computed
     struct Batch {
       int32_t ch[U];
       uint32_t ok[U];
@@ -1248,15 +1248,19 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
         }
       }
     };
-    Batch B0, B1;
+    Batch B0, B1, B2;
     load_batch(0, B0);
+    if (U < cpt) load_batch(U, B1);
 #pragma unroll 1
-    for (int i0 = 0; i0 < cpt; i0 += 2 * U) {
-      if (i0 + U < cpt) load_batch(i0 + U, B1);
+    for (int i0 = 0; i0 < cpt; i0 += 3 * U) {
+      if (i0 + 2 * U < cpt) load_batch(i0 + 2 * U, B2);
       compute_batch(B0);
       if (i0 + U >= cpt) break;
-      if (i0 + 2 * U < cpt) load_batch(i0 + 2 * U, B0);
+      if (i0 + 3 * U < cpt) load_batch(i0 + 3 * U, B0);
       compute_batch(B1);
+      if (i0 + 2 * U >= cpt) break;
+      if (i0 + 4 * U < cpt) load_batch(i0 + 4 * U, B1);
+      compute_batch(B2);
     }
     if (bad) sh.dev_err = 1;
     if (do_n && lo == 0 && lane == 0 && nr) atomicAdd(&sh.nr[jn & 1], nr);
