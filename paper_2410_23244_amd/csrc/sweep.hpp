@@ -158,6 +158,7 @@ struct Shared {
   float dlt_m[2];              // residual deltas of the two children in that case
   double wave_part[kWaves];
   double sigma2;
+  double sig_gamma;  // Gamma((nu+n)/2, 1) variate of the next sigma^2 draw
   double dec_logr;
   // constants of tree j's decision that do not depend on its sums, computed
   // while the mailboxes fill: per rank of a leaf whose count is known, the new
@@ -272,22 +273,27 @@ __device__ __noinline__ void gen_normals(const SweepArgs *__restrict__ A, uint64
 }
 
 // Proposals of sweep s for the trees >= j0 this workgroup owns (tree j is
-// owned by workgroup j mod G), one thread per tree.
+// owned by workgroup j mod G), one wave per tree.
 __device__ __noinline__ void gen_proposals(const SweepArgs *__restrict__ A, uint64_t seed, int64_t s,
                                            int j0) {
   const Key key = chain_key(seed, A->chain);
-  for (int tr = wg_id(A) + A->G * (int)threadIdx.x; tr < A->m; tr += A->G * kBlock)
+  const int wv = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  for (int tr = wg_id(A) + A->G * wv; tr < A->m; tr += A->G * kWaves)
     if (tr >= j0) propose_tree(A, key, tr, s, A->prop[tr]);
 }
 
 // sigma^2 | rest ~ InvGamma((nu+n)/2, (nu lambda + SSR)/2), the conjugate
-// update of the prior lambda nu / sigma^2 ~ chi^2_nu (eq. bartdef).
-__device__ __noinline__ double draw_sigma2(const SweepArgs *__restrict__ A, uint64_t seed, int64_t s,
-                                           double ssr) {
+// update of the prior lambda nu / sigma^2 ~ chi^2_nu (eq. bartdef), drawn as
+// scale / g with g ~ Gamma((nu+n)/2, 1).  g depends only on the random
+// stream of sweep s, so it is drawn before the SSR is known.
+__device__ __noinline__ double sigma2_gamma(const SweepArgs *__restrict__ A, uint64_t seed,
+                                            int64_t s) {
   const Key key = chain_key(seed, A->chain);
-  const double shape = 0.5 * (A->nu + (double)A->n);
-  const double scale = 0.5 * (A->nu * A->lambda + ssr);
-  return scale / gamma_mt(key, (uint64_t)s, shape);
+  return gamma_mt(key, (uint64_t)s, 0.5 * (A->nu + (double)A->n));
+}
+__device__ __forceinline__ double sigma2_of(const SweepArgs *__restrict__ A, double ssr,
+                                            double g) {
+  return 0.5 * (A->nu * A->lambda + ssr) / g;
 }
 
 // Probit latent of one observation (sec. 5 "Mild limitations"; Albert and
@@ -664,6 +670,10 @@ __device__ __forceinline__ void sigma2_tail(const SweepArgs *__restrict__ A, con
   const int t = threadIdx.x, w = wg_id(A), m = A->m;
   const uint64_t seed = Lc.seed;
   const bool tracing = Lc.trace != nullptr;
+  // the gamma variate of this sweep's sigma^2 draw, on the last wave (one
+  // that owns no tree unless a workgroup owns more than 7), while the
+  // others propose
+  if (!A->probit && t == kBlock - 64) sh.sig_gamma = sigma2_gamma(A, seed, s);
   // the next sweep's proposals (owners) and normals, published by the
   // release below together with this sweep's tree writes
   gen_proposals(A, seed, s + 1, 0);
@@ -680,7 +690,7 @@ __device__ __forceinline__ void sigma2_tail(const SweepArgs *__restrict__ A, con
   if (t == 0) {
     const double ssr_all = sh.tot[0];
     // the probit model holds sigma^2 at 1 and draws latents instead
-    const double s2 = A->probit ? sh.sigma2 : draw_sigma2(A, seed, s, ssr_all);
+    const double s2 = A->probit ? sh.sigma2 : sigma2_of(A, ssr_all, sh.sig_gamma);
     sh.sigma2 = s2;
     if (w == 0) {
       A->ctl->sigma2 = s2;
