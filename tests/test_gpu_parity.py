@@ -182,6 +182,23 @@ def test_lockstep_big_trees(shape, residency):
     assert rep.moves > 0
 
 
+@pytest.mark.parametrize("residency", [REGS, STREAM])
+def test_lockstep_exhausted_axes(residency):
+    """Three predictors with three cuts each under depth-8 trees: paths run
+    out of cuts on an axis within a few splits, so growable leaves, the axis
+    pick (which skips exhausted axes) and the split probabilities of the
+    children depend on the exhausted-axis count at every depth (the axes
+    with cuts are fewer than the deepest path, so no shortcut applies)."""
+    inp = make_inputs(5, n=20011, p=3, m=8)
+    inp.X_b = (inp.X_b // 64).astype(np.uint8)  # 4 bins: cuts 1..3
+    inp.n_cuts = np.full(inp.p, 3, np.int32)
+    g = _gpu(inp, residency=residency)
+    g.set_state(_full_trees(inp, 3, np.random.default_rng(11)))
+    rep = parity.lockstep(inp, g, seed=9, warm_sweeps=0, n_steps=3 * (inp.m + 1))
+    print(f"  {rep}", flush=True)
+    assert rep.moves > 0
+
+
 def test_lockstep_full_size_streamed():
     """Workload 4 (n = 1e7, u16 index cache): residuals streamed from HBM."""
     inp = make_inputs(4)
