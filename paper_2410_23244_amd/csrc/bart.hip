@@ -164,13 +164,29 @@ __global__ void k_init_probit(const float *y, uint8_t *ybin, float *latent, floa
   }
 }
 
-__global__ void k_fill_idx(uint8_t *idx, int64_t entries, int ib) {
+// Every observation starts in the root (slot 1); padding entries of a row
+// (n <= i < n_pad) hold 0, a slot that is never a leaf.
+__global__ void k_fill_idx(uint8_t *idx, int64_t entries, int ib, int64_t n, int64_t n_pad) {
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < entries;
        i += (int64_t)gridDim.x * blockDim.x) {
+    const int v = i % n_pad < n ? 1 : 0;
     if (ib == 1)
-      idx[i] = 1;
+      idx[i] = (uint8_t)v;
     else
-      ((uint16_t *)idx)[i] = 1;
+      ((uint16_t *)idx)[i] = (uint16_t)v;
+  }
+}
+
+// Padding entries (n <= i < n_pad) of m index rows back to 0.
+__global__ void k_zero_idx_pad(uint8_t *idx, int ib, int64_t n, int64_t n_pad, int64_t m) {
+  const int64_t per = n_pad - n;
+  for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < m * per;
+       q += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = (q / per) * n_pad + n + q % per;
+    if (ib == 1)
+      idx[i] = 0;
+    else
+      ((uint16_t *)idx)[i] = 0;
   }
 }
 
@@ -252,8 +268,11 @@ __global__ void k_leaf_index(const uint8_t *X, int64_t ldx, int64_t n, int p, co
 }
 
 // Per-leaf counts of every tree from the index cache (after a state load).
+// Leaf counts of every tree from the index cache; an entry of a real
+// observation outside slots 1..2H-1 (0 marks padding) flags the cache as
+// inconsistent.
 __global__ void k_recount(const uint8_t *idx, int64_t ldi, int ib, int32_t *count, int32_t n,
-                          int H) {
+                          int H, uint32_t *error) {
   __shared__ int hist[256];
   const int j = blockIdx.y;
   for (int k = threadIdx.x; k < 256; k += blockDim.x) hist[k] = 0;
@@ -261,7 +280,10 @@ __global__ void k_recount(const uint8_t *idx, int64_t ldi, int ib, int32_t *coun
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
     const int v = ib == 1 ? idx[j * ldi + i] : ((const uint16_t *)idx)[j * ldi + i];
-    if (v < 2 * H) atomicAdd(&hist[v], 1);
+    if (v >= 1 && v < 2 * H)
+      atomicAdd(&hist[v], 1);
+    else
+      atomicOr(error, BART_DEVERR_CACHE);
   }
   __syncthreads();
   for (int k = threadIdx.x; k < 2 * H; k += blockDim.x)
@@ -578,7 +600,8 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
       k_init_resid<<<grid_for(lay.n_pad, 256), 256, 0, st>>>(atc<float>(h, c, lay.resid), y_c,
                                                                cfg->n, lay.n_pad);
       k_fill_idx<<<grid_for(entries, 256), 256, 0, st>>>(atc<uint8_t>(h, c, lay.idx), entries,
-                                                           cfg->idx_bytes ? cfg->idx_bytes : 1);
+                                                           cfg->idx_bytes ? cfg->idx_bytes : 1,
+                                                           cfg->n, lay.n_pad);
       k_init_trees<<<grid_for((int64_t)cfg->ntree * 2 * h->H, 256), 256, 0, st>>>(
           atc<uint16_t>(h, c, lay.axis), atc<uint8_t>(h, c, lay.cut), atc<float>(h, c, lay.leaf),
           atc<int32_t>(h, c, lay.count), cfg->ntree, h->H, cfg->n);
@@ -719,10 +742,14 @@ int bart_set_state(bart_handle *h, const bart_state *s) {
   HIP_TRY(hipMemcpyAsync(atc<void>(h, ch, L.cut), s->cut, m * H, hipMemcpyDeviceToDevice, st));
   HIP_TRY(hipMemcpyAsync(atc<void>(h, ch, L.leaf), s->leaf, 4 * m * 2 * H, hipMemcpyDeviceToDevice,
                          st));
-  if (c.idx_bytes)
+  if (c.idx_bytes) {
     HIP_TRY(hipMemcpy2DAsync(atc<void>(h, ch, L.idx), (size_t)L.n_pad * c.idx_bytes, s->idx,
                              (size_t)c.n * c.idx_bytes, (size_t)c.n * c.idx_bytes, m,
                              hipMemcpyDeviceToDevice, st));
+    if (L.n_pad > c.n)
+      k_zero_idx_pad<<<grid_for((int64_t)m * (L.n_pad - c.n), 256), 256, 0, st>>>(
+          atc<uint8_t>(h, ch, L.idx), c.idx_bytes, c.n, L.n_pad, (int64_t)m);
+  }
   HIP_TRY(hipMemcpyAsync(atc<void>(h, ch, L.resid), s->resid, 4 * (size_t)c.n,
                          hipMemcpyDeviceToDevice, st));
   if (c.probit)
@@ -733,7 +760,8 @@ int bart_set_state(bart_handle *h, const bart_state *s) {
   if (c.idx_bytes) {
     dim3 g(std::min<int64_t>(((int64_t)c.n + 1023) / 1024, 64), (unsigned)m);
     k_recount<<<g, 1024, 0, st>>>(atc<uint8_t>(h, ch, L.idx), L.n_pad, c.idx_bytes,
-                                  atc<int32_t>(h, ch, L.count), c.n, h->H);
+                                  atc<int32_t>(h, ch, L.count), c.n, h->H,
+                                  &atc<Ctl>(h, ch, L.ctl)->error);
   } else {
     dim3 g(grid_for(c.n, 256), (unsigned)m);
     k_leaf_index<<<g, 256, 0, st>>>(h->X, c.x_stride, c.n, c.p, atc<uint16_t>(h, ch, L.axis),

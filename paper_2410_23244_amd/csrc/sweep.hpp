@@ -37,8 +37,10 @@
 namespace bart {
 
 constexpr uint32_t kSpinLimit = 1u << 21;
+constexpr int kNullRank = kMaxLeaves;  // rank of a padding point: no bin, zero delta
 constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
 constexpr int kBinRanks = kBinFloats / (kWaves * 64);  // ranks per pass of the LDS bins (64)
+static_assert(kMaxLeaves % kBinRanks == 0, "the null rank must fall outside every bin pass");
 constexpr int kSlotRanks = kBinRanks / 4;  // the same with a bin per chunk position (16)
 
 __device__ __forceinline__ uint64_t ld_dev(const uint64_t *p) {
@@ -126,7 +128,7 @@ __device__ __forceinline__ void wave_totals3(double &a, double &b, double &c) {
 struct Ctx {
   Prop pr;
   uint8_t rank_of[256];          // heap slot -> rank among larger-tree leaves (0xFF: none)
-  uint16_t heap_of[kMaxLeaves];  // rank -> heap slot
+  uint16_t heap_of[kMaxLeaves + 1];  // rank -> heap slot; the null rank -> 0
   uint16_t ax[kMaxLeaves];       // without an index cache: the tree's axis and cut per
   uint8_t ct[kMaxLeaves];        // internal heap slot, for Algorithm 1
 };
@@ -153,7 +155,7 @@ struct Shared {
   double S[kMaxLeaves];
   double cntd[kMaxLeaves];
   float newv[kMaxLeaves];      // new value of each larger-tree leaf if it stays a leaf
-  float dlt[kMaxLeaves];       // its residual delta: old value - new value
+  float dlt[kMaxLeaves + 1];   // its residual delta: old value - new value; 0 at the null rank
   float newv_m;                // new value of eta if the move ends merged
   float dlt_m[2];              // residual deltas of the two children in that case
   double wave_part[kWaves];
@@ -769,7 +771,9 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     sh.dev_err = 0;
     sh.nr[0] = sh.nr[1] = 0;
     sh.sigma2 = A->ctl->sigma2;
+    sh.dlt[kNullRank] = 0.f;
   }
+  if (t < kRing) sh.ctx[t].heap_of[kNullRank] = 0;
   if (t < 6) sh.stats[t] = 0;
   int uncounted = -1;  // tree step whose move statistics workgroup 0 has yet to count
 
@@ -803,11 +807,10 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       for (int b = 0; b < 4; ++b) {
         const int ci = IC::get(rawc[v], b);
         const int xi = (rawx[v] >> (8 * b)) & 0xff;
-        const uint32_t ok = (okm[v] >> b) & 1u;
         const int in = ci == grow_eta;
         const int right = xi >= cutv;
         cp[v][b] = (in ? 2 * eta + right : ci) & 255;
-        nr += (ok && in && right) ? 1 : 0;
+        nr += (in && right) ? 1 : 0;
       }
     int r0[V][4];
 #pragma unroll
@@ -820,10 +823,12 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       uint32_t pk = 0;
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
-        const uint32_t ok = (okm[v] >> b) & 1u;
-        bad |= ok & (r0[v][b] == 0xFF);
-        // padding observations and (invalid) non-leaf indices use rank 0
-        const int rnk = (ok && r0[v][b] != 0xFF) ? r0[v][b] : 0;
+        // slot 0 marks a padding point (its index entry, or no load at all
+        // past the last chunk): the null rank, whose delta is 0 and which
+        // falls in no bin, so no per-point mask is needed; any other
+        // non-leaf slot is an inconsistent cache (also the null rank)
+        bad |= (r0[v][b] == 0xFF) & (cp[v][b] != 0);
+        const int rnk = r0[v][b] != 0xFF ? r0[v][b] : kNullRank;
         pk |= (uint32_t)rnk << (8 * b);
       }
       out[v] = pk;
@@ -846,7 +851,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
           const int rnk = ((rks[v] >> (8 * b)) & 0xff) - base;
-          const bool in = rnk >= 0 && rnk < kBinRanks && ((okm[v] >> b) & 1u);
+          const bool in = rnk >= 0 && rnk < kBinRanks;
           sh.bins[(((in ? rnk : 0) * kWaves + wave) << 6) | lane] += in ? r[v][b] : 0.f;
         }
       lds_barrier();
@@ -962,7 +967,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
           const int rnk = (rk[v] >> (8 * b)) & 0xff;
           const bool to_eta = merged && ((rnk == kl) || (rnk == kr));
           const float d = to_eta ? (rnk == kl ? dml : dmr) : dl[v][b];
-          r[v][b] += ((okm[v] >> b) & 1u) ? d : 0.f;
+          r[v][b] += d;
         }
       if (changed) {
 #pragma unroll
@@ -1072,7 +1077,9 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     sh.dev_err = 0;
     sh.nr[0] = sh.nr[1] = 0;
     sh.sigma2 = A->ctl->sigma2;
+    sh.dlt[kNullRank] = 0.f;
   }
+  if (t < kRing) sh.ctx[t].heap_of[kNullRank] = 0;
   if (t < 6) sh.stats[t] = 0;
   int uncounted = -1;  // tree step whose move statistics workgroup 0 has yet to count
 
