@@ -40,8 +40,9 @@ constexpr uint32_t kSpinLimit = 1u << 21;
 constexpr int kNullRank = kMaxLeaves;  // rank of a padding point: no bin, zero delta
 constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
 constexpr int kBinRanks = kBinFloats / (kWaves * 64);  // ranks per pass of the LDS bins (64)
-static_assert(kMaxLeaves % kBinRanks == 0, "the null rank must fall outside every bin pass");
 constexpr int kSlotRanks = kBinRanks / 4;  // the same with a bin per chunk position (16)
+static_assert(kMaxLeaves % kBinRanks == 0 && kMaxLeaves % kSlotRanks == 0,
+              "the null rank must fall outside every bin pass");
 
 __device__ __forceinline__ uint64_t ld_dev(const uint64_t *p) {
   return __hip_atomic_load(gbl(const_cast<uint64_t *>(p)), __ATOMIC_RELAXED,
@@ -1083,10 +1084,12 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   if (t < 6) sh.stats[t] = 0;
   int uncounted = -1;  // tree step whose move statistics workgroup 0 has yet to count
 
-  // leaf ranks in tree c's larger tree of the 4 points of a chunk (0 for
-  // padding); GROW right-count into nr
-  auto ranks4 = [&](const Ctx &c, ChunkT rc, uint32_t rx, uint32_t ok, int &nr,
-                    uint32_t &bad) -> uint32_t {
+  // leaf ranks in tree c's larger tree of the 4 points of a chunk; GROW
+  // right-count into nr.  Index 0 marks a padding point (its entry in the
+  // row, or a chunk past the end whose loaded values were zeroed): the null
+  // rank, whose delta is 0 and which falls in no bin; any other non-leaf
+  // slot is an inconsistent cache (also the null rank).
+  auto ranks4 = [&](const Ctx &c, ChunkT rc, uint32_t rx, int &nr, uint32_t &bad) -> uint32_t {
     const int move = c.pr.move, eta = c.pr.eta, cutv = c.pr.cut;
     const int grow_eta = move == kGrow ? eta : -1;
     uint32_t pk = 0;
@@ -1094,13 +1097,13 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     for (int b = 0; b < 4; ++b) {
       const int ci = IC::get(rc, b);
       const int xi = (rx >> (8 * b)) & 0xff;
-      const uint32_t okb = (ok >> b) & 1u;
       const int in = ci == grow_eta;
       const int right = xi >= cutv;
-      const int r0 = c.rank_of[(in ? 2 * eta + right : ci) & 255];
-      nr += __popcll(__ballot(okb && in && right));
-      bad |= okb & (r0 == 0xFF);
-      pk |= (uint32_t)((okb && r0 != 0xFF) ? r0 : 0) << (8 * b);
+      const int cp = (in ? 2 * eta + right : ci) & 255;
+      const int r0 = c.rank_of[cp];
+      nr += __popcll(__ballot(in && right));
+      bad |= (r0 == 0xFF) & (cp != 0);
+      pk |= (uint32_t)(r0 != 0xFF ? r0 : kNullRank) << (8 * b);
     }
     return pk;
   };
@@ -1146,7 +1149,9 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     };
     // every lane loads (chunk 0 stands in for chunks past the end) and only
     // workgroup-uniform conditions select loads, so all of them are in
-    // flight at once; padding points are masked by ok in the arithmetic
+    // flight at once; the arithmetic zeroes what a chunk past the end
+    // loaded, after which its points are padding like those of a partial
+    // chunk (index entry 0, residual 0)
     auto load_batch = [&](int i0, Batch &B) {
       int32_t cu[U];
 #pragma unroll
@@ -1175,6 +1180,12 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       ChunkT (&rn)[U] = B.rn;
       uint32_t (&xa4)[U] = B.xa4;
       uint32_t (&xn4)[U] = B.xn4;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (!ok[u]) {
+          ra[u] = rn[u] = (ChunkT)0;
+          rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
       if (trav) {
         // leaves of tree jn by Algorithm 1 on its structure snapshot, level
         // by level with the predictor bytes of all 4 U points in flight
@@ -1209,7 +1220,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
         for (int u = 0; u < U; ++u) {
           ChunkT pk = 0;
 #pragma unroll
-          for (int b = 0; b < 4; ++b) pk = IC::put(pk, b, hh[u][b]);
+          for (int b = 0; b < 4; ++b) pk = IC::put(pk, b, ((ok[u] >> b) & 1u) ? hh[u][b] : 0);
           rn[u] = pk;
           if (ok[u]) rown[ch[u]] = pk;
         }
@@ -1218,7 +1229,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       for (int u = 0; u < U; ++u) {
         int nra = 0;
         if (do_a) {
-          const uint32_t rk = ranks4(ca, ra[u], xa4[u], ok[u], nra, bad);
+          const uint32_t rk = ranks4(ca, ra[u], xa4[u], nra, bad);
           float dl[4];
 #pragma unroll
           for (int b = 0; b < 4; ++b) dl[b] = sh.dlt[(rk >> (8 * b)) & 0xff];
@@ -1229,7 +1240,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
             const int rnk = (rk >> (8 * b)) & 0xff;
             const bool pair = (rnk == kl) || (rnk == kr);
             const float d = (merged && pair) ? (rnk == kl ? dml : dmr) : dl[b];
-            rv[u][b] += ((ok[u] >> b) & 1u) ? d : 0.f;
+            rv[u][b] += d;
             touch |= pair;
             if (changed) out = IC::put(out, b, (merged && pair) ? eta_a : (int)ca.heap_of[rnk]);
           }
@@ -1239,22 +1250,22 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
         if (want_ssr) {
 #pragma unroll
           for (int b = 0; b < 4; ++b) {
-            const double x = ((ok[u] >> b) & 1u) ? (double)rv[u][b] : 0.0;
+            const double x = (double)rv[u][b];  // 0 at padding points
             ssr += x * x;
           }
         }
         if (do_n) {
           // a private bin per lane and chunk position: the 4 points of a
           // chunk never share one, so the chunk is one batch of independent
-          // read-modify-writes (chunks follow in LDS order); points that are
-          // padding or outside the pass add 0 to a bin of the pass
-          const uint32_t rk = ranks4(cn, rn[u], xn4[u], ok[u], nr, bad);
+          // read-modify-writes (chunks follow in LDS order); points of the
+          // null rank or outside the pass add 0 to a bin of the pass
+          const uint32_t rk = ranks4(cn, rn[u], xn4[u], nr, bad);
           int q[4];
           float add[4], cur[4];
 #pragma unroll
           for (int b = 0; b < 4; ++b) {
             const int rl = (int)((rk >> (8 * b)) & 0xff) - lo;
-            const bool in = rl >= 0 && rl < kSlotRanks && ((ok[u] >> b) & 1u);
+            const bool in = rl >= 0 && rl < kSlotRanks;
             q[b] = ((((in ? rl : 0) * 4 + b) * kWaves + wave) << 6) | lane;
             add[b] = in ? rv[u][b] : 0.f;
           }

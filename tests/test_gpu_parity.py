@@ -87,7 +87,8 @@ def test_steps_compose_and_are_deterministic():
 
 
 def test_set_state_roundtrip_continues_identically():
-    inp = make_inputs(1, n=2000, p=8, m=12)
+    # n = 2001: the last chunk of 4 points holds one point and three padding
+    inp = make_inputs(1, n=2001, p=8, m=12)
     a = _gpu(inp)
     a.step(4, 3)
     st = a.get_state()
@@ -99,6 +100,27 @@ def test_set_state_roundtrip_continues_identically():
     for k in ["axis", "cut", "leaf", "idx", "resid"]:
         np.testing.assert_array_equal(sa[k], sb[k], err_msg=k)
     assert a.status() == 0 and b.status() == 0
+
+
+def test_set_state_flags_an_inconsistent_index_cache():
+    """Index entry 0 marks a padding point; a real point whose entry is 0
+    (or any slot outside 1..2H-1) makes the leaf recount that set_state runs
+    report an inconsistent cache (BART_DEVERR_CACHE = 2)."""
+    inp = make_inputs(1, n=2001, p=8, m=12)
+    a = _gpu(inp)
+    a.step(3, 3)
+    st = a.get_state()
+    assert a.status() == 0
+    for bad_value in (0, 1 << (inp.D - 1 + 1)):
+        bad = dict(st)
+        bad["idx"] = st["idx"].copy()
+        bad["idx"][3, 17] = bad_value
+        b = _gpu(inp)
+        b.set_state(bad)
+        assert b.status() == 2, bad_value
+    c = _gpu(inp)
+    c.set_state(st)
+    assert c.status() == 0
 
 
 def test_launch_modes_agree():
