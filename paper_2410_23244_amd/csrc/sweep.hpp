@@ -689,7 +689,10 @@ __device__ __forceinline__ void sigma2_tail(const SweepArgs *__restrict__ A, con
     st_dev(mailbox(A, par, w), mk_word(seq, pack_f64(acc)));
   }
   gather_total(A, sh, par, seq, 1);
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  // acquire by the wave whose lanes polled (its cache invalidation serves
+  // the whole workgroup: the other waves' reads follow the barrier at the
+  // end of this step, so they happen after it)
+  if (t < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   if (t == 0) {
     const double ssr_all = sh.tot[0];
     // the probit model holds sigma^2 at 1 and draws latents instead
@@ -903,7 +906,8 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   __syncthreads();
   if (t == 0) st_dev(mailbox(A, 1, w), mk_word(1, 0));
   gather_total(A, sh, 1, 1, 0);
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  // acquire by the polling wave; the barrier orders the other waves after it
+  if (t < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __syncthreads();
   if (j < m && !sh.abort_flag) refill(j, s);
 
@@ -1363,7 +1367,8 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   __syncthreads();
   if (t == 0) st_dev(mailbox(A, 1, w), mk_word(1, 0));
   gather_total(A, sh, 1, 1, 0);
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  // acquire by the polling wave; the barrier orders the other waves after it
+  if (t < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __syncthreads();
   if (j < m && !sh.abort_flag) refill(j, s);
   bool have_ssr = false;
