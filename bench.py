@@ -10,7 +10,10 @@ Prints one JSON line.
 
 --chains C runs C independent chains in the same launches (multi-chain
 batching); value is then the chain-sweeps per second summed over the chains
-and the roofline counts every chain's bytes.
+and the roofline counts every chain's bytes.  The single-chain headline run
+also times 4 chains batched on the same workload after its own measurement
+and reports them in a separate 'batched' object (--batched sets the count,
+0 turns it off); value stays the single chain's.
 
 Roofline: the algorithmic bytes of a tree step are (9 + 2 s_idx) per
 observation (read the index row and the predictor row, read and write the
@@ -165,6 +168,10 @@ def main() -> int:
     ap.add_argument("--cpu-sweeps", type=int, default=20, help="oracle sweeps (0 = skip)")
     ap.add_argument("--seed", type=int, default=3)
     ap.add_argument("--chains", type=int, default=1, help="independent chains per launch")
+    ap.add_argument("--batched", type=int, default=-1, metavar="C",
+                    help="after the main line's measurement, also time C chains batched in the "
+                         "same launches on the same workload and report them under 'batched' "
+                         "(-1: 4 for the single-chain headline workload, else off; 0: off)")
     ap.add_argument("--grid", type=int, default=0, help="workgroups per chain (0 = automatic)")
     ap.add_argument("--no-index-cache", action="store_true",
                     help="run without the [ntree][n] index cache (Algorithm 1 every tree step)")
@@ -242,6 +249,36 @@ def main() -> int:
         cpu = cpu_baseline(inp, st, args.seed, args.cpu_sweeps)
         print(f"[bench] oracle {cpu['value']:.3f} sweeps/s", file=sys.stderr, flush=True)
 
+    batched = None
+    nb = args.batched if args.batched >= 0 else (
+        4 if args.config == 3 and C == 1 and args.grid == 0 and not args.no_index_cache else 0)
+    if nb > 1:
+        # the same workload with nb chains in the same launches: chain-sweeps
+        # per second summed over the chains, timed like the main line
+        gb = from_inputs(inp, launch=mode, nchain=nb)
+        ib = gb.launch_info()
+        for _ in range(args.warmup // S):
+            gb.step(S, args.seed)
+        torch.cuda.synchronize()
+        Lb = max(1, (args.steps // 2) // S)
+        evb = [torch.cuda.Event(enable_timing=True) for _ in range(2 * Lb)]
+        for i in range(Lb):
+            evb[2 * i].record(gb.stream)
+            gb.step(S, args.seed)
+            evb[2 * i + 1].record(gb.stream)
+        torch.cuda.synchronize()
+        assert gb.status() == 0, "device error during the batched sweeps"
+        msb = evb[0].elapsed_time(evb[-1])
+        avgb = sum(evb[2 * i].elapsed_time(evb[2 * i + 1]) for i in range(Lb)) / Lb
+        achb = nb * model_bytes_per_sweep(inp.n, inp.m, max(1, inp.idx_bytes)) * S / (avgb / 1e3) / 1e9
+        batched = {"chains": nb, "value": nb * Lb * S / (msb / 1e3), "unit": "chain-sweeps/s",
+                   "steps": Lb * S, "ms_per_step": msb / (Lb * S), "grid_per_chain": ib.grid,
+                   "chunks_per_thread": ib.chunks_per_thread,
+                   "roofline_achieved_gbs": achb, "roofline_frac": achb / HBM_PEAK_GBS}
+        print(f"[bench] {nb} chains batched: {batched['value']:.1f} chain-sweeps/s",
+              file=sys.stderr, flush=True)
+        gb.close()
+
     metric = METRIC
     if args.config != 3 or C > 1 or args.no_index_cache:
         metric = (f"full MCMC sweeps/sec (all trees) at n={inp.n},p={inp.p},ntree={inp.m},"
@@ -273,6 +310,8 @@ def main() -> int:
                      "algorithmic_bytes_per_launch": per_sweep * S},
         "cpu_baseline": cpu,
     }
+    if batched is not None:
+        line["batched"] = batched
     print(json.dumps(line), flush=True)
     g.close()
     torch.cuda.synchronize()
