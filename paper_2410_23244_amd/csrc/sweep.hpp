@@ -160,6 +160,7 @@ struct Shared {
   float newv_m;                // new value of eta if the move ends merged
   float dlt_m[2];              // residual deltas of the two children in that case
   double wave_part[kWaves];
+  uint64_t solo[kMaxLeaves + 1];  // one workgroup per chain: its own mailbox words
   double sigma2;
   double sig_gamma;  // Gamma((nu+n)/2, 1) variate of the next sigma^2 draw
   double dec_logr;
@@ -339,6 +340,18 @@ __device__ __forceinline__ uint64_t *mailbox(const SweepArgs *__restrict__ A, in
   return A->pub + ((int64_t)par * A->G + g) * kStride;
 }
 
+// Word k of this workgroup's mailbox in buffer par.  A chain of one
+// workgroup keeps it in LDS instead: the gather reads it back unchanged, so
+// the totals are bit-identical, without a round trip through device memory.
+template <class SH>
+__device__ __forceinline__ void post(const SweepArgs *__restrict__ A, SH &sh, int par, int k,
+                                     uint64_t word) {
+  if (A->G == 1)
+    sh.solo[k] = word;
+  else
+    st_dev(mailbox(A, par, wg_id(A)) + k, word);
+}
+
 // Poll word k < K of every mailbox of buffer par until all carry step number
 // seq.  The workgroups are split into nseg segments of 8 nb consecutive
 // workgroups, nb the fewest batches of 8 that let nseg * K threads cover
@@ -351,6 +364,17 @@ template <class SH>
 __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH &sh, int par,
                                             uint32_t seq, int K, int nsum) {
   const int t = threadIdx.x, G = A->G;
+  if (G == 1) {
+    // thread k posted word k itself (post)
+    if (t < K) {
+      const uint64_t wv = sh.solo[t];
+      double acc = 0.0;
+      acc += t < nsum ? unpack_f64(wv) : (double)(wv & kPayloadMask);
+      sh.part[t] = acc;
+    }
+    lds_barrier();
+    return 1;
+  }
   int nb = 1;
   while (K * ((G + 8 * nb - 1) / (8 * nb)) > kBlock) ++nb;
   const int span = 8 * nb;
@@ -486,11 +510,13 @@ __device__ __forceinline__ void pre_decide(const SweepArgs *__restrict__ A, Shar
   const int move = c.pr.move, eta = c.pr.eta, L = c.pr.L;
   const int kl = c.pr.rank_l, kr = c.pr.rank_r;
   const double s2 = sh.sigma2, v2 = A->sigma_mu * A->sigma_mu;
-  const double iv2 = 1.0 / v2, mm = A->mu_mu * iv2;
+  // prec = n / s2 + 1 / v2 = e / (s2 v2) with e = s2 + n v2, so the draw
+  // mean + z / sqrt(prec) is S v2 / e + mu_mu s2 / e + z sqrt(s2 v2 / e):
+  // one division and one square root
   auto consts = [&](double n, double z, double &la, double &lb) {
-    const double prec = n / s2 + iv2;
-    la = 1.0 / (s2 * prec);
-    lb = mm / prec + z / sqrt(prec);
+    const double ie = 1.0 / (s2 + n * v2);
+    la = v2 * ie;
+    lb = A->mu_mu * s2 * ie + z * sqrt(s2 * v2 * ie);
   };
   if (u < L) {
     const int h = c.heap_of[u];
@@ -503,13 +529,18 @@ __device__ __forceinline__ void pre_decide(const SweepArgs *__restrict__ A, Shar
   } else if (u == L && move != kNone) {
     const double n = move == kGrow ? (double)td.eta_cnt : (double)td.cnt[kl] + (double)td.cnt[kr];
     consts(n, td.eta_z, sh.ma, sh.mb);
-  } else if (u == L + 1 && move == kPrune) {
+  } else if (u >= L + 1 && u <= L + 4 && move == kPrune) {
+    // one quantity per thread, so the divisions and the log run side by side
     const double nl = (double)td.cnt[kl], nr = (double)td.cnt[kr], np = nl + nr;
     const double eL = s2 + nl * v2, eR = s2 + nr * v2, eP = s2 + np * v2;
-    sh.pdL = 1.0 / eL;
-    sh.pdR = 1.0 / eR;
-    sh.pdP = 1.0 / eP;
-    sh.pdet = 0.5 * log(s2 * eP / (eL * eR));
+    if (u == L + 1)
+      sh.pdL = 1.0 / eL;
+    else if (u == L + 2)
+      sh.pdR = 1.0 / eR;
+    else if (u == L + 3)
+      sh.pdP = 1.0 / eP;
+    else
+      sh.pdet = 0.5 * log(s2 * eP / (eL * eR));
   } else if (u == L + 1 && move == kGrow) {
     // the parent eta of a GROW keeps its count: its denominator is known
     const double eP = s2 + (double)td.eta_cnt * v2;
@@ -686,7 +717,7 @@ __device__ __forceinline__ void sigma2_tail(const SweepArgs *__restrict__ A, con
   if (t == 0) {
     double acc = 0.0;
     for (int u = 0; u < kWaves; ++u) acc += sh.wave_part[u];
-    st_dev(mailbox(A, par, w), mk_word(seq, pack_f64(acc)));
+    post(A, sh, par, 0, mk_word(seq, pack_f64(acc)));
   }
   gather_total(A, sh, par, seq, 1);
   // acquire by the wave whose lanes polled (its cache invalidation serves
@@ -904,7 +935,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   __syncthreads();
-  if (t == 0) st_dev(mailbox(A, 1, w), mk_word(1, 0));
+  if (t == 0) post(A, sh, 1, 0, mk_word(1, 0));
   gather_total(A, sh, 1, 1, 0);
   // acquire by the polling wave; the barrier orders the other waves after it
   if (t < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
@@ -932,7 +963,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       if (more1) route(j + 1, rk2);
       if (t <= L) {
         const uint64_t pay = t < L ? pack_f64(partial(L, t)) : (uint64_t)sh.nr[j & 1];
-        st_dev(mailbox(A, par, w) + t, mk_word(seq, pay));
+        post(A, sh, par, t, mk_word(seq, pay));
       }
       // 2. while the mailboxes fill: load rows of j+2, the decision data of
       //    j+1 and the proposal of j+3
@@ -1365,7 +1396,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   __syncthreads();
-  if (t == 0) st_dev(mailbox(A, 1, w), mk_word(1, 0));
+  if (t == 0) post(A, sh, 1, 0, mk_word(1, 0));
   gather_total(A, sh, 1, 1, 0);
   // acquire by the polling wave; the barrier orders the other waves after it
   if (t < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
@@ -1385,7 +1416,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       const bool more3 = more1 && (j + 3 < m);
       if (t <= L) {
         const uint64_t pay = t < L ? pack_f64(partial(L, t)) : (uint64_t)sh.nr[j & 1];
-        st_dev(mailbox(A, par, w) + t, mk_word(seq, pay));
+        post(A, sh, par, t, mk_word(seq, pay));
       }
       const int j1 = more1 ? j + 1 : j, j3 = more3 ? j + 3 : j;
       const TdRegs tdn = load_tree_data(A, sh.ctx[j1 & (kRing - 1)], j1, s);
