@@ -976,8 +976,12 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       if (t == L) sh.nr[j & 1] = 0;
       // 3. totals of tree j, in the same order in every workgroup: polls into
       //    per-segment partials, then one wave reduces a word over the
-      //    segments with the fixed-order DPP tree (nseg <= 32 lanes)
+      //    segments with the fixed-order DPP tree (nseg <= 32 lanes).  Before
+      //    that, waves 0-3 build the rank table of tree j+2 (its proposal was
+      //    staged a step ago) while waves 4-7 compute tree j's count-only
+      //    constants
       const int K = L + 1;
+      if (more2) build_ranks(A, sh.ctx[(j + 2) & (kRing - 1)]);
       pre_decide(A, sh, c, sh.td[j & 1], w == 0 ? uncounted : -1);
       const int nseg = gather_polls(A, sh, par, seq, K, L);
       decide_step(A, sh, c, sh.td[j & 1], nseg);
@@ -1022,8 +1026,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       }
       finish_tree(A, Lc, sh, c, j, s, step);
       uncounted = j;
-      // 5. tree j+1: rank table of j+3, partial sums from the updated residuals
-      if (more3) build_ranks(A, sh.ctx[(j + 3) & (kRing - 1)]);
+      // 5. tree j+1: partial sums from the updated residuals
       if (more1) {
         reduce(j + 1, rk2);
 #pragma unroll
