@@ -874,8 +874,9 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   };
   // partial sums of tree `tree` from the current residuals: per-lane private
   // LDS bins for up to kBinRanks ranks at a time (a plain read-modify-write:
-  // LDS float atomics are many times slower; padding points and ranks outside
-  // the pass add 0 to a bin of the pass, so there is no branch per point),
+  // LDS float atomics are many times slower; ranks outside the pass, the
+  // null rank of padding points among them, add 0 to a bin of the pass, so
+  // there is no branch per point),
   // then a fixed-order fp64 reduction into sh.red; larger trees take several
   // passes.  Ends with an LDS barrier.
   auto reduce = [&](int tree, const uint32_t (&rks)[V]) {
