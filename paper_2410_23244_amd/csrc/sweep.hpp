@@ -781,15 +781,21 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   uint32_t rk2[V];  // ranks of the next tree
   ChunkT rawc[V];
   uint32_t rawx[V];
-  uint32_t okm[V];  // bit b: observation 4*chunk+b exists
+  // chunk v of this thread exists iff t + v kBlock < lim, lim uniform over
+  // the workgroup: no per-chunk mask is kept across the loop (a chunk past
+  // the end has no load of its own and routes to the null rank)
+  const int32_t lim = A->chunks - w * V * kBlock;
+  auto chunk_ok = [&](int v) { return t + v * kBlock < lim; };
+  // bit b: observation 4 chunk + b exists (sigma^2 step and epilogue)
+  auto ok4 = [&](int v) -> uint32_t {
+    const int32_t rem = A->n - 4 * ((w * V + v) * kBlock + t);
+    return !chunk_ok(v) ? 0u : (rem >= 4 ? 15u : ((1u << rem) - 1u));
+  };
 #pragma unroll
   for (int v = 0; v < V; ++v) {
     const int32_t ch = (w * V + v) * kBlock + t;
-    okm[v] = 0;
     r[v][0] = r[v][1] = r[v][2] = r[v][3] = 0.f;
-    if (ch < A->chunks) {
-      const int32_t rem = A->n - 4 * ch;
-      okm[v] = rem >= 4 ? 15u : ((1u << rem) - 1u);
+    if (chunk_ok(v)) {
       const gptr<const float> q = gbl((const float *)A->resid) + 4 * (int64_t)ch;
       r[v][0] = q[0];
       r[v][1] = q[1];
@@ -819,13 +825,14 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     const gptr<const ChunkT> row =
         gbl((const ChunkT *)((const char *)A->idx + (int64_t)tree * A->ldi * IB));
     const gptr<const uint32_t> xrow = gbl((const uint32_t *)(A->X + (int64_t)c.pr.axis * A->ldx));
+    // unconditional loads (chunk 0 stands in for a chunk past the end)
 #pragma unroll
-    for (int v = 0; v < V; ++v)
-      if (okm[v]) {
-        const int32_t ch = (w * V + v) * kBlock + t;
-        rawc[v] = row[ch];
-        rawx[v] = xrow[ch];
-      }
+    for (int v = 0; v < V; ++v) {
+      const int32_t ch = (w * V + v) * kBlock + t;
+      const int32_t cc = chunk_ok(v) ? ch : 0;
+      rawc[v] = row[cc];
+      rawx[v] = xrow[cc];
+    }
   };
   // route this workgroup's points through tree `tree` (rows already loaded):
   // rank of each point's leaf in the larger tree, GROW right-count into nr
@@ -837,16 +844,19 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     int cp[V][4];
     int nr = 0;
 #pragma unroll
-    for (int v = 0; v < V; ++v)
+    for (int v = 0; v < V; ++v) {
+      // a chunk past the end: index 0, the null rank, for all its points
+      const ChunkT rc = chunk_ok(v) ? rawc[v] : (ChunkT)0;
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
-        const int ci = IC::get(rawc[v], b);
+        const int ci = IC::get(rc, b);
         const int xi = (rawx[v] >> (8 * b)) & 0xff;
         const int in = ci == grow_eta;
         const int right = xi >= cutv;
         cp[v][b] = (in ? 2 * eta + right : ci) & 255;
         nr += (in && right) ? 1 : 0;
       }
+    }
     int r0[V][4];
 #pragma unroll
     for (int v = 0; v < V; ++v)
@@ -1022,7 +1032,8 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
             touch |= pair;
             out = IC::put(out, b, (merged && pair) ? eta : (int)c.heap_of[rnk]);
           }
-          if (touch && okm[v]) row[(w * V + v) * kBlock + t] = out;
+          // only an existing chunk has a point of the move's pair
+          if (touch) row[(w * V + v) * kBlock + t] = out;
         }
       }
       finish_tree(A, Lc, sh, c, j, s, step);
@@ -1047,7 +1058,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       for (int v = 0; v < V; ++v)
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
-          const double x = ((okm[v] >> b) & 1u) ? (double)r[v][b] : 0.0;
+          const double x = (double)r[v][b];  // 0 at padding points
           ssr += x * x;
         }
       ssr = wave_total63(ssr);
@@ -1056,7 +1067,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       if (A->probit)
 #pragma unroll
         for (int v = 0; v < V; ++v)
-          if (okm[v]) latent_chunk(A, seed, s, (w * V + v) * kBlock + t, okm[v], r[v]);
+          if (const uint32_t ok = ok4(v)) latent_chunk(A, seed, s, (w * V + v) * kBlock + t, ok, r[v]);
       j = 0;
       ++s;
       if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s);
@@ -1066,7 +1077,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   // ---- epilogue: residuals back to HBM, statistics, device errors
 #pragma unroll
   for (int v = 0; v < V; ++v)
-    if (okm[v]) {
+    if (chunk_ok(v)) {
       const int32_t ch = (w * V + v) * kBlock + t;
       const gptr<float> q = gbl(A->resid) + 4 * (int64_t)ch;
       q[0] = r[v][0];
