@@ -127,6 +127,30 @@ __device__ __forceinline__ uint32_t exhausted_set(const Anc &P, int h) {
   return e;
 }
 
+// exhausted_set for a wave-uniform path (the node of the move): lane u < 7
+// takes ancestor u; all 64 lanes must call it
+__device__ __forceinline__ uint32_t exhausted_set_wave(const Anc &P, int h) {
+  const int u = threadIdx.x & 63;
+  uint32_t wu = P.w[0];
+#pragma unroll
+  for (int i = 1; i < kMaxAnc; ++i) wu = u == i ? P.w[i] : wu;
+  const int a = wd_axis(wu);
+  bool rep = u < P.d;
+  int lo = 0, hi = wd_nc(wu);
+#pragma unroll
+  for (int v = kMaxAnc - 1; v >= 0; --v) {
+    const bool same = v < P.d && wd_axis(P.w[v]) == a;
+    rep = rep && !(v > u && same);
+    if (same) {
+      if ((h >> v) & 1)
+        lo = wd_cut(P.w[v]);
+      else
+        hi = wd_cut(P.w[v]) - 1;
+    }
+  }
+  return (uint32_t)__ballot(rep && hi - lo <= 0) & ((1u << kMaxAnc) - 1u);
+}
+
 __device__ __forceinline__ double prob_grow(const SweepArgs *__restrict__ A, int nG, int nP) {
   return nP == 0 ? 1.0 : (nG == 0 ? 0.0 : A->p_grow);
 }
@@ -244,6 +268,9 @@ __device__ __noinline__ void propose_tree(const SweepArgs *__restrict__ A, Key k
   double c_prior = 0.0;
   uint64_t big[4] = {leaf[0], leaf[1], leaf[2], leaf[3]};
   int rank_l = -1, rank_r = -1;
+  // arguments of the logarithms of the count-free ratio (1 when unused)
+  double ps_eta = 1.0, ps_l = 0.0, ps_r = 0.0, pg_small = 1.0, pg_big = 0.0;
+  int nG_small = 1, nP_big = 1;
   if (nG > 0 || nP > 0) {
     move = unit(b.w0) < prob_grow(A, nG, nP) ? kGrow : kPrune;
     uint64_t cand[4];
@@ -253,34 +280,28 @@ __device__ __noinline__ void propose_tree(const SweepArgs *__restrict__ A, Key k
     const Anc Pe = ancestors(T, eta, H);
     const int d = Pe.d;
     // a PRUNE needs only the sign of P_d at eta, known when every node keeps an axis
-    const uint32_t ex = move == kGrow || !all_avail ? exhausted_set(Pe, eta) : 0u;
+    const uint32_t ex = move == kGrow || !all_avail ? exhausted_set_wave(Pe, eta) : 0u;
     const int nex = __popc(ex);
     const int padj_eta = A->p_nz - nex;
-    const double ps_eta = psplit(A, tab, d, padj_eta);
+    ps_eta = psplit(A, tab, d, padj_eta);
     const bool sib_leaf = eta > 1 && bit4(leaf, eta ^ 1);
-    double ps_l, ps_r;
-    int nG_small, nP_small, nG_big, nP_big;
+    int nP_small, nG_big;
     if (move == kGrow) {
-      // the idx-th axis with cuts that is not exhausted at eta: skip the
-      // exhausted ranks in increasing order
-      int idx = pick((uint32_t)(b.w1 >> 32), padj_eta);
+      // the idx0-th axis with cuts that is not exhausted at eta: skipping the
+      // exhausted ranks in increasing order (each at or below the running
+      // index moves it up by one) ends at the least r >= idx0 with
+      // r = idx0 + #{exhausted ranks <= r}, which lies in idx0..idx0+7;
+      // lane c tests r = idx0 + c
+      const int idx0 = pick((uint32_t)(b.w1 >> 32), padj_eta);
       int rk[kMaxAnc];
 #pragma unroll
       for (int u = 0; u < kMaxAnc; ++u) rk[u] = node_rank(T, u < d ? eta >> (u + 1) : 1, H);
-      int prev = INT32_MIN;
+      const int rc = idx0 + l;
+      int below = 0;
 #pragma unroll
-      for (int pass = 0; pass < kMaxAnc; ++pass) {
-        int best = INT32_MAX;
-#pragma unroll
-        for (int u = 0; u < kMaxAnc; ++u) {
-          const int k8 = rk[u] * 8 + u;  // ties broken by ancestor
-          if (((ex >> u) & 1u) && k8 > prev && k8 < best) best = k8;
-        }
-        if (best != INT32_MAX) {
-          idx += ((best >> 3) <= idx);
-          prev = best;
-        }
-      }
+      for (int u = 0; u < kMaxAnc; ++u) below += (((ex >> u) & 1u) && rk[u] <= rc) ? 1 : 0;
+      const uint64_t fixed = __ballot(l <= kMaxAnc && idx0 + below == rc);
+      const int idx = idx0 + __ffsll((long long)fixed) - 1;
       a = gbl(A->nz_list)[idx];
       int lo = 0, hi = ncut[a];
       path_bounds(Pe, eta, a, lo, hi);
@@ -299,28 +320,39 @@ __device__ __noinline__ void propose_tree(const SweepArgs *__restrict__ A, Key k
     } else {
       const Anc Pl = ancestors(T, 2 * eta, H), Pr = ancestors(T, 2 * eta + 1, H);
       ps_l = psplit(A, tab, d + 1,
-                    all_avail ? A->p_nz : A->p_nz - __popc(exhausted_set(Pl, 2 * eta)));
+                    all_avail ? A->p_nz : A->p_nz - __popc(exhausted_set_wave(Pl, 2 * eta)));
       ps_r = psplit(A, tab, d + 1,
-                    all_avail ? A->p_nz : A->p_nz - __popc(exhausted_set(Pr, 2 * eta + 1)));
+                    all_avail ? A->p_nz : A->p_nz - __popc(exhausted_set_wave(Pr, 2 * eta + 1)));
       nG_big = nG;
       nP_big = nP;
       nG_small = nG - (ps_l > 0.0) - (ps_r > 0.0) + (ps_eta > 0.0);
       nP_small = nP - 1 + (sib_leaf ? 1 : 0);
     }
-    // count-free part of log r = log[pi(big)/pi(small)] + log[q(big->small)/q(small->big)];
-    // the 1/(p_adj avail) factors of prior and proposal cancel
-    const double pg_small = prob_grow(A, nG_small, nP_small);
-    const double pg_big = prob_grow(A, nG_big, nP_big);
-    const double lr = log(ps_eta) - log(1.0 - ps_eta) + log(1.0 - ps_l) + log(1.0 - ps_r) +
-                      log(1.0 - pg_big) - log((double)nP_big) - log(pg_small) +
-                      log((double)nG_small);
-    c_prior = move == kGrow ? lr : -lr;
+    pg_small = prob_grow(A, nG_small, nP_small);
+    pg_big = prob_grow(A, nG_big, nP_big);
     rank_l = bits_below(big, 2 * eta);
     rank_r = rank_l + 1;
   }
+  // count-free part of log r = log[pi(big)/pi(small)] + log[q(big->small)/q(small->big)]
+  // (the 1/(p_adj avail) factors of prior and proposal cancel), its eight
+  // logarithms one per lane and summed in a fixed order; lane 8 the log of
+  // the accept uniform
+  double arg = unit(b.w3);
+  arg = l == 0 ? ps_eta : arg;
+  arg = l == 1 ? 1.0 - ps_eta : arg;
+  arg = l == 2 ? 1.0 - ps_l : arg;
+  arg = l == 3 ? 1.0 - ps_r : arg;
+  arg = l == 4 ? 1.0 - pg_big : arg;
+  arg = l == 5 ? (double)nP_big : arg;
+  arg = l == 6 ? pg_small : arg;
+  arg = l == 7 ? (double)nG_small : arg;
+  const double lg = log(arg);
+  const double lr = __shfl(lg, 0) - __shfl(lg, 1) + __shfl(lg, 2) + __shfl(lg, 3) +
+                    __shfl(lg, 4) - __shfl(lg, 5) - __shfl(lg, 6) + __shfl(lg, 7);
+  const double ln_u = __shfl(lg, 8);
+  if (move != kNone) c_prior = move == kGrow ? lr : -lr;
   int L = 0;
   for (int k = 0; k < 4; ++k) L += __popcll(big[k]);
-  const double ln_u = log(unit(b.w3));
 
   if (l == 0) {
     P.move = move;
