@@ -365,7 +365,7 @@ __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH 
                                             uint32_t seq, int K, int nsum) {
   const int t = threadIdx.x, G = A->G;
   if (G == 1) {
-    // thread k posted word k itself (post)
+    lds_barrier();  // the words were staged by the waves that formed them
     if (t < K) {
       const uint64_t wv = sh.solo[t];
       double acc = 0.0;
@@ -887,9 +887,13 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   // LDS float atomics are many times slower; ranks outside the pass, the
   // null rank of padding points among them, add 0 to a bin of the pass, so
   // there is no branch per point),
-  // then a fixed-order fp64 reduction into sh.red; larger trees take several
-  // passes.  Ends with an LDS barrier.
-  auto reduce = [&](int tree, const uint32_t (&rks)[V]) {
+  // then a fixed-order fp64 reduction; larger trees take several passes.
+  // The wave that forms the total of rank k posts it as word k of this
+  // workgroup's mailbox for the step that decides the tree (buffer par,
+  // step number seq), and after the first bin barrier thread kBlock-1 posts
+  // the GROW right-count that route(tree) gathered as word L: no barrier
+  // stands between the totals and the post (only between passes).
+  auto reduce = [&](int tree, const uint32_t (&rks)[V], int par, uint32_t seq) {
     const int L = sh.ctx[tree & (kRing - 1)].pr.L;
     for (int base = 0; base < L; base += kBinRanks) {
 #pragma unroll
@@ -901,6 +905,11 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
           sh.bins[(((in ? rnk : 0) * kWaves + wave) << 6) | lane] += in ? r[v][b] : 0.f;
         }
       lds_barrier();
+      if (base == 0 && t == kBlock - 1) {
+        // cleared for route(tree + 2), the next to count into this slot
+        post(A, sh, par, L, mk_word(seq, (uint64_t)sh.nr[tree & 1]));
+        sh.nr[tree & 1] = 0;
+      }
       for (int k = base + wave; k < min(L, base + kBinRanks); k += kWaves) {
         double acc = 0.0;
 #pragma unroll
@@ -910,16 +919,15 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
           sh.bins[q] = 0.f;
         }
         const double tot = wave_total63(acc);
-        if (lane == 63) sh.red[k] = tot;
+        if (lane == 63) post(A, sh, par, k, mk_word(seq, pack_f64(tot)));
       }
-      lds_barrier();
+      if (base + kBinRanks < L) lds_barrier();
     }
   };
-  // this workgroup's partial sum of rank k (after reduce)
-  auto partial = [&](int, int k) { return sh.red[k]; };
   // proposals of trees j0.. j0+2 into the ring, rank tables, rows of j0,
   // route of j0, rows of j0+1, decision data of j0, partial sums of j0
-  auto refill = [&](int j0, int64_t s) {
+  // (posted for launch step `next`, which decides tree j0)
+  auto refill = [&](int j0, int64_t s, int next) {
     for (int q = 0; q < 3; ++q)
       if (j0 + q < m) {
         const uint32_t wd = load_prop_word(A, j0 + q);
@@ -934,7 +942,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     route(j0, rk);
     if (j0 + 1 < m) issue_rows(j0 + 1);
     store_tree_data(sh.td[j0 & 1], sh.ctx[j0 & (kRing - 1)], tr0);
-    reduce(j0, rk);
+    reduce(j0, rk, next & 1, (uint32_t)next + 2);
   };
 
   // ---- prologue: proposals and normals of the first sweep, grid rendezvous
@@ -951,7 +959,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   // acquire by the polling wave; the barrier orders the other waves after it
   if (t < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __syncthreads();
-  if (j < m && !sh.abort_flag) refill(j, s);
+  if (j < m && !sh.abort_flag) refill(j, s, 0);
 
 #pragma unroll 1
   for (int step = 0; step < Lc.n_steps; ++step) {
@@ -969,13 +977,10 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       const bool more1 = (j + 1 < m) && (step + 1 < Lc.n_steps);  // tree j+1 follows
       const bool more2 = more1 && (j + 2 < m);
       const bool more3 = more2 && (j + 3 < m);
-      // 1. route tree j+1 (its rows were loaded a step ago), then post this
-      //    workgroup's partial sums of tree j and its GROW right-count
+      // 1. route tree j+1 (its rows were loaded a step ago); this
+      //    workgroup's partial sums of tree j and its GROW right-count were
+      //    posted by the reduce that formed them
       if (more1) route(j + 1, rk2);
-      if (t <= L) {
-        const uint64_t pay = t < L ? pack_f64(partial(L, t)) : (uint64_t)sh.nr[j & 1];
-        post(A, sh, par, t, mk_word(seq, pay));
-      }
       // 2. while the mailboxes fill: load rows of j+2, the decision data of
       //    j+1 and the proposal of j+3
       // (the small loads first: nothing waits behind the row loads)
@@ -983,8 +988,6 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       const TdRegs tdn = load_tree_data(A, sh.ctx[j1 & (kRing - 1)], j1, s);
       const uint32_t pw3 = load_prop_word(A, j3);
       if (more2) issue_rows(j + 2);
-      lds_barrier();  // nr[j&1] read by the poster before it is cleared
-      if (t == L) sh.nr[j & 1] = 0;
       // 3. totals of tree j, in the same order in every workgroup: polls into
       //    per-segment partials, then one wave reduces a word over the
       //    segments with the fixed-order DPP tree (nseg <= 32 lanes).  Before
@@ -1040,7 +1043,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       uncounted = j;
       // 5. tree j+1: partial sums from the updated residuals
       if (more1) {
-        reduce(j + 1, rk2);
+        reduce(j + 1, rk2, (step + 1) & 1, (uint32_t)step + 3);
 #pragma unroll
         for (int v = 0; v < V; ++v) rk[v] = rk2[v];
       } else {
@@ -1070,7 +1073,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
           if (const uint32_t ok = ok4(v)) latent_chunk(A, seed, s, (w * V + v) * kBlock + t, ok, r[v]);
       j = 0;
       ++s;
-      if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s);
+      if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s, step + 1);
     }
   }
 
@@ -1437,7 +1440,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       const TdRegs tdn = load_tree_data(A, sh.ctx[j1 & (kRing - 1)], j1, s);
       const uint32_t pw3 = load_prop_word(A, j3);
       const uint32_t sw3 = CF ? struct_word(j3) : 0u;
-      lds_barrier();
+      // the poster of the count word clears it (see the register kernel)
       if (t == L) sh.nr[j & 1] = 0;
       pre_decide(A, sh, c, sh.td[j & 1], w == 0 ? uncounted : -1);
       const int nseg = gather_polls(A, sh, par, seq, L + 1, L);
