@@ -158,7 +158,6 @@ struct Shared {
   float newv[kMaxLeaves];      // new value of each larger-tree leaf if it stays a leaf
   float dlt[kMaxLeaves + 1];   // its residual delta: old value - new value; 0 at the null rank
   float newv_m;                // new value of eta if the move ends merged
-  float dlt_m[2];              // residual deltas of the two children in that case
   double wave_part[kWaves];
   uint64_t solo[kMaxLeaves + 1];  // one workgroup per chain: its own mailbox words
   double sigma2;
@@ -479,7 +478,8 @@ __device__ __noinline__ void trace_tree_step(bart_trace *R, Shared &sh, const Ct
 // decision, each child's own draw, the merged draw), waves 4-7 the other
 // leaves; each wave sums the segments of the words it needs with the
 // fixed-order DPP tree (nseg <= 32).  Writes sh.flags, dec_logr, and per
-// rank cntd, S, newv, dlt, plus newv_m and dlt_m for a merged move.
+// rank cntd, S, newv and the final residual delta dlt, plus newv_m for a
+// merged move.
 // Move statistics of workgroup 0 (GROW proposed, PRUNE proposed, GROW
 // accepted, PRUNE accepted, tree steps, leaves after the step) for the tree
 // step whose proposal is c and whose decision flags are still in sh.flags.
@@ -550,8 +550,9 @@ __device__ __forceinline__ void pre_decide(const SweepArgs *__restrict__ A, Shar
 }
 
 // Tree j's decision once the sums are in (sec. 3.3 items 8-10): wave 0 the
-// MH ratio and accept, waves 1-2 the draws of the two move leaves, wave 3
-// the merged draw, waves 4-7 every other leaf.  Every workgroup runs this on
+// MH ratio and accept, waves 1-2 the draws of the two move leaves (each
+// takes the decision as well, so the residual delta it stores is final),
+// wave 3 the merged draw, waves 4-7 every other leaf.  Every workgroup runs this on
 // identical totals.
 __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Shared &sh,
                                             const Ctx &c, const TreeData &td, int nseg) {
@@ -596,13 +597,13 @@ __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Sha
       const double Sr = grow ? Rr + nr * (double)mor : Rr + lnmr;
       const double mm = A->mu_mu;
       const double tL = Sl - nl * mm, tR = Sr - nr * mm, tP = (Sl + Sr) - (nl + nr) * mm;
-      if (wave == 0) {
-        // log marginal-likelihood ratio of splitting a leaf into (L, R): the
-        // partial residuals of a leaf with n points, its N(mu_mu, v2) value
-        // integrated out (sec. 2.1), are N(mu_mu 1, s2 I + v2 1 1^T), so
-        // LLR = 1/2 ln(s2 eP / (eL eR)) + v2 / (2 s2) (tL^2/eL + tR^2/eR -
-        // tP^2/eP) with e = s2 + n v2 and t = S - n mu_mu; the count-only
-        // parts come from pre_decide
+      // log r: the log marginal-likelihood ratio of splitting a leaf into
+      // (L, R) -- the partial residuals of a leaf with n points, its
+      // N(mu_mu, v2) value integrated out (sec. 2.1), are N(mu_mu 1,
+      // s2 I + v2 1 1^T), so LLR = 1/2 ln(s2 eP / (eL eR)) + v2 / (2 s2)
+      // (tL^2/eL + tR^2/eR - tP^2/eP) with e = s2 + n v2 and t = S - n mu_mu,
+      // the count-only parts from pre_decide -- plus the count-free terms
+      auto log_r = [&]() {
         double llr;
         if (grow) {
           const double eL = s2 + nl * v2, eR = s2 + nr * v2;
@@ -612,27 +613,34 @@ __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Sha
         } else {
           llr = pdet + v2 / (2.0 * s2) * (tL * tL * pdL + tR * tR * pdR - tP * tP * pdP);
         }
-        const double logr = c_prior + (grow ? llr : -llr);
+        return c_prior + (grow ? llr : -llr);
+      };
+      const float vm = (float)((Sl + Sr) * ma + mb);
+      if (wave == 0) {
+        const double logr = log_r();
         const int acc = ln_u < logr ? 1 : 0;
         const int merged = (grow && !acc) || (move == kPrune && acc);
         sh.dec_logr = logr;
         sh.flags = acc | (merged << 1);
       } else if (wave == 3) {
-        const float vm = (float)((Sl + Sr) * ma + mb);
         sh.newv_m = vm;
-        sh.dlt_m[0] = mol - vm;
-        sh.dlt_m[1] = mor - vm;
       } else {
+        // the two leaves of the move: each of waves 1 and 2 takes the
+        // decision too (the same arithmetic on the same totals as wave 0),
+        // so its residual delta is final: the child's own draw, or the
+        // merged value of eta
         const bool left = wave == 1;
         const int k = left ? kl : kr;
         const double Sk = left ? Sl : Sr, nk = left ? nl : nr;
         const float mo = left ? mol : mor;
         const float v = grow ? draw_child(s2 + nk * v2, Sk, left ? zl : zr)
                              : (float)(Sk * (left ? lal : lar) + (left ? lbl : lbr));
+        const int acc = ln_u < log_r() ? 1 : 0;
+        const int merged = (grow && !acc) || (move == kPrune && acc);
         sh.cntd[k] = nk;
         sh.S[k] = Sk;
         sh.newv[k] = v;
-        sh.dlt[k] = mo - v;
+        sh.dlt[k] = merged ? mo - vm : mo - v;
       }
     }
   }
@@ -1003,11 +1011,11 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       if (more3 && t < kPropWords) ((uint32_t *)&sh.ctx[(j + 3) & (kRing - 1)].pr)[t] = pw3;
       if (more1) store_tree_data(sh.td[(j + 1) & 1], sh.ctx[(j + 1) & (kRing - 1)], tdn);
       lds_barrier();
-      // 4. residuals and index row (item 11): a point in a child of eta of a
-      //    merged move takes the merged value and the index eta
+      // 4. residuals and index row (item 11): the delta of every rank is
+      //    final (a point in a child of eta of a merged move takes the
+      //    merged value); such a point also takes the index eta
       const int flags = sh.flags, acc = flags & 1, merged = (flags >> 1) & 1;
       const bool changed = acc && move != kNone;
-      const float vm = sh.newv_m, dml = sh.dlt_m[0], dmr = sh.dlt_m[1];
       const gptr<ChunkT> row = gbl((ChunkT *)((char *)A->idx + (int64_t)j * A->ldi * IB));
       float dl[V][4];
 #pragma unroll
@@ -1017,12 +1025,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
 #pragma unroll
       for (int v = 0; v < V; ++v)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const int rnk = (rk[v] >> (8 * b)) & 0xff;
-          const bool to_eta = merged && ((rnk == kl) || (rnk == kr));
-          const float d = to_eta ? (rnk == kl ? dml : dmr) : dl[v][b];
-          r[v][b] += d;
-        }
+        for (int b = 0; b < 4; ++b) r[v][b] += dl[v][b];
       if (changed) {
 #pragma unroll
         for (int v = 0; v < V; ++v) {
@@ -1172,7 +1175,6 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     const int flags = sh.flags, acc = flags & 1, merged = (flags >> 1) & 1;
     const int kl = ca.pr.rank_l, kr = ca.pr.rank_r, eta_a = ca.pr.eta;
     const bool changed = do_a && acc && ca.pr.move != kNone;
-    const float dml = sh.dlt_m[0], dmr = sh.dlt_m[1];
     const bool xa = do_a && ca.pr.move == kGrow, xn = do_n && cn.pr.move == kGrow;
     const int Ln = do_n ? cn.pr.L : 0;
     // index rows of trees ja and jn: rows of the cache, or without one the
@@ -1292,8 +1294,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           for (int b = 0; b < 4; ++b) {
             const int rnk = (rk >> (8 * b)) & 0xff;
             const bool pair = (rnk == kl) || (rnk == kr);
-            const float d = (merged && pair) ? (rnk == kl ? dml : dmr) : dl[b];
-            rv[u][b] += d;
+            rv[u][b] += dl[b];  // final delta of the rank
             touch |= pair;
             if (changed) out = IC::put(out, b, (merged && pair) ? eta_a : (int)ca.heap_of[rnk]);
           }
