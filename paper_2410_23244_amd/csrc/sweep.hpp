@@ -37,7 +37,8 @@
 namespace bart {
 
 constexpr uint32_t kSpinLimit = 1u << 21;
-constexpr int kNullRank = kMaxLeaves;  // rank of a padding point: no bin, zero delta
+constexpr int kNullRank = kMaxLeaves;  // rank of a padding point (slot 0): no bin, zero delta
+constexpr int kBadRank = 255;          // rank of any other non-leaf slot: likewise, and flagged
 constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
 constexpr int kBinRanks = kBinFloats / (kWaves * 64);  // ranks per pass of the LDS bins (64)
 constexpr int kSlotRanks = kBinRanks / 4;  // the same with a bin per chunk position (16)
@@ -98,16 +99,6 @@ __device__ __forceinline__ double wave_total63(double v) {
   return v;
 }
 
-// Sum of an int over the wave into lane 63, with the steps of wave_total63.
-__device__ __forceinline__ int wave_sum63_i32(int v) {
-  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, true);
-  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, true);
-  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, true);
-  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, true);
-  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, true);
-  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, true);
-  return v;
-}
 
 // wave_total63 of three values at once, the steps interleaved so that the
 // three DPP chains overlap.
@@ -128,8 +119,9 @@ __device__ __forceinline__ void wave_totals3(double &a, double &b, double &c) {
 // Per-workgroup view of one tree's proposal.
 struct Ctx {
   Prop pr;
-  uint8_t rank_of[256];          // heap slot -> rank among larger-tree leaves (0xFF: none)
-  uint16_t heap_of[kMaxLeaves + 1];  // rank -> heap slot; the null rank -> 0
+  uint8_t rank_of[256];   // heap slot -> rank among larger-tree leaves (kNullRank: slot 0,
+                          // kBadRank: another non-leaf)
+  uint16_t heap_of[256];  // rank -> heap slot; 0 from kNullRank on
   uint16_t ax[kMaxLeaves];       // without an index cache: the tree's axis and cut per
   uint8_t ct[kMaxLeaves];        // internal heap slot, for Algorithm 1
 };
@@ -156,7 +148,7 @@ struct Shared {
   double S[kMaxLeaves];
   double cntd[kMaxLeaves];
   float newv[kMaxLeaves];      // new value of each larger-tree leaf if it stays a leaf
-  float dlt[kMaxLeaves + 1];   // its residual delta: old value - new value; 0 at the null rank
+  float dlt[256];              // its residual delta: old value - new value; 0 from kNullRank on
   float newv_m;                // new value of eta if the move ends merged
   double wave_part[kWaves];
   uint64_t solo[kMaxLeaves + 1];  // one workgroup per chain: its own mailbox words
@@ -206,7 +198,7 @@ __device__ __forceinline__ void build_ranks(const SweepArgs *__restrict__ A, Ctx
   const int t = threadIdx.x;
   if (t < 256) {
     const int h = t;
-    uint8_t r = 0xFF;
+    uint8_t r = h == 0 ? kNullRank : kBadRank;
     if (h < 2 * A->H && ((c.pr.mask[h >> 6] >> (h & 63)) & 1ull)) {
       int k = 0;
       for (int u = 0; u < (h >> 6); ++u) k += __popcll(c.pr.mask[u]);
@@ -441,7 +433,7 @@ __device__ __noinline__ void trace_tree_step(bart_trace *R, Shared &sh, const Ct
   const int acc = sh.flags & 1, merged = (sh.flags >> 1) & 1;
   if (t < 256) {
     const int rnk = c.rank_of[t];
-    const bool in = rnk != 0xFF && t < 2 * H;
+    const bool in = rnk < kNullRank && t < 2 * H;  // a leaf of the larger tree
     R->count[t] = in ? (int32_t)sh.cntd[rnk] : 0;
     R->sum[t] = in ? sh.S[rnk] : 0.0;
     float lv = 0.f;
@@ -820,9 +812,11 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     sh.dev_err = 0;
     sh.nr[0] = sh.nr[1] = 0;
     sh.sigma2 = A->ctl->sigma2;
-    sh.dlt[kNullRank] = 0.f;
   }
-  if (t < kRing) sh.ctx[t].heap_of[kNullRank] = 0;
+  // ranks from kNullRank on: zero delta, slot 0
+  if (t >= kNullRank && t < 256) sh.dlt[t] = 0.f;
+  for (int q = t; q < kRing * (256 - kNullRank); q += kBlock)
+    sh.ctx[q / (256 - kNullRank)].heap_of[kNullRank + q % (256 - kNullRank)] = 0;
   if (t < 6) sh.stats[t] = 0;
   int uncounted = -1;  // tree step whose move statistics workgroup 0 has yet to count
 
@@ -859,10 +853,10 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       for (int b = 0; b < 4; ++b) {
         const int ci = IC::get(rc, b);
         const int xi = (rawx[v] >> (8 * b)) & 0xff;
-        const int in = ci == grow_eta;
+        const bool in = ci == grow_eta;
         const int right = xi >= cutv;
-        cp[v][b] = (in ? 2 * eta + right : ci) & 255;
-        nr += (in && right) ? 1 : 0;
+        cp[v][b] = in ? 2 * eta + right : ci;  // below 256: eta < 128
+        nr += __popcll(__ballot(in && right));  // wave-uniform
       }
     }
     int r0[V][4];
@@ -870,25 +864,23 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     for (int v = 0; v < V; ++v)
 #pragma unroll
       for (int b = 0; b < 4; ++b) r0[v][b] = c.rank_of[cp[v][b]];
-    uint32_t bad = 0;
+    // slot 0 marks a padding point (its index entry, or no load at all past
+    // the last chunk) and has the null rank, whose delta is 0 and which falls
+    // in no bin, so no per-point mask is needed; any other non-leaf slot is
+    // an inconsistent cache, rank kBadRank (no bin, zero delta), flagged
+    int worst = 0;
 #pragma unroll
     for (int v = 0; v < V; ++v) {
       uint32_t pk = 0;
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
-        // slot 0 marks a padding point (its index entry, or no load at all
-        // past the last chunk): the null rank, whose delta is 0 and which
-        // falls in no bin, so no per-point mask is needed; any other
-        // non-leaf slot is an inconsistent cache (also the null rank)
-        bad |= (r0[v][b] == 0xFF) & (cp[v][b] != 0);
-        const int rnk = r0[v][b] != 0xFF ? r0[v][b] : kNullRank;
-        pk |= (uint32_t)rnk << (8 * b);
+        worst = max(worst, r0[v][b]);
+        pk |= (uint32_t)r0[v][b] << (8 * b);
       }
       out[v] = pk;
     }
-    if (bad) sh.dev_err = 1;
-    nr = wave_sum63_i32(nr);
-    if (lane == 63 && nr) atomicAdd(&sh.nr[tree & 1], nr);
+    if (worst == kBadRank) sh.dev_err = 1;
+    if (lane == 0 && nr) atomicAdd(&sh.nr[tree & 1], nr);
   };
   // partial sums of tree `tree` from the current residuals: per-lane private
   // LDS bins for up to kBinRanks ranks at a time (a plain read-modify-write:
@@ -1134,9 +1126,11 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     sh.dev_err = 0;
     sh.nr[0] = sh.nr[1] = 0;
     sh.sigma2 = A->ctl->sigma2;
-    sh.dlt[kNullRank] = 0.f;
   }
-  if (t < kRing) sh.ctx[t].heap_of[kNullRank] = 0;
+  // ranks from kNullRank on: zero delta, slot 0
+  if (t >= kNullRank && t < 256) sh.dlt[t] = 0.f;
+  for (int q = t; q < kRing * (256 - kNullRank); q += kBlock)
+    sh.ctx[q / (256 - kNullRank)].heap_of[kNullRank + q % (256 - kNullRank)] = 0;
   if (t < 6) sh.stats[t] = 0;
   int uncounted = -1;  // tree step whose move statistics workgroup 0 has yet to count
 
@@ -1144,7 +1138,8 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   // right-count into nr.  Index 0 marks a padding point (its entry in the
   // row, or a chunk past the end whose loaded values were zeroed): the null
   // rank, whose delta is 0 and which falls in no bin; any other non-leaf
-  // slot is an inconsistent cache (also the null rank).
+  // slot is an inconsistent cache, rank kBadRank (likewise inert), and bad
+  // keeps the largest rank seen so the pass can flag it.
   auto ranks4 = [&](const Ctx &c, ChunkT rc, uint32_t rx, int &nr, uint32_t &bad) -> uint32_t {
     const int move = c.pr.move, eta = c.pr.eta, cutv = c.pr.cut;
     const int grow_eta = move == kGrow ? eta : -1;
@@ -1153,13 +1148,12 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     for (int b = 0; b < 4; ++b) {
       const int ci = IC::get(rc, b);
       const int xi = (rx >> (8 * b)) & 0xff;
-      const int in = ci == grow_eta;
+      const bool in = ci == grow_eta;
       const int right = xi >= cutv;
-      const int cp = (in ? 2 * eta + right : ci) & 255;
-      const int r0 = c.rank_of[cp];
+      const int r0 = c.rank_of[in ? 2 * eta + right : ci];  // slot below 256: eta < 128
       nr += __popcll(__ballot(in && right));
-      bad |= (r0 == 0xFF) & (cp != 0);
-      pk |= (uint32_t)(r0 != 0xFF ? r0 : kNullRank) << (8 * b);
+      bad = max(bad, (uint32_t)r0);
+      pk |= (uint32_t)r0 << (8 * b);
     }
     return pk;
   };
@@ -1344,7 +1338,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       if (i0 + 4 * U < cpt) load_batch(i0 + 4 * U, B1);
       compute_batch(B2);
     }
-    if (bad) sh.dev_err = 1;
+    if (bad == kBadRank) sh.dev_err = 1;  // bad: the largest rank seen
     if (do_n && lo == 0 && lane == 0 && nr) atomicAdd(&sh.nr[jn & 1], nr);
     if (want_ssr) {
       const double tot = wave_total63(ssr);
