@@ -895,14 +895,17 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   // stands between the totals and the post (only between passes).
   auto reduce = [&](int tree, const uint32_t (&rks)[V], int par, uint32_t seq) {
     const int L = sh.ctx[tree & (kRing - 1)].pr.L;
+    const int wl = wave * 64 + lane;
     for (int base = 0; base < L; base += kBinRanks) {
+      // the bin of rank k is k mod kBinRanks; a point outside the pass adds
+      // 0 to its bin there (exact: a bin never holds -0)
 #pragma unroll
       for (int v = 0; v < V; ++v)
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
-          const int rnk = ((rks[v] >> (8 * b)) & 0xff) - base;
-          const bool in = rnk >= 0 && rnk < kBinRanks;
-          sh.bins[(((in ? rnk : 0) * kWaves + wave) << 6) | lane] += in ? r[v][b] : 0.f;
+          const uint32_t rb = (rks[v] >> (8 * b)) & 0xffu;
+          const bool in = rb / kBinRanks == (uint32_t)(base / kBinRanks);
+          sh.bins[(int)(rb % kBinRanks) * (kWaves * 64) + wl] += in ? r[v][b] : 0.f;
         }
       lds_barrier();
       if (base == 0 && t == kBlock - 1) {
