@@ -250,6 +250,20 @@ def test_chains_lockstep(nchain, grid, residency, launch):
     assert not np.array_equal(states[0]["leaf"], states[1]["leaf"])
 
 
+def test_chains_of_one_workgroup_lockstep():
+    """Small n: every chain is one workgroup, whose mailbox words stay in LDS;
+    six chains in lockstep with their oracle streams (ragged n: a partial
+    last chunk of padding points)."""
+    inp = make_inputs(1, n=997, p=8, m=20)
+    g = _gpu(inp, launch=ORDINARY, nchain=6)
+    info = g.launch_info()
+    assert info.grid == 1 and info.nchain == 6
+    reps = parity.lockstep_chains(inp, g, seed=13, warm_sweeps=3, n_steps=21 * 3)
+    for rep in reps:
+        print(f"  {rep}", flush=True)
+        assert rep.tree_steps > 0 and rep.moves > 0
+
+
 def test_chain0_equals_a_lone_chain():
     inp = make_inputs(2, n=30011, p=16, m=20)
     many = _gpu(inp, grid=6, nchain=5)
