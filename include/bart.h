@@ -214,8 +214,11 @@ int bart_get_state(bart_handle *h, bart_state *dst);
 
 /* Replace the state of chain src->chain from caller device buffers (index
  * cache and trees must be consistent: every idx entry a leaf of its tree).
- * Per-leaf counts are recomputed on the device.  The position (sweep, next)
- * is shared by all chains: setting it moves every chain. */
+ * Per-leaf counts are recomputed on the device; an idx entry outside heap
+ * slots 1..2H-1 sets BART_DEVERR_CACHE (reported by bart_status), and a
+ * leaf index that is not a leaf of its tree does so during the next
+ * sweep.  The position (sweep, next) is shared by all chains: setting it
+ * moves every chain. */
 int bart_set_state(bart_handle *h, const bart_state *src);
 
 /* Run the next n_steps steps (tree steps and sigma^2 steps, in order, from
