@@ -193,24 +193,26 @@ __device__ __forceinline__ uint32_t load_prop_word(const SweepArgs *__restrict__
   return (gbl((const uint32_t *)(A->prop + j)))[threadIdx.x % kPropWords];
 }
 
-// Rank table of the larger tree from the proposal record already in LDS.
-__device__ __forceinline__ void build_ranks(const SweepArgs *__restrict__ A, Ctx &c) {
-  const int t = threadIdx.x;
-  if (t < 256) {
-    const int h = t;
-    uint8_t r = h == 0 ? kNullRank : kBadRank;
-    if (h < 2 * A->H && ((c.pr.mask[h >> 6] >> (h & 63)) & 1ull)) {
-      int k = 0;
-      for (int u = 0; u < (h >> 6); ++u) k += __popcll(c.pr.mask[u]);
-      // leaves below h in its 64-slot word: h & 63 is this thread's lane
-      const uint64_t mw = c.pr.mask[h >> 6];
-      k += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mw >> 32),
-                                          __builtin_amdgcn_mbcnt_lo((uint32_t)mw, 0u));
-      r = (uint8_t)k;
-      c.heap_of[k] = (uint16_t)h;
-    }
-    c.rank_of[h] = r;
+// Rank-table entry of heap slot h of the larger tree, from the proposal
+// record already in LDS; the calling lane must be h mod 64.
+__device__ __forceinline__ void build_rank_slot(const SweepArgs *__restrict__ A, Ctx &c, int h) {
+  uint8_t r = h == 0 ? kNullRank : kBadRank;
+  if (h < 2 * A->H && ((c.pr.mask[h >> 6] >> (h & 63)) & 1ull)) {
+    int k = 0;
+    for (int u = 0; u < (h >> 6); ++u) k += __popcll(c.pr.mask[u]);
+    // leaves below h in its 64-slot word: h & 63 is this lane
+    const uint64_t mw = c.pr.mask[h >> 6];
+    k += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mw >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((uint32_t)mw, 0u));
+    r = (uint8_t)k;
+    c.heap_of[k] = (uint16_t)h;
   }
+  c.rank_of[h] = r;
+}
+
+// Rank table of the larger tree: threads 0..255, one slot each.
+__device__ __forceinline__ void build_ranks(const SweepArgs *__restrict__ A, Ctx &c) {
+  if (threadIdx.x < 256) build_rank_slot(A, c, (int)threadIdx.x);
 }
 
 // Per-thread registers of one tree's decision data in flight (thread t holds
@@ -994,11 +996,13 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       // 3. totals of tree j, in the same order in every workgroup: polls into
       //    per-segment partials, then one wave reduces a word over the
       //    segments with the fixed-order DPP tree (nseg <= 32 lanes).  Before
-      //    that, waves 0-3 build the rank table of tree j+2 (its proposal was
-      //    staged a step ago) while waves 4-7 compute tree j's count-only
-      //    constants
+      //    that, wave 3 builds the rank table of tree j+2 (its proposal was
+      //    staged a step ago; 4 slots per lane, off the polling waves 0-2)
+      //    while waves 4-7 compute tree j's count-only constants
       const int K = L + 1;
-      if (more2) build_ranks(A, sh.ctx[(j + 2) & (kRing - 1)]);
+      if (more2 && wave == 3)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) build_rank_slot(A, sh.ctx[(j + 2) & (kRing - 1)], 64 * i + lane);
       pre_decide(A, sh, c, sh.td[j & 1], w == 0 ? uncounted : -1);
       const int nseg = gather_polls(A, sh, par, seq, K, L);
       decide_step(A, sh, c, sh.td[j & 1], nseg);
