@@ -36,6 +36,7 @@ CASES = {
     # residuals streamed from HBM: ragged chunks per thread, u16 cache, depth 8
     "w2_stream": (2, dict(n=40003, p=30, m=40), 2, 41 * 2, 4, ORDINARY, STREAM),
     "w1_stream_tiny": (1, dict(n=37, p=3, m=5), 2, 3 * 6, 0, COOP, STREAM),
+    "w1_stream_one_wg": (1, dict(n=997, p=8, m=12), 2, 13 * 2, 1, ORDINARY, STREAM),
     "w4_stream_u16": (4, dict(n=70001, p=20, m=50), 2, 51 + 10, 0, COOP, STREAM),
     "w5_stream_depth8": (5, dict(n=25003, p=1000, m=120), 2, 121 + 5, 3, COOP, STREAM),
 }
