@@ -77,6 +77,16 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Wait for every outstanding vector memory operation of this wave, as an
+// instruction the compiler's own wait analysis sees.  Vector stores count in
+// the same counter as loads, so after the step's stores (index row, mailbox
+// words) the compiler, unable to count them through loops, would otherwise
+// wait for all of them before the next use of an earlier load; issued where
+// only loads are outstanding, this lets later uses go without a wait.
+__device__ __forceinline__ void wait_vm_loads() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), expcnt and lgkmcnt unconstrained
+}
+
 // One DPP move of an fp64 value (both 32-bit halves from the same lane);
 // lanes whose source is disabled or out of range read 0.
 template <int kCtrl, int kRowMask>
@@ -947,6 +957,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     route(j0, rk);
     if (j0 + 1 < m) issue_rows(j0 + 1);
     store_tree_data(sh.td[j0 & 1], sh.ctx[j0 & (kRing - 1)], tr0);
+    wait_vm_loads();  // the rows of j0 + 1 are in before the posts
     reduce(j0, rk, next & 1, (uint32_t)next + 2);
   };
 
@@ -1010,6 +1021,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       if (more3 && t < kPropWords) ((uint32_t *)&sh.ctx[(j + 3) & (kRing - 1)].pr)[t] = pw3;
       if (more1) store_tree_data(sh.td[(j + 1) & 1], sh.ctx[(j + 1) & (kRing - 1)], tdn);
       lds_barrier();
+      wait_vm_loads();  // the rows of j+2 are in before this step's stores
       // 4. residuals and index row (item 11): the delta of every rank is
       //    final (a point in a child of eta of a merged move takes the
       //    merged value); such a point also takes the index eta
@@ -1188,8 +1200,12 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     const gptr<ChunkT> rowa = row_of(do_a ? ja : 0);
     const gptr<ChunkT> rown = row_of(do_n ? jn : 0);
     const bool trav = CF && do_n && lo == 0;  // Algorithm 1 for tree jn
-    const gptr<const uint32_t> xra = gbl((const uint32_t *)(A->X + (int64_t)ca.pr.axis * A->ldx));
-    const gptr<const uint32_t> xrn = gbl((const uint32_t *)(A->X + (int64_t)cn.pr.axis * A->ldx));
+    // a tree's axis is read only when it takes part (a ring slot may not
+    // hold a proposal yet); every proposal's axis is a valid row
+    const gptr<const uint32_t> xra =
+        gbl((const uint32_t *)(A->X + (int64_t)(do_a ? ca.pr.axis : 0) * A->ldx));
+    const gptr<const uint32_t> xrn =
+        gbl((const uint32_t *)(A->X + (int64_t)(do_n ? cn.pr.axis : 0) * A->ldx));
     const gptr<f32x4> res = gbl((f32x4 *)A->resid);
     double ssr = 0.0;
     int nr = 0;
@@ -1203,11 +1219,14 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       ChunkT ra[U], rn[U];
       uint32_t xa4[U], xn4[U];
     };
-    // every lane loads (chunk 0 stands in for chunks past the end) and only
-    // workgroup-uniform conditions select loads, so all of them are in
-    // flight at once; the arithmetic zeroes what a chunk past the end
-    // loaded, after which its points are padding like those of a partial
-    // chunk (index entry 0, residual 0)
+    // every lane issues every load, so each batch is the same fixed number
+    // of loads and the compiler can wait for one batch while the next two
+    // stay in flight (a skipped load would leave it unable to count them,
+    // and it would drain them all); chunk 0 stands in for chunks past the
+    // end and for a load whose value goes unused (one cached line per wave).
+    // The arithmetic zeroes what a chunk past the end loaded, after which
+    // its points are padding like those of a partial chunk (index entry 0,
+    // residual 0)
     auto load_batch = [&](int i0, Batch &B) {
       int32_t cu[U];
 #pragma unroll
@@ -1220,13 +1239,13 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
         B.rv[u] = res[cu[u]];
       }
 #pragma unroll
-      for (int u = 0; u < U; ++u) B.ra[u] = do_a ? rowa[cu[u]] : (ChunkT)0;
+      for (int u = 0; u < U; ++u) B.ra[u] = rowa[do_a ? cu[u] : 0];
 #pragma unroll
-      for (int u = 0; u < U; ++u) B.xa4[u] = xa ? xra[cu[u]] : 0u;
+      for (int u = 0; u < U; ++u) B.xa4[u] = xra[xa ? cu[u] : 0];
 #pragma unroll
-      for (int u = 0; u < U; ++u) B.rn[u] = do_n && !trav ? rown[cu[u]] : (ChunkT)0;
+      for (int u = 0; u < U; ++u) B.rn[u] = rown[do_n && !trav ? cu[u] : 0];
 #pragma unroll
-      for (int u = 0; u < U; ++u) B.xn4[u] = xn ? xrn[cu[u]] : 0u;
+      for (int u = 0; u < U; ++u) B.xn4[u] = xrn[xn ? cu[u] : 0];
     };
     auto compute_batch = [&](Batch &B) {
       int32_t (&ch)[U] = B.ch;
@@ -1331,18 +1350,20 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
         }
       }
     };
+    // batches past the last are loaded too (chunk 0, unused), so every
+    // path through the loop issues the same loads
     Batch B0, B1, B2;
     load_batch(0, B0);
-    if (U < cpt) load_batch(U, B1);
+    load_batch(U, B1);
 #pragma unroll 1
     for (int i0 = 0; i0 < cpt; i0 += 3 * U) {
-      if (i0 + 2 * U < cpt) load_batch(i0 + 2 * U, B2);
+      load_batch(i0 + 2 * U, B2);
       compute_batch(B0);
       if (i0 + U >= cpt) break;
-      if (i0 + 3 * U < cpt) load_batch(i0 + 3 * U, B0);
+      load_batch(i0 + 3 * U, B0);
       compute_batch(B1);
       if (i0 + 2 * U >= cpt) break;
-      if (i0 + 4 * U < cpt) load_batch(i0 + 4 * U, B1);
+      load_batch(i0 + 4 * U, B1);
       compute_batch(B2);
     }
     if (bad == kBadRank) sh.dev_err = 1;  // bad: the largest rank seen
