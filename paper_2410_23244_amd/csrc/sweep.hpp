@@ -10,10 +10,12 @@
 // (predictor-major u8, coalesced 4-byte chunks).
 //
 // There is no coordinating workgroup.  Per tree step j, every workgroup
-//   1. posts its per-leaf partial residual sums of tree j (and, for a GROW,
+//   1. has its per-leaf partial residual sums of tree j (and, for a GROW,
 //      the count of its points going right) in its own mailbox, as 64-bit
 //      words carrying a 20-bit step number over a 44-bit payload, so a
-//      reader needs no fence and no separate flag;
+//      reader needs no fence and no separate flag (posted by the waves that
+//      formed them at the end of the previous step; the streamed kernel
+//      posts them at the start of the step);
 //   2. routes its points through tree j+1 (the route depends only on the
 //      index cache and the proposal, sec. 3.3 "Computations parallel across
 //      trees") while the other mailboxes fill;
@@ -24,7 +26,8 @@
 //   4. applies r += old - new to its residuals and rewrites its part of the
 //      index row where the tree changed (item 11);
 //   5. accumulates tree j+1's partial sums from the updated residuals in
-//      per-lane private LDS bins and reduces them in a fixed order.
+//      per-lane private LDS bins and reduces them in a fixed order; the wave
+//      that forms a total posts it (item 1 of step j+1).
 // One cross-workgroup hop per tree.  Tree j's structure, leaf values and
 // counts are written by its owner workgroup (j mod G) and read by all in
 // the next sweep; the sigma^2 step publishes them with release/acquire
