@@ -4,9 +4,10 @@ A step is one full MCMC sweep (every tree updated in order, then sigma^2)
 over the synthetic workload n=1e6, p=100, ntree=200, depth 6, uint8 index
 cache.  Inputs are generated and uploaded before the timed region.  Warm-up
 and timed sweeps run as bart_step calls of --sweeps-per-launch sweeps each
-(one kernel launch per call); each timed launch is bracketed by HIP events on
-the chain's stream, and the whole timed region by device synchronisations.
-Prints one JSON line.
+(one kernel launch per call), the remainder as one shorter call, so any
+--steps >= 1 and --warmup >= 0 run; each timed launch is bracketed by HIP
+events on the chain's stream, and the whole timed region by device
+synchronisations.  Prints one JSON line.
 
 --chains C runs C independent chains in the same launches (multi-chain
 batching); value is then the chain-sweeps per second summed over the chains
@@ -21,7 +22,9 @@ residual, write the index row) plus 4 bytes per observation per sweep for
 sigma^2; achieved = algorithmic bytes per launch / average launch duration,
 against 8 TB/s.  traffic = HBM bytes per launch measured by the FETCH_SIZE
 and WRITE_SIZE counters (calibrated on a plain copy) for the current kernel
-sources, else null.
+sources, else null; measured_hbm_gbs = traffic / average launch duration.
+copy_ceiling = the bandwidth of a plain 1 GiB device copy timed in the same
+run, the ceiling a streaming kernel can reach on this GPU.
 """
 from __future__ import annotations
 
@@ -42,15 +45,35 @@ def model_bytes_per_sweep(n: int, m: int, idx_bytes: int) -> int:
     return m * n * (9 + 2 * idx_bytes) + 4 * n
 
 
-def cpu_baseline(inp, state, seed: int, sweeps: int) -> dict:
-    """The oracle, single-threaded, on the host, from the device chain's state."""
-    import oracle
-    from tests.parity import chain_from_state
+def launch_plan(sweeps: int, per_launch: int) -> list:
+    """Sweeps of each bart_step call (one kernel launch each) that together run
+    `sweeps` sweeps: full launches of per_launch, then one shorter launch for
+    the remainder.  Any sweeps >= 0 and per_launch >= 1 are accepted."""
+    if sweeps < 0 or per_launch < 1:
+        raise ValueError("sweeps must be >= 0 and per_launch >= 1")
+    plan = [per_launch] * (sweeps // per_launch)
+    if sweeps % per_launch:
+        plan.append(sweeps % per_launch)
+    return plan
 
-    ch = chain_from_state(inp, state)
-    t = time.perf_counter()
-    ch.sweeps(seed, sweeps)
-    dt = time.perf_counter() - t
+
+def cpu_baseline(inp, state, seed: int, sweeps: int) -> dict:
+    """The oracle, single-threaded and pinned to one host core, on the host,
+    from the device chain's state."""
+    import oracle
+
+    ch = oracle.chain_from_state(inp, state)
+    prev = os.sched_getaffinity(0) if hasattr(os, "sched_getaffinity") else None
+    core = min(prev) if prev else None
+    if core is not None:
+        os.sched_setaffinity(0, {core})
+    try:
+        t = time.perf_counter()
+        ch.sweeps(seed, sweeps)
+        dt = time.perf_counter() - t
+    finally:
+        if prev is not None:
+            os.sched_setaffinity(0, prev)
     cpu = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -63,8 +86,8 @@ def cpu_baseline(inp, state, seed: int, sweeps: int) -> dict:
     del oracle
     return {"value": sweeps / dt, "unit": "sweeps/s", "cores": 1, "kind": "oracle",
             "sample": f"{sweeps} sweeps of the same workload from the device chain's state "
-                      f"after warm-up, {dt:.1f} s on 1 thread of {cpu} "
-                      f"(host has {os.cpu_count()} logical CPUs)"}
+                      f"after the timed sweeps, {dt:.1f} s on 1 thread pinned to core {core} "
+                      f"of {cpu} (host has {os.cpu_count()} logical CPUs)"}
 
 
 def copy_probe(mib: int) -> int:
@@ -80,6 +103,29 @@ def copy_probe(mib: int) -> int:
     print(json.dumps({"copy_probe_bytes_read": 4 * n, "copy_probe_bytes_written": 4 * n,
                       "launches": 3}), flush=True)
     return 0
+
+
+def copy_ceiling_gbs(mib: int = 1024, reps: int = 5) -> float:
+    """HBM bandwidth a plain device copy sustains on this GPU: read + write
+    bytes of a 1 GiB f32 copy over its HIP-event time (best of reps)."""
+    import torch
+
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    best = float("inf")
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2 * 4 * n / (best / 1e3) / 1e9
 
 
 SWEEP_SOURCES = ("common.hpp", "propose.hpp", "rng.hpp", "sweep.hpp")
@@ -154,7 +200,7 @@ def bench_predict(args, inp, g) -> int:
     return 0
 
 
-def main() -> int:
+def make_parser() -> argparse.ArgumentParser:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000, help="timed sweeps")
@@ -177,18 +223,33 @@ def main() -> int:
                     help="run without the [ntree][n] index cache (Algorithm 1 every tree step)")
     ap.add_argument("--predict", type=int, default=0, metavar="NT",
                     help="after the warm-up, time bart_predict on NT points instead of sweeps")
+    ap.add_argument("--no-copy-ceiling", dest="copy_ceiling", action="store_false",
+                    help="skip the timed plain copy that gives roofline.copy_ceiling")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (read MIB, write MIB) three "
                          "times, to calibrate HBM byte counters, and exit")
-    args = ap.parse_args()
+    return ap
+
+
+def plans(args) -> tuple:
+    """Sweeps per warm-up launch and per timed launch; ValueError on bad sizes."""
+    if args.steps < 1 or args.warmup < 0 or args.sweeps_per_launch < 1:
+        raise ValueError("--steps and --sweeps-per-launch must be >= 1, --warmup >= 0")
+    return (launch_plan(args.warmup, args.sweeps_per_launch),
+            launch_plan(args.steps, args.sweeps_per_launch))
+
+
+def main() -> int:
+    args = make_parser().parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(the sweep is built and measured on a single MI355X)", file=sys.stderr)
         return 2
     S = args.sweeps_per_launch
-    if S < 1 or args.steps < S or args.steps % S or args.warmup % S:
-        print("--steps must be a positive multiple of --sweeps-per-launch, --warmup a multiple",
-              file=sys.stderr)
+    try:
+        warm_plan, plan = plans(args)
+    except ValueError as e:
+        print(str(e), file=sys.stderr)
         return 2
 
     import torch
@@ -213,21 +274,22 @@ def main() -> int:
               f"{'true' if inp.idx_bytes == 0 else 'false'}>" if info.residency == 2 else
               f"bart::sweep_kernel<{info.chunks_per_thread}, {inp.idx_bytes}>")
     stream = g.stream
-    for _ in range(args.warmup // S):
-        g.step(S, args.seed)
+    for k in warm_plan:
+        g.step(k, args.seed)
     torch.cuda.synchronize()
     assert g.status() == 0, "device error during warm-up"
-    print(f"[bench] warm-up {args.warmup} sweeps done", file=sys.stderr, flush=True)
+    print(f"[bench] warm-up {args.warmup} sweeps done in {len(warm_plan)} launches",
+          file=sys.stderr, flush=True)
     if args.predict:
         return bench_predict(args, inp, g)
 
-    L = args.steps // S
+    L = len(plan)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * L)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    for i in range(L):
+    for i, k in enumerate(plan):
         ev[2 * i].record(stream)
-        g.step(S, args.seed)
+        g.step(k, args.seed)
         ev[2 * i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
@@ -235,13 +297,15 @@ def main() -> int:
     ms = ev[0].elapsed_time(ev[-1])
     launch_ms = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(L)]
     avg_launch = sum(launch_ms) / L
+    sweeps_per_launch = args.steps / L  # mean over the timed launches
     sweeps_per_s = C * args.steps / (ms / 1e3)
     # without an index cache the same model bytes as the u8 cache are counted
     per_sweep = C * model_bytes_per_sweep(inp.n, inp.m, max(1, inp.idx_bytes))
-    achieved = per_sweep * S / (avg_launch / 1e3) / 1e9
-    print(f"[bench] {args.steps} sweeps in {L} launches: events {ms:.1f} ms, wall "
-          f"{wall * 1e3:.1f} ms, per launch {min(launch_ms):.2f}..{max(launch_ms):.2f} ms",
+    achieved = per_sweep * sweeps_per_launch / (avg_launch / 1e3) / 1e9
+    print(f"[bench] {args.steps} sweeps in {L} launches {plan}: events {ms:.2f} ms, wall "
+          f"{wall * 1e3:.1f} ms, per launch {min(launch_ms):.3f}..{max(launch_ms):.3f} ms",
           file=sys.stderr, flush=True)
+    copy_gbs = copy_ceiling_gbs() if args.copy_ceiling else None
 
     cpu = None
     if args.cpu_sweeps > 0:
@@ -257,28 +321,50 @@ def main() -> int:
         # per second summed over the chains, timed like the main line
         gb = from_inputs(inp, launch=mode, nchain=nb)
         ib = gb.launch_info()
-        for _ in range(args.warmup // S):
-            gb.step(S, args.seed)
+        for k in warm_plan:
+            gb.step(k, args.seed)
         torch.cuda.synchronize()
-        Lb = max(1, (args.steps // 2) // S)
+        planb = launch_plan(max(1, args.steps // 2), S)
+        Lb = len(planb)
         evb = [torch.cuda.Event(enable_timing=True) for _ in range(2 * Lb)]
-        for i in range(Lb):
+        for i, k in enumerate(planb):
             evb[2 * i].record(gb.stream)
-            gb.step(S, args.seed)
+            gb.step(k, args.seed)
             evb[2 * i + 1].record(gb.stream)
         torch.cuda.synchronize()
         assert gb.status() == 0, "device error during the batched sweeps"
         msb = evb[0].elapsed_time(evb[-1])
-        avgb = sum(evb[2 * i].elapsed_time(evb[2 * i + 1]) for i in range(Lb)) / Lb
-        achb = nb * model_bytes_per_sweep(inp.n, inp.m, max(1, inp.idx_bytes)) * S / (avgb / 1e3) / 1e9
-        batched = {"chains": nb, "value": nb * Lb * S / (msb / 1e3), "unit": "chain-sweeps/s",
-                   "steps": Lb * S, "ms_per_step": msb / (Lb * S), "grid_per_chain": ib.grid,
+        sweeps_b = sum(planb)
+        achb = (nb * model_bytes_per_sweep(inp.n, inp.m, max(1, inp.idx_bytes)) * sweeps_b /
+                (sum(evb[2 * i].elapsed_time(evb[2 * i + 1]) for i in range(Lb)) / 1e3) / 1e9)
+        batched = {"chains": nb, "value": nb * sweeps_b / (msb / 1e3), "unit": "chain-sweeps/s",
+                   "steps": sweeps_b, "ms_per_step": msb / sweeps_b, "grid_per_chain": ib.grid,
                    "chunks_per_thread": ib.chunks_per_thread,
                    "roofline_achieved_gbs": achb, "roofline_frac": achb / HBM_PEAK_GBS}
         print(f"[bench] {nb} chains batched: {batched['value']:.1f} chain-sweeps/s",
               file=sys.stderr, flush=True)
         gb.close()
 
+    traffic = (stored_traffic(inp.workload, sweeps_per_launch)
+               if C == 1 and not args.no_index_cache else None)
+    roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernel": kernel,
+                "avg_launch_ms": avg_launch, "sweeps_per_launch": sweeps_per_launch,
+                "algorithmic_bytes_per_launch": per_sweep * sweeps_per_launch,
+                # HBM bytes the counters measured per launch over the launch time: with
+                # residuals in registers the kernel moves far fewer bytes than the
+                # algorithmic count and is bound by the latency of its per-tree steps
+                "measured_hbm_gbs": traffic / (avg_launch / 1e3) / 1e9 if traffic else None,
+                "limiter": ("per-tree-step latency (grid exchange and decision); residuals "
+                            "stay in registers" if info.residency != 2 else
+                            "HBM bandwidth and the latency of the fused per-tree pass")}
+    if traffic:
+        roofline["measured_hbm_frac"] = roofline["measured_hbm_gbs"] / HBM_PEAK_GBS
+    if copy_gbs:
+        roofline["copy_ceiling"] = {"gbs": copy_gbs, "frac_of_peak": copy_gbs / HBM_PEAK_GBS,
+                                    "achieved_frac_of_copy": achieved / copy_gbs,
+                                    "kernel": "device-to-device copy of 1 GiB (f32), "
+                                              "read + write bytes over its event time"}
     metric = METRIC
     if args.config != 3 or C > 1 or args.no_index_cache:
         metric = (f"full MCMC sweeps/sec (all trees) at n={inp.n},p={inp.p},ntree={inp.m},"
@@ -292,6 +378,7 @@ def main() -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "launches": plan,
         "ms_per_step": ms / args.steps,
         "higher_is_better": True,
         "scaling": "weak",
@@ -303,11 +390,7 @@ def main() -> int:
                    "launch": args.launch, "grid": info.grid, "nchain": C,
                    "residency": "streamed" if info.residency == 2 else "registers",
                    "chunks_per_thread": info.chunks_per_thread, "parallelism": "1 GPU"},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": stored_traffic(inp.workload, S) if C == 1 else None,
-                     "kernel": kernel, "avg_launch_ms": avg_launch,
-                     "algorithmic_bytes_per_launch": per_sweep * S},
+        "roofline": roofline,
         "cpu_baseline": cpu,
     }
     if batched is not None:

@@ -304,3 +304,27 @@ class Chain:
         lib().oc_predict(C.byref(self.cfg), _ptr(self.axis), _ptr(self.cut), _ptr(self.leaf),
                          _ptr(Xt), Xt.shape[1], Xt.shape[1], offset, _ptr(out))
         return out
+
+
+def config_for(inp, fix_sigma2=False, chain=0) -> Config:
+    """Oracle configuration of a generated workload (an ``Inputs`` object of the
+    seeded input generators: shapes in n, p, m, D, idx_bytes, hyperparameters
+    in ``hyper``).  The oracle always keeps an index cache: u8 when the device
+    runs without one."""
+    h = inp.hyper
+    probit = bool(getattr(inp, "probit", False))
+    return make_config(n=inp.n, p=inp.p, m=inp.m, D=inp.D, idx_bytes=inp.idx_bytes or 1,
+                       alpha=h.alpha, beta=h.beta, mu_mu=h.mu_mu, sigma_mu=h.sigma_mu,
+                       nu=h.nu, lam=h.lam, p_grow=h.p_grow, fix_sigma2=fix_sigma2,
+                       chain=chain, probit=probit,
+                       probit_offset=inp.offset if probit else 0.0)
+
+
+def chain_from_state(inp, st: dict, chain: int = 0) -> Chain:
+    """An oracle chain of workload inp (random stream `chain`) loaded with a
+    state snapshot: a dict with axis, cut, leaf, idx, resid, sigma2, sweep,
+    next (and latent for probit), in the layouts of ``Chain``."""
+    ch = Chain(config_for(inp, chain=chain), inp.X_b, inp.n_cuts, inp.y_c, st["sigma2"])
+    ch.load(st["axis"], st["cut"], st["leaf"], st["idx"], st["resid"], st["sigma2"],
+            st["sweep"], st["next"], latent=st.get("latent"))
+    return ch

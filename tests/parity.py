@@ -42,22 +42,8 @@ class Report:
     notes: list = field(default_factory=list)
 
 
-def oracle_config(inp, fix_sigma2=False, chain=0):
-    h = inp.hyper
-    # the oracle always keeps an index cache (u8 when the device has none)
-    return oracle.make_config(n=inp.n, p=inp.p, m=inp.m, D=inp.D, idx_bytes=inp.idx_bytes or 1,
-                              alpha=h.alpha, beta=h.beta, mu_mu=h.mu_mu, sigma_mu=h.sigma_mu,
-                              nu=h.nu, lam=h.lam, p_grow=h.p_grow, fix_sigma2=fix_sigma2,
-                              chain=chain, probit=getattr(inp, "probit", False),
-                              probit_offset=inp.offset if getattr(inp, "probit", False) else 0.0)
-
-
 def chain_from_state(inp, st, chain=0) -> oracle.Chain:
-    ch = oracle.Chain(oracle_config(inp, chain=chain), inp.X_b, inp.n_cuts, inp.y_c,
-                      st["sigma2"])
-    ch.load(st["axis"], st["cut"], st["leaf"], st["idx"], st["resid"], st["sigma2"],
-            st["sweep"], st["next"], latent=st.get("latent"))
-    return ch
+    return oracle.chain_from_state(inp, st, chain=chain)
 
 
 def _leaf_l1(inp, idx_row, resid, leaf_row, move, eta, a, s):
