@@ -192,6 +192,25 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c,
  * calls of k sweeps equal one call of 2k. */
 int bart_step(bart_handle *h, int32_t k_sweeps, uint64_t seed);
 
+/* For callers that cannot allocate device memory or must not have the
+ * library touch caller memory beyond the handle's state (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * sweeps as bart_step, with the same arguments, results and error behaviour,
+ * but the sweep kernel's cross-workgroup mailboxes (its only scratch data:
+ * per-workgroup partial sums tagged with step numbers) live in a static
+ * device array of the library instead of the workspace.  The array holds 2 x
+ * 256 x 144 64-bit words (576 KiB) per device, enough for every launch shape
+ * bart_init accepts (grid x nchain <= 256 workgroups); it is held by each
+ * device the library runs on until the process ends.  The call allocates
+ * nothing and enqueues only kernels (a fill kernel clears the mailboxes at
+ * the start of every launch, so contents left by earlier calls are never
+ * read).  All calls on one device share that array: calls that overlap on
+ * one device (handles driven from different streams or threads at the same
+ * time) race and produce wrong results; calls ordered on one stream, or
+ * separated by synchronisation, are safe.  BART_ENOTSUP if the handle's
+ * mailboxes would not fit the array. */
+int bart_step_static(bart_handle *h, int32_t k_sweeps, uint64_t seed);
+
 /* Add f(x) and f(x)^2, in fp64 before rounding, to sum and sumsq (device
  * f64 [nchain][n_t]) for every chain: called once per kept sweep it
  * accumulates the posterior mean and variance of f at the points of Xt

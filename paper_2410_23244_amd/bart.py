@@ -81,6 +81,7 @@ def lib():
         L.bart_workspace_bytes.restype = C.c_size_t
         L.bart_init.argtypes = [P(Config), vp, vp, vp, vp, C.c_size_t, vp, P(vp)]
         L.bart_step.argtypes = [vp, C.c_int32, C.c_uint64]
+        L.bart_step_static.argtypes = [vp, C.c_int32, C.c_uint64]
         L.bart_predict.argtypes = [vp, vp, C.c_int64, C.c_int64, C.c_double, vp]
         L.bart_predict_accumulate.argtypes = [vp, vp, C.c_int64, C.c_int64, C.c_double, vp, vp]
         L.bart_cutpoints.argtypes = [vp, C.c_int64, C.c_int32, C.c_int64, C.c_int32, C.c_int32,
@@ -97,7 +98,7 @@ def lib():
         L.bart_destroy.argtypes = [vp]
         L.bart_destroy.restype = None
         L.bart_last_error.restype = C.c_char_p
-        for f in ["bart_init", "bart_step", "bart_predict", "bart_get_state", "bart_set_state",
+        for f in ["bart_init", "bart_step", "bart_step_static", "bart_predict", "bart_get_state", "bart_set_state",
                   "bart_debug_steps", "bart_status", "bart_launch_info",
                   "bart_predict_accumulate", "bart_cutpoints", "bart_bin", "bart_default_hyper",
                   "bart_move_stats"]:
@@ -128,6 +129,10 @@ def bart_init(cfg: Config, X_b_ptr: int, y_c_ptr: int, n_cuts: np.ndarray, ws_pt
 
 def bart_step(h: int, k_sweeps: int, seed: int) -> None:
     _check(lib().bart_step(h, int(k_sweeps), int(seed)))
+
+
+def bart_step_static(h: int, k_sweeps: int, seed: int) -> None:
+    _check(lib().bart_step_static(h, int(k_sweeps), int(seed)))
 
 
 def bart_predict(h: int, xt_ptr: int, xt_stride: int, n_t: int, offset: float,
@@ -270,6 +275,9 @@ class Bart:
     # -- running
     def step(self, k_sweeps: int, seed: int) -> None:
         bart_step(self.h, k_sweeps, seed)
+
+    def step_static(self, k_sweeps: int, seed: int) -> None:
+        bart_step_static(self.h, k_sweeps, seed)
 
     def debug_steps(self, n_steps: int, seed: int) -> np.ndarray:
         torch = self.torch

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -46,7 +47,7 @@ struct Layout {
   int32_t nchain;
   int32_t gcap;  // workgroups per chain the mailboxes are sized for
   size_t resid, idx, axis, cut, leaf, count, prop, z, ctl, pub, latent, chain_bytes;
-  size_t n_cuts, nz_list, nz_rank, ybin, args, total;
+  size_t n_cuts, nz_list, nz_rank, ybin, args, args_static, total;
 };
 
 int nchain_of(const bart_config &c) { return c.nchain > 0 ? c.nchain : 1; }
@@ -115,6 +116,9 @@ Layout make_layout(const bart_config &c) {
   L.nz_rank = take(sizeof(int32_t) * c.p);
   L.ybin = take(c.probit ? L.n_pad : 0);
   L.args = take(sizeof(SweepArgs) * L.nchain);
+  // the same arguments with the mailboxes in the library's static scratch
+  // array (bart_step_static)
+  L.args_static = take(sizeof(SweepArgs) * L.nchain);
   L.total = o;
   return L;
 }
@@ -139,6 +143,38 @@ SweepFn sweep_fn(int V, int IB) { return IB == 1 ? regs_fn<1>(V) : regs_fn<2>(V)
 SweepFn stream_fn(int IB) {
   return IB == 0 ? sweep_kernel_stream<1, true>
                  : (IB == 1 ? sweep_kernel_stream<1, false> : sweep_kernel_stream<2, false>);
+}
+
+// ------------------------------------------------------- static scratch
+// Mailboxes of bart_step_static: a file-scope device array instead of the
+// workspace, for callers that cannot allocate.  Chain c of a handle with
+// nchain chains uses words [c, c + 1) x kStaticChainWords with
+// kStaticChainWords = 2 (kMaxGrid / nchain) kStride: the same per-chain
+// capacity the workspace reserves.  Each device holds its own copy; host
+// code never uses the array's name as an address, only the per-device
+// address from hipGetSymbolAddress (scratch_ptr).
+constexpr int64_t kScratchWords = 2 * (int64_t)kMaxGrid * kStride;  // 576 KiB
+static __device__ __align__(256) uint64_t scratch[kScratchWords];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint64_t *g_scratch[kMaxDevices];  // device address of scratch, per device
+
+// The address of this device's scratch array; looked up once per device,
+// with that device current (bart_init).
+int scratch_ptr(int device, uint64_t **out) {
+  if (device < 0 || device >= kMaxDevices)
+    return fail(BART_ENOTSUP, "device %d beyond the %d devices the library tracks", device,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch[device]) {
+    void *p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(BART_EHIP, "hipGetSymbolAddress returned NULL for the scratch array");
+    g_scratch[device] = (uint64_t *)p;
+  }
+  *out = g_scratch[device];
+  return BART_OK;
 }
 
 // ---------------------------------------------------------------- kernels
@@ -385,6 +421,7 @@ struct bart_handle {
   int32_t next;
   std::vector<int32_t> n_cuts, nz_list, nz_rank;
   SweepFn fn;
+  uint64_t *scratch_dev;  // device address of this device's scratch array
 };
 
 namespace {
@@ -445,14 +482,19 @@ SweepArgs make_args(bart_handle *h, int ch) {
 }
 
 int launch_sweep(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace,
-                 int64_t trace_stride) {
+                 int64_t trace_stride, bool in_scratch) {
   HIP_TRY(hipSetDevice(h->device));
-  // mailbox words carry launch-relative step numbers: clear both buffers
+  // mailbox words carry launch-relative step numbers: clear both buffers of
+  // every chain (a fill kernel, so the call can be captured into a graph)
   const int64_t words = 2 * (int64_t)h->G * kStride;
-  k_clear_mailboxes<<<dim3(grid_for(words, 256), h->nchain), 256, 0, h->stream>>>(
-      h->ws, h->lay.pub, h->lay.chain_bytes, words);
+  if (in_scratch)
+    k_clear_mailboxes<<<dim3(grid_for(words, 256), h->nchain), 256, 0, h->stream>>>(
+        (char *)h->scratch_dev, 0, sizeof(uint64_t) * 2 * h->lay.gcap * kStride, words);
+  else
+    k_clear_mailboxes<<<dim3(grid_for(words, 256), h->nchain), 256, 0, h->stream>>>(
+        h->ws, h->lay.pub, h->lay.chain_bytes, words);
   HIP_TRY(hipGetLastError());
-  const SweepArgs *A = at<SweepArgs>(h, h->lay.args);
+  const SweepArgs *A = at<SweepArgs>(h, in_scratch ? h->lay.args_static : h->lay.args);
   Launch Lc{h->sweep, h->next, n_steps, seed, trace, trace_stride};
   void *args[] = {&A, &Lc};
   // the grid holds at most one workgroup per compute unit (checked at init)
@@ -474,11 +516,12 @@ void advance(bart_handle *h, int64_t steps) {
 
 // Steps in launches of at most kMaxLaunchSteps (the mailbox step numbers
 // are 20 bits wide and restart with every launch).
-int run_steps(bart_handle *h, int64_t steps, uint64_t seed, bart_trace *trace) {
+int run_steps(bart_handle *h, int64_t steps, uint64_t seed, bart_trace *trace,
+              bool in_scratch = false) {
   int64_t done = 0;
   while (done < steps) {
     const int32_t k = (int32_t)std::min<int64_t>(steps - done, kMaxLaunchSteps);
-    const int rc = launch_sweep(h, k, seed, trace ? trace + done : nullptr, steps);
+    const int rc = launch_sweep(h, k, seed, trace ? trace + done : nullptr, steps, in_scratch);
     if (rc) return rc;
     advance(h, k);
     done += k;
@@ -519,6 +562,8 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
   const int64_t chunks = ((int64_t)cfg->n + 3) / 4;
   int device = 0;
   HIP_TRY(hipGetDevice(&device));
+  uint64_t *scratch_dev = nullptr;
+  if (const int rc = scratch_ptr(device, &scratch_dev)) return rc;
   hipDeviceProp_t prop;
   HIP_TRY(hipGetDeviceProperties(&prop, device));
   // launch shape: one workgroup per CU at most, every workgroup owns a slice
@@ -583,6 +628,7 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
   h->nz_list = nzl;
   h->nz_rank = nzr;
   h->fn = fn;
+  h->scratch_dev = scratch_dev;
   if (h->nz_list.empty()) h->nz_list.push_back(0);
 
   auto init = [&]() -> int {
@@ -616,6 +662,12 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
     }
     HIP_TRY(hipMemcpyAsync(at<SweepArgs>(h, lay.args), args.data(), sizeof(SweepArgs) * nchain,
                            hipMemcpyHostToDevice, st));
+    // bart_step_static: chain c's mailboxes in its slice of the scratch array
+    std::vector<SweepArgs> args_s(args);
+    for (int c = 0; c < nchain; ++c)
+      args_s[c].pub = h->scratch_dev + (int64_t)c * 2 * lay.gcap * kStride;
+    HIP_TRY(hipMemcpyAsync(at<SweepArgs>(h, lay.args_static), args_s.data(),
+                           sizeof(SweepArgs) * nchain, hipMemcpyHostToDevice, st));
     // the host copies of n_cuts must stay valid until the copies ran
     HIP_TRY(hipStreamSynchronize(st));
     return BART_OK;
@@ -636,6 +688,20 @@ int bart_step(bart_handle *h, int32_t k_sweeps, uint64_t seed) {
                                 (long long)h->sweep, h->next);
   const int64_t steps = (int64_t)k_sweeps * (h->cfg.ntree + 1);
   return run_steps(h, steps, seed, nullptr);
+}
+
+int bart_step_static(bart_handle *h, int32_t k_sweeps, uint64_t seed) {
+  if (!h) return fail(BART_EINVAL, "handle is NULL");
+  if (k_sweeps < 0) return fail(BART_EINVAL, "k_sweeps must be >= 0");
+  if (h->next != 0) return fail(BART_ESTATE, "chain is inside sweep %lld (step %d)",
+                                (long long)h->sweep, h->next);
+  const int64_t need = (int64_t)h->nchain * 2 * h->lay.gcap * kStride;
+  if (need > kScratchWords)
+    return fail(BART_ENOTSUP, "the mailboxes need %lld words, the static scratch holds %lld",
+                (long long)need, (long long)kScratchWords);
+  if (!h->scratch_dev) return fail(BART_ESTATE, "no static scratch address for device %d", h->device);
+  const int64_t steps = (int64_t)k_sweeps * (h->cfg.ntree + 1);
+  return run_steps(h, steps, seed, nullptr, true);
 }
 
 int bart_debug_steps(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace) {

@@ -1,0 +1,64 @@
+"""bart_step_static (the entry point that allocates nothing: mailboxes in the
+library's static scratch array) against bart_step, through the C ABI: the
+same sweeps from the same state must give bit-identical chains.  Two calls
+in a row on different handles, the second smaller (fewer observations,
+workgroups and chains), so the second reads a scratch array that still holds
+the first call's words."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from paper_2410_23244_amd.inputs import make_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _pair(inp, **kw):
+    from paper_2410_23244_amd.bart import from_inputs
+
+    return from_inputs(inp, **kw), from_inputs(inp, **kw)
+
+
+def _same(a, b, nchain):
+    for c in range(nchain):
+        sa, sb = a.get_state(c), b.get_state(c)
+        for k in ["axis", "cut", "leaf", "idx", "resid"]:
+            np.testing.assert_array_equal(sa[k], sb[k], err_msg=f"{k} chain {c}")
+        assert sa["sigma2"] == sb["sigma2"] and sa["sweep"] == sb["sweep"]
+
+
+@pytest.mark.parametrize("launch", [0, 1])
+def test_step_static_equals_step_on_two_calls(launch):
+    # first call: 2 chains of 10 workgroups, 40003 observations
+    inp = make_inputs(2, n=40003, p=30, m=40)
+    a, b = _pair(inp, grid=10, nchain=2, launch=launch)
+    print(f"call 1: n={inp.n} grid={a.launch_info().grid} nchain=2", flush=True)
+    a.step(3, 17)
+    b.step_static(3, 17)
+    assert a.status() == 0 and b.status() == 0
+    _same(a, b, 2)
+    # second call, smaller: one chain of 3 workgroups, 5003 observations
+    inp2 = make_inputs(1, n=5003, p=8, m=12)
+    a2, b2 = _pair(inp2, grid=3, launch=launch)
+    print(f"call 2: n={inp2.n} grid={a2.launch_info().grid} nchain=1", flush=True)
+    a2.step(4, 5)
+    b2.step_static(4, 5)
+    assert a2.status() == 0 and b2.status() == 0
+    _same(a2, b2, 1)
+    # and the first handle again after the smaller one, continuing its chains
+    a.step(1, 17)
+    b.step_static(1, 17)
+    assert a.status() == 0 and b.status() == 0
+    _same(a, b, 2)
+
+
+def test_step_static_rejects_mid_sweep():
+    from paper_2410_23244_amd.bart import BART_ESTATE, BartError, from_inputs
+
+    inp = make_inputs(1, n=2001, p=8, m=6)
+    g = from_inputs(inp)
+    g.debug_steps(3, 1)
+    with pytest.raises(BartError) as e:
+        g.step_static(1, 1)
+    assert e.value.code == BART_ESTATE
