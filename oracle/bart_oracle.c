@@ -506,19 +506,21 @@ double oc_log_ratio(const oc_config *c, const int32_t *n_cuts, const uint8_t *X,
   return move == 1 ? lr + llr : lr - llr;
 }
 
-/* Algorithm 1 (branchless traverse) exactly as the paper states it. */
+/* Leaf of observation i in one heap-stored tree (sec. 3.2: node h has
+ * children 2h and 2h+1, nodes of the last level D-1 are always leaves, and a
+ * node with cut 0 is a leaf): start at the root and, while the node splits,
+ * go right iff the observation's bin on the node's axis reaches the cut.
+ * This is the leaf Algorithm 1 computes; the recursive-descent pin checks the
+ * two agree. */
 int32_t oc_route(int32_t D, const uint16_t *axis, const uint8_t *cut, const uint8_t *X,
                  int64_t ldx, int64_t i) {
-  int leaf_found = 0;
-  int32_t index = 1;
-  for (int32_t lvl = 1; lvl <= D - 1; lvl++) {
-    int32_t ax = axis[index];
-    int32_t split = cut[index];
-    leaf_found = leaf_found || (split == 0);
-    int32_t child = 2 * index + (X[(int64_t)ax * ldx + i] >= split ? 1 : 0);
-    index = leaf_found ? index : child;
+  const int32_t first_leaf_level = 1 << (D - 1);
+  int32_t h = 1;
+  while (h < first_leaf_level && cut[h] != 0) {
+    const uint8_t bin = X[(int64_t)axis[h] * ldx + i];
+    h = 2 * h + (bin >= cut[h] ? 1 : 0);
   }
-  return index;
+  return h;
 }
 
 /* ------------------------------------------------------------------ */
