@@ -137,6 +137,10 @@ typedef struct {
   int32_t next;   /* next step of that sweep: 0..ntree-1 trees, ntree = sigma^2 */
   int32_t chain;  /* in [0, nchain) */
   float *latent;  /* probit: [n] latents z_i (NULL: not copied); ignored otherwise */
+  int32_t *count; /* bart_get_state only: per-leaf counts i32 [ntree][2H] the sampler
+                     keeps (slot h, a leaf: observations in it; other slots hold
+                     stale values nothing reads), NULL: not copied; bart_set_state
+                     ignores it and recounts from idx */
 } bart_state;
 
 /* Per-step record written by bart_debug_steps (4224 bytes).  Slots are heap

@@ -47,7 +47,7 @@ class State(C.Structure):
     _fields_ = [("axis", C.c_void_p), ("cut", C.c_void_p), ("leaf", C.c_void_p),
                 ("idx", C.c_void_p), ("resid", C.c_void_p), ("sigma2", C.c_double),
                 ("sweep", C.c_int64), ("next", C.c_int32), ("chain", C.c_int32),
-                ("latent", C.c_void_p)]
+                ("latent", C.c_void_p), ("count", C.c_void_p)]
 
 
 class LaunchInfo(C.Structure):
@@ -339,9 +339,11 @@ class Bart:
                     resid=torch.empty(n, dtype=torch.float32, device=self.device))
         if self.probit:
             bufs["latent"] = torch.empty(n, dtype=torch.float32, device=self.device)
+        bufs["count"] = torch.empty((m, 2 * H), dtype=torch.int32, device=self.device)
         st = State(bufs["axis"].data_ptr(), bufs["cut"].data_ptr(), bufs["leaf"].data_ptr(),
                    bufs["idx"].data_ptr(), bufs["resid"].data_ptr(), 0.0, 0, 0, int(chain),
-                   bufs["latent"].data_ptr() if self.probit else None)
+                   bufs["latent"].data_ptr() if self.probit else None,
+                   bufs["count"].data_ptr())
         bart_get_state(self.h, st)
         out = {k: v.cpu().numpy() for k, v in bufs.items()}
         out["axis"] = out["axis"].view(np.uint16)
@@ -352,7 +354,7 @@ class Bart:
 
     def sigma2(self, chain: int = 0) -> float:
         """Current sigma^2 of a chain (no array copies)."""
-        st = State(None, None, None, None, None, 0.0, 0, 0, int(chain), None)
+        st = State(None, None, None, None, None, 0.0, 0, 0, int(chain), None, None)
         bart_get_state(self.h, st)
         return st.sigma2
 
@@ -368,7 +370,7 @@ class Bart:
         st = State(dev["axis"].data_ptr(), dev["cut"].data_ptr(), dev["leaf"].data_ptr(),
                    dev["idx"].data_ptr(), dev["resid"].data_ptr(), float(s["sigma2"]),
                    int(s["sweep"]), int(s.get("next", 0)), int(chain),
-                   dev["latent"].data_ptr() if self.probit else None)
+                   dev["latent"].data_ptr() if self.probit else None, None)
         bart_set_state(self.h, st)
         self.stream.synchronize()
 

@@ -777,6 +777,9 @@ int bart_get_state(bart_handle *h, bart_state *d) {
   if (d->resid)
     HIP_TRY(hipMemcpyAsync(d->resid, atc<void>(h, ch, L.resid), 4 * (size_t)c.n,
                            hipMemcpyDeviceToDevice, st));
+  if (d->count)
+    HIP_TRY(hipMemcpyAsync(d->count, atc<void>(h, ch, L.count), 4 * m * 2 * H,
+                           hipMemcpyDeviceToDevice, st));
   if (d->latent && c.probit)
     HIP_TRY(hipMemcpyAsync(d->latent, atc<void>(h, ch, L.latent), 4 * (size_t)c.n,
                            hipMemcpyDeviceToDevice, st));

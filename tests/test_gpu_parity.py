@@ -5,6 +5,8 @@ Small cases cover every workload shape (u8 and u16 index caches, depth 6 and
 headline shapes in the launch configuration the benchmark times."""
 from __future__ import annotations
 
+import functools
+
 import numpy as np
 import pytest
 
@@ -16,6 +18,13 @@ pytestmark = pytest.mark.gpu
 
 COOP, ORDINARY = 0, 1  # BART_LAUNCH_COOPERATIVE, BART_LAUNCH_ORDINARY
 AUTO, REGS, STREAM = 0, 1, 2  # BART_RESID_AUTO, BART_RESID_REGISTERS, BART_RESID_STREAMED
+
+
+@functools.lru_cache(maxsize=None)
+def _full(cfg):
+    """A full-size workload, generated once per test session (the large ones
+    take tens of seconds); the tests that use it do not modify it."""
+    return make_inputs(cfg)
 
 
 def _gpu(inp, grid=0, launch=COOP, residency=AUTO, nchain=1):
@@ -139,12 +148,60 @@ def test_launch_modes_agree():
 @pytest.mark.parametrize("cfg", [2, 3, 5])
 def test_lockstep_full_size(cfg):
     """Full size, in the launch mode the benchmark times, after the benchmark's
-    warm-up length (trees near their stationary size)."""
-    inp = make_inputs(cfg)
+    warm-up length (trees near their stationary size): the untraced warm-up
+    leaves a state that meets the cache invariants, then a whole sweep runs
+    in lockstep with the oracle."""
+    inp = _full(cfg)
     print(f"full workload {cfg}: n={inp.n} p={inp.p} m={inp.m}", flush=True)
     g = _gpu(inp, launch=ORDINARY)
-    rep = parity.lockstep(inp, g, seed=inp.seed, warm_sweeps=100, n_steps=inp.m + 1)
+    g.step(100, inp.seed)
+    assert g.status() == 0
+    inv = parity.check_invariants(inp, g.get_state(), sweeps=100)
+    print(f"  invariants after 100 untraced sweeps: {inv}", flush=True)
+    rep = parity.lockstep(inp, g, seed=inp.seed, warm_sweeps=0, n_steps=inp.m + 1)
     print(f"  {rep}", flush=True)
+
+
+# sweeps in lockstep from the initial state (root-only trees, where GROW
+# dominates): every sweep of the tiny workload, ten of workload 2, two of the
+# large ones
+FROM_INIT = {1: 100, 2: 10, 3: 2, 4: 2, 5: 2}
+
+
+@pytest.mark.parametrize("cfg", sorted(FROM_INIT))
+def test_lockstep_from_init(cfg):
+    inp = _full(cfg)
+    k = FROM_INIT[cfg]
+    print(f"workload {cfg} from init: n={inp.n} p={inp.p} m={inp.m}, {k} sweeps", flush=True)
+    g = _gpu(inp, launch=ORDINARY)
+    rep = parity.lockstep(inp, g, seed=inp.seed, warm_sweeps=0, n_steps=k * (inp.m + 1))
+    print(f"  {rep}", flush=True)
+    assert rep.tree_steps == k * inp.m and rep.moves > 0
+
+
+@pytest.mark.parametrize("cfg", [3, 4, 5])
+def test_timed_path_equals_traced_path(cfg):
+    """bart_step (no trace: the call bench.py times) and bart_debug_steps (the
+    call the lockstep tests compare with the oracle) from one state give the
+    same chain bit for bit, at full size in the benchmark's launch mode."""
+    inp = _full(cfg)
+    g = _gpu(inp, launch=ORDINARY)
+    g.step(3, inp.seed)
+    s0 = g.get_state()
+    g.step(2, inp.seed)
+    a = g.get_state()
+    g.set_state(s0)
+    g.debug_steps(2 * (inp.m + 1), inp.seed)
+    b = g.get_state()
+    assert g.status() == 0
+    for key in ["axis", "cut", "leaf", "idx", "resid"]:
+        np.testing.assert_array_equal(a[key], b[key], err_msg=key)
+    # the counts of the leaves (set_state recounted b's from the index cache,
+    # so slots that are no longer leaves differ: nothing reads them)
+    for j in range(inp.m):
+        lv = parity.leaf_slots(a["cut"][j])
+        np.testing.assert_array_equal(a["count"][j][lv], b["count"][j][lv], err_msg=f"count {j}")
+    assert a["sigma2"] == b["sigma2"] and a["sweep"] == b["sweep"] == s0["sweep"] + 2
 
 
 def _full_trees(inp, depth, rng):
@@ -224,11 +281,15 @@ def test_lockstep_exhausted_axes(residency):
 
 def test_lockstep_full_size_streamed():
     """Workload 4 (n = 1e7, u16 index cache): residuals streamed from HBM."""
-    inp = make_inputs(4)
+    inp = _full(4)
     print(f"full workload 4: n={inp.n} p={inp.p} m={inp.m}", flush=True)
     g = _gpu(inp, launch=ORDINARY)
     assert g.launch_info().residency == STREAM
-    rep = parity.lockstep(inp, g, seed=inp.seed, warm_sweeps=20, n_steps=inp.m + 1)
+    g.step(20, inp.seed)
+    assert g.status() == 0
+    inv = parity.check_invariants(inp, g.get_state(), sweeps=20)
+    print(f"  invariants after 20 untraced sweeps: {inv}", flush=True)
+    rep = parity.lockstep(inp, g, seed=inp.seed, warm_sweeps=0, n_steps=inp.m + 1)
     print(f"  {rep}", flush=True)
 
 
