@@ -192,7 +192,10 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c,
  * then sigma^2; sec. 2.2 "The BART MCMC").  The chains must be at a sweep
  * boundary (BART_ESTATE otherwise).  Random draws of chain c, sweep s, tree j
  * are a pure function of (seed, c, s, j): Philox4x64-10 with key (seed,
- * 0x42415254 + c 2^32), so chain 0 draws what a lone chain draws, and two
+ * 0x42415254) and counter (s, j, q, c 2^32 + t), the chain offset in counter
+ * word 3 (q selects the proposal block, the leaf normals or the sigma^2
+ * gamma attempts, t the slot pair or attempt, always below 2^32), so chain 0
+ * draws what a lone chain draws, no two chains share a counter, and two
  * calls of k sweeps equal one call of 2k. */
 int bart_step(bart_handle *h, int32_t k_sweeps, uint64_t seed);
 
@@ -222,6 +225,17 @@ int bart_step_static(bart_handle *h, int32_t k_sweeps, uint64_t seed);
  * for bart_predict. */
 int bart_predict_accumulate(bart_handle *h, const uint8_t *Xt, int64_t xt_stride, int64_t n_t,
                             double offset, double *sum, double *sumsq);
+
+/* Posterior mean and sd of f at n_t points from the sums that
+ * bart_predict_accumulate gathered over n_keep kept sweeps of every chain
+ * (sec. 2.2: the kept samples of the chains approximate the posterior; the
+ * chains are pooled).  Per point, chain c's mean m_c = sum[c] / n_keep and
+ * variance v_c = sumsq[c] / n_keep - m_c^2; mean = the average of the m_c;
+ * sd = sqrt(max(0, average of the v_c + variance of the m_c over the
+ * chains)), the law of total variance.  sum, sumsq: device f64
+ * [nchain][n_t]; mean, sd: device f64 [n_t]. */
+int bart_posterior_summary(bart_handle *h, const double *sum, const double *sumsq, int64_t n_t,
+                           int64_t n_keep, double *mean, double *sd);
 
 /* Sum-of-trees prediction f(x) = offset + sum_j g(x; T_j, M_j) (eq. bartdef),
  * each tree traversed by Algorithm 1, summed in fp64 in tree order and

@@ -84,6 +84,7 @@ def lib():
         L.bart_step_static.argtypes = [vp, C.c_int32, C.c_uint64]
         L.bart_predict.argtypes = [vp, vp, C.c_int64, C.c_int64, C.c_double, vp]
         L.bart_predict_accumulate.argtypes = [vp, vp, C.c_int64, C.c_int64, C.c_double, vp, vp]
+        L.bart_posterior_summary.argtypes = [vp, vp, vp, C.c_int64, C.c_int64, vp, vp]
         L.bart_cutpoints.argtypes = [vp, C.c_int64, C.c_int32, C.c_int64, C.c_int32, C.c_int32,
                                      vp, vp]
         L.bart_bin.argtypes = [vp, C.c_int64, C.c_int32, C.c_int64, vp, vp, C.c_int32, vp,
@@ -100,7 +101,7 @@ def lib():
         L.bart_last_error.restype = C.c_char_p
         for f in ["bart_init", "bart_step", "bart_step_static", "bart_predict", "bart_get_state", "bart_set_state",
                   "bart_debug_steps", "bart_status", "bart_launch_info",
-                  "bart_predict_accumulate", "bart_cutpoints", "bart_bin", "bart_default_hyper",
+                  "bart_predict_accumulate", "bart_posterior_summary", "bart_cutpoints", "bart_bin", "bart_default_hyper",
                   "bart_move_stats"]:
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -144,6 +145,12 @@ def bart_predict_accumulate(h: int, xt_ptr: int, xt_stride: int, n_t: int, offse
                             sum_ptr: int, sumsq_ptr: int) -> None:
     _check(lib().bart_predict_accumulate(h, xt_ptr, int(xt_stride), int(n_t), float(offset),
                                          sum_ptr, sumsq_ptr))
+
+
+def bart_posterior_summary(h: int, sum_ptr: int, sumsq_ptr: int, n_t: int, n_keep: int,
+                           mean_ptr: int, sd_ptr: int) -> None:
+    _check(lib().bart_posterior_summary(h, sum_ptr, sumsq_ptr, int(n_t), int(n_keep), mean_ptr,
+                                        sd_ptr))
 
 
 def bart_cutpoints(X: np.ndarray, K: int, grid: int) -> tuple[np.ndarray, np.ndarray]:
@@ -318,6 +325,15 @@ class Bart:
         bart_predict_accumulate(self.h, Xd.data_ptr(), Xd.shape[1], nt, offset,
                                 acc_sum.data_ptr(), acc_sumsq.data_ptr())
 
+    def posterior_summary(self, acc_sum, acc_sumsq, nt: int, n_keep: int):
+        """Pooled posterior mean and sd (float64 device tensors [nt]) from the
+        accumulators of predict_accumulate over n_keep kept sweeps."""
+        mean = self.torch.empty(nt, dtype=self.torch.float64, device=self.device)
+        sd = self.torch.empty_like(mean)
+        bart_posterior_summary(self.h, acc_sum.data_ptr(), acc_sumsq.data_ptr(), nt, n_keep,
+                               mean.data_ptr(), sd.data_ptr())
+        return mean, sd
+
     def status(self) -> int:
         return bart_status(self.h)
 
@@ -436,10 +452,10 @@ class Regressor:
                 sig[k, c] = g.sigma2(c)
         if g.status():
             raise BartError(BART_EDEVICE, "device error during sampling")
-        mean = (s / n_keep).cpu().numpy()
-        var = (s2 / n_keep).cpu().numpy() - mean ** 2
-        self.chain_mean = mean                       # [nchain][n_test]
-        self.mean = mean.mean(axis=0)                # posterior mean over all chains
-        self.sd = np.sqrt(np.maximum(var.mean(axis=0) + mean.var(axis=0), 0.0))
+        mean, sd = g.posterior_summary(s, s2, nt, n_keep)
+        self.mean = mean.cpu().numpy()               # posterior mean over all chains
+        self.sd = sd.cpu().numpy()
+        self.sums = (s.cpu().numpy(), s2.cpu().numpy())  # [nchain][n_test] each
+        self.n_keep = n_keep
         self.sigma2_trace = sig
         return self

@@ -399,6 +399,29 @@ __global__ void __launch_bounds__(kPredBlock)
   }
 }
 
+// Posterior mean and sd of f at each point from the per-chain sums of f and
+// f^2 over n_keep kept sweeps: chain means m_c and variances v_c = E_c[f^2] -
+// m_c^2, pooled by the law of total variance (mean of the v_c plus the
+// variance of the m_c over the chains); one thread per point, fp64.
+__global__ void k_posterior_summary(const double *sum, const double *sumsq, int64_t nt, int nchain,
+                                    double inv_keep, double *mean, double *sd) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nt;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    double mbar = 0.0;
+    for (int c = 0; c < nchain; ++c) mbar += sum[c * nt + i] * inv_keep;
+    mbar /= nchain;
+    double within = 0.0, between = 0.0;
+    for (int c = 0; c < nchain; ++c) {
+      const double mc = sum[c * nt + i] * inv_keep;
+      within += sumsq[c * nt + i] * inv_keep - mc * mc;
+      between += (mc - mbar) * (mc - mbar);
+    }
+    const double var = (within + between) / nchain;
+    mean[i] = mbar;
+    sd[i] = var > 0.0 ? sqrt(var) : 0.0;
+  }
+}
+
 int grid_for(int64_t work, int block) {
   int64_t g = (work + block - 1) / block;
   return (int)std::max<int64_t>(1, std::min<int64_t>(g, 65536));
@@ -740,6 +763,20 @@ int bart_predict_accumulate(bart_handle *h, const uint8_t *Xt, int64_t xt_stride
       Xt, xt_stride, n_t, h->cfg.p, atc<uint16_t>(h, 0, h->lay.axis),
       atc<uint8_t>(h, 0, h->lay.cut), atc<float>(h, 0, h->lay.leaf), h->cfg.ntree,
       h->cfg.max_depth, h->H, offset, h->lay.chain_bytes, nullptr, sum, sumsq);
+  HIP_TRY(hipGetLastError());
+  return BART_OK;
+}
+
+int bart_posterior_summary(bart_handle *h, const double *sum, const double *sumsq, int64_t n_t,
+                           int64_t n_keep, double *mean, double *sd) {
+  if (!h) return fail(BART_EINVAL, "handle is NULL");
+  if (n_t < 0) return fail(BART_EINVAL, "n_t must be >= 0");
+  if (n_keep < 1) return fail(BART_EINVAL, "n_keep must be >= 1");
+  if (n_t == 0) return BART_OK;
+  if (!sum || !sumsq || !mean || !sd) return fail(BART_EINVAL, "NULL pointer argument");
+  HIP_TRY(hipSetDevice(h->device));
+  k_posterior_summary<<<grid_for(n_t, 256), 256, 0, h->stream>>>(sum, sumsq, n_t, h->nchain,
+                                                                 1.0 / (double)n_keep, mean, sd);
   HIP_TRY(hipGetLastError());
   return BART_OK;
 }

@@ -62,7 +62,8 @@ def test_device_rmse_on_the_paper_dgp():
     assert 0.8 < math.sqrt(r.sigma2_trace[-50:].mean()) < 1.2
     # the chains agree with each other to well within the signal sd (their
     # posterior means carry Monte Carlo error of the order of rmse_f)
-    assert math.sqrt(np.mean((r.chain_mean[0] - r.chain_mean[1]) ** 2)) < 0.4
+    chain_mean = r.sums[0] / r.n_keep
+    assert math.sqrt(np.mean((chain_mean[0] - chain_mean[1]) ** 2)) < 0.4
     # posterior sd of f: positive, below the prior scale
     assert (r.sd > 0).all() and np.median(r.sd) < 0.6
     # the oracle on the same data lands at the same accuracy
@@ -113,4 +114,11 @@ def test_predict_accumulate_sums_the_kept_sweeps():
     tol = 5 * 6e-8 * np.abs(want).max()
     assert np.abs(got - want).max() <= tol
     assert np.abs(got2 - want2).max() <= 2 * tol * np.abs(want).max()
+    # pooled posterior mean and sd over the 3 chains (law of total variance)
+    mean, sd = g.posterior_summary(s, s2, nt, 5)
+    m_c = got / 5
+    v_c = got2 / 5 - m_c ** 2
+    np.testing.assert_allclose(mean.cpu().numpy(), m_c.mean(axis=0), rtol=1e-12, atol=1e-12)
+    want_sd = np.sqrt(np.maximum(v_c.mean(axis=0) + m_c.var(axis=0), 0.0))
+    np.testing.assert_allclose(sd.cpu().numpy(), want_sd, rtol=1e-9, atol=1e-9)
     assert g.status() == 0
