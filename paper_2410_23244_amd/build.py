@@ -19,18 +19,25 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False, extra: list[str] | None = None) -> str:
+CLOCKS_LIB = os.path.join(HERE, "libbart_clocks.so")
+
+
+def build(verbose: bool = False, extra: list[str] | None = None, clocks: bool = False) -> str:
+    """libbart.so; with clocks=True the diagnostic variant libbart_clocks.so
+    (phase clocks of the register sweep kernel, see phase_budget.py)."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB + ".tmp"
-    cmd = [hipcc, *FLAGS, *(extra or []), SRC, "-o", tmp]
+    out = CLOCKS_LIB if clocks else LIB
+    tmp = out + ".tmp"
+    cmd = [hipcc, *FLAGS, *(["-DBART_PHASE_CLOCKS"] if clocks else []), *(extra or []), SRC,
+           "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("hipcc failed to build libbart.so")
-    os.replace(tmp, LIB)
-    return LIB
+        raise RuntimeError(f"hipcc failed to build {os.path.basename(out)}")
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

@@ -928,6 +928,20 @@ int bart_launch_info(const bart_handle *h, bart_launch *o) {
 
 void bart_destroy(bart_handle *h) { delete h; }
 
+#ifdef BART_PHASE_CLOCKS
+// Diagnostic build only: the phase clocks of the last launch of the register
+// kernel, u64 [kMaxGrid][kClockSteps][kClockPh] (see sweep.hpp), into host
+// memory of `words` u64; synchronises the device.
+int bart_phase_clocks(uint64_t *host, size_t words) {
+  if (!host || words < (size_t)kMaxGrid * kClockSteps * kClockPh)
+    return fail(BART_EINVAL, "need %zu words", (size_t)kMaxGrid * kClockSteps * kClockPh);
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpyFromSymbol(host, HIP_SYMBOL(g_phase_clock),
+                              sizeof(uint64_t) * kMaxGrid * kClockSteps * kClockPh));
+  return BART_OK;
+}
+#endif
+
 }  // extern "C"
 
 // host-side input preparation (bart_cutpoints, bart_bin, bart_default_hyper)

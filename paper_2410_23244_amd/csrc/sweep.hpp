@@ -40,6 +40,32 @@
 namespace bart {
 
 constexpr uint32_t kSpinLimit = 1u << 21;
+
+// Phase clocks (diagnostic build, -DBART_PHASE_CLOCKS, read by
+// bart_phase_clocks): thread 0 of every workgroup of the register kernel
+// stamps the wall clock (100 MHz) at the phase boundaries of the tree steps
+// kClockStart .. kClockStart + kClockSteps - 1 of a launch, and every
+// workgroup counts the mailbox loads its polls issue in each of them.  The
+// ordinary build compiles none of it.
+constexpr int kClockStart = 205, kClockSteps = 64, kClockPh = 10;
+#ifdef BART_PHASE_CLOCKS
+__device__ uint64_t g_phase_clock[kMaxGrid][kClockSteps][kClockPh];
+__shared__ uint64_t clk_lds[kClockSteps][kClockPh];
+__device__ __forceinline__ int clock_slot(int step) {
+  return step >= kClockStart && step < kClockStart + kClockSteps ? step - kClockStart : -1;
+}
+#define BART_CLOCK(slot, ph)                                                              \
+  do {                                                                                    \
+    if (threadIdx.x == 0 && (slot) >= 0) clk_lds[slot][ph] = wall_clock64();              \
+  } while (0)
+#define BART_POLL_COUNT(n) (poll_loads += (n))
+#else
+__device__ __forceinline__ constexpr int clock_slot(int) { return -1; }
+#define BART_CLOCK(slot, ph) \
+  do {                       \
+  } while (0)
+#define BART_POLL_COUNT(n) ((void)0)
+#endif
 constexpr int kNullRank = kMaxLeaves;  // rank of a padding point (slot 0): no bin, zero delta
 constexpr int kBadRank = 255;          // rank of any other non-leaf slot: likewise, and flagged
 constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
@@ -368,8 +394,11 @@ __device__ __forceinline__ void post(const SweepArgs *__restrict__ A, SH &sh, in
 // order.  Returns nseg.  Ends with an LDS barrier.
 template <class SH>
 __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH &sh, int par,
-                                            uint32_t seq, int K, int nsum) {
+                                            uint32_t seq, int K, int nsum, int clk = -1) {
   const int t = threadIdx.x, G = A->G;
+#ifdef BART_PHASE_CLOCKS
+  uint32_t poll_loads = 0;
+#endif
   if (G == 1) {
     lds_barrier();  // the words were staged by the waves that formed them
     if (t < K) {
@@ -397,6 +426,7 @@ __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH 
       uint32_t spins = 0;
       const uint64_t *pb = base + (int64_t)gb * kStride;
       while (pending) {
+        BART_POLL_COUNT(__popc(pending));
 #pragma unroll
         for (int u = 0; u < 8; ++u)
           if ((pending >> u) & 1u) wv[u] = ld_dev(pb + u * kStride);
@@ -418,6 +448,10 @@ __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH 
     }
     sh.part[t] = acc;
   }
+#ifdef BART_PHASE_CLOCKS
+  if (clk >= 0 && poll_loads) atomicAdd((unsigned long long *)&clk_lds[clk][kClockPh - 1],
+                                        (unsigned long long)poll_loads);
+#endif
   lds_barrier();
   return nseg;
 }
@@ -999,7 +1033,10 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       // 1. route tree j+1 (its rows were loaded a step ago); this
       //    workgroup's partial sums of tree j and its GROW right-count were
       //    posted by the reduce that formed them
+      const int clk = clock_slot(step);
+      BART_CLOCK(clk, 0);
       if (more1) route(j + 1, rk2);
+      BART_CLOCK(clk, 1);
       // 2. while the mailboxes fill: load rows of j+2, the decision data of
       //    j+1 and the proposal of j+3
       // (the small loads first: nothing waits behind the row loads)
@@ -1018,12 +1055,16 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
 #pragma unroll
         for (int i = 0; i < 4; ++i) build_rank_slot(A, sh.ctx[(j + 2) & (kRing - 1)], 64 * i + lane);
       pre_decide(A, sh, c, sh.td[j & 1], w == 0 ? uncounted : -1);
-      const int nseg = gather_polls(A, sh, par, seq, K, L);
+      BART_CLOCK(clk, 2);
+      const int nseg = gather_polls(A, sh, par, seq, K, L, clk);
+      BART_CLOCK(clk, 3);
       decide_step(A, sh, c, sh.td[j & 1], nseg);
+      BART_CLOCK(clk, 4);
       // stage what later trees need
       if (more3 && t < kPropWords) ((uint32_t *)&sh.ctx[(j + 3) & (kRing - 1)].pr)[t] = pw3;
       if (more1) store_tree_data(sh.td[(j + 1) & 1], sh.ctx[(j + 1) & (kRing - 1)], tdn);
       lds_barrier();
+      BART_CLOCK(clk, 5);
       wait_vm_loads();  // the rows of j+2 are in before this step's stores
       // 4. residuals and index row (item 11): the delta of every rank is
       //    final (a point in a child of eta of a merged move takes the
@@ -1056,8 +1097,10 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
           if (touch) row[(w * V + v) * kBlock + t] = out;
         }
       }
+      BART_CLOCK(clk, 6);
       finish_tree(A, Lc, sh, c, j, s, step);
       uncounted = j;
+      BART_CLOCK(clk, 7);
       // 5. tree j+1: partial sums from the updated residuals
       if (more1) {
         reduce(j + 1, rk2, (step + 1) & 1, (uint32_t)step + 3);
@@ -1066,6 +1109,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       } else {
         lds_barrier();
       }
+      BART_CLOCK(clk, 8);
       ++j;
     } else {
       // ================= sigma^2 step (sec. 3.3, "Sampling the error variance")
@@ -1117,9 +1161,19 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
 template <int V, int IB>
 __global__ void __launch_bounds__(kBlock) sweep_kernel(const SweepArgs *__restrict__ A, Launch Lc) {
   __shared__ Shared sh;
+#ifdef BART_PHASE_CLOCKS
+  for (int q = threadIdx.x; q < kClockSteps * kClockPh; q += kBlock)
+    clk_lds[q / kClockPh][q % kClockPh] = 0;
+  __syncthreads();
+#endif
   const int c = (int)blockIdx.x / A->G;
   if (Lc.trace) Lc.trace += c * Lc.trace_stride;
   sweep_body<V, IB>(A + c, Lc, sh);
+#ifdef BART_PHASE_CLOCKS
+  __syncthreads();
+  for (int q = threadIdx.x; q < kClockSteps * kClockPh; q += kBlock)
+    g_phase_clock[blockIdx.x][q / kClockPh][q % kClockPh] = clk_lds[q / kClockPh][q % kClockPh];
+#endif
 }
 
 // ------------------------------------------------------------------ streamed
