@@ -199,7 +199,7 @@ struct Shared {
   // value is S la + lb and S = R + lnm; the merged leaf likewise (ma, mb);
   // for a PRUNE, the count-only parts of the likelihood ratio
   double la[kMaxLeaves], lb[kMaxLeaves], lnm[kMaxLeaves];
-  double ma, mb, pdet, pdL, pdR, pdP, gs2eP;
+  double ma, mb, pdet, pdL, pdR, pdP, gs2eP, lgs2eP;
   uint64_t stats[6];  // workgroup 0: move statistics of this launch
   int nr[2];  // GROW right-counts of the trees being routed, by tree parity
   int flags;  // bit0 accept, bit1 merged
@@ -587,8 +587,30 @@ __device__ __forceinline__ void pre_decide(const SweepArgs *__restrict__ A, Shar
     const double eP = s2 + (double)td.eta_cnt * v2;
     sh.pdP = 1.0 / eP;
     sh.gs2eP = s2 * eP;
+    sh.lgs2eP = log(s2 * eP);
   }
 }
+
+// 1/x from the hardware reciprocal and two Newton steps (within an ulp or two
+// of the division; used where the sums have just arrived, on the critical
+// path of the tree step).
+__device__ __forceinline__ double rcp_fast(double x) {
+  double r = __builtin_amdgcn_rcp(x);
+  r = fma(fma(-x, r, 1.0), r, r);
+  return fma(fma(-x, r, 1.0), r, r);
+}
+
+// ln x for a positive normal x to about 3e-7 absolute: the exponent exactly,
+// the logarithm of the mantissa m in [0.5, 1) in fp32.
+__device__ __forceinline__ double log_fast(double x) {
+  const int e = __builtin_amdgcn_frexp_exp(x);
+  const double m = __builtin_amdgcn_frexp_mant(x);
+  return (double)e * 0.69314718055994530942 + (double)__logf((float)m);
+}
+// The accept decisions use log_fast only where it cannot change them: when
+// ln u lies within this margin (times 1 + |ln x|) of the fast log r, the
+// full fp64 logarithm decides, so every decision is the one fp64 takes.
+constexpr double kLogFastMargin = 1e-5;
 
 // Tree j's decision once the sums are in (sec. 3.3 items 8-10): wave 0 the
 // MH ratio and accept, waves 1-2 the draws of the two move leaves (each
@@ -612,9 +634,11 @@ __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Sha
   // conditional draw of a GROW child, whose count n comes with the sums:
   // with e = s2 + n v2, prec = e / (s2 v2), the mean is (S v2 + mu_mu s2) / e
   // and the sd sqrt(s2 v2 / e)
+  // (the sd in fp32: its relative error, ~6e-8, is far below the leaf
+  // tolerance)
   auto draw_child = [&](double e, double Sf, double z) {
-    const double ie = 1.0 / e;
-    return (float)((Sf * v2 + A->mu_mu * s2) * ie + z * sqrt(s2 * v2 * ie));
+    const double ie = rcp_fast(e);
+    return (float)((Sf * v2 + A->mu_mu * s2) * ie + z * (double)sqrtf((float)(s2 * v2 * ie)));
   };
   if (move != kNone && wave < 4) {
     // everything this part reads from LDS besides the sums, read up front
@@ -626,6 +650,7 @@ __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Sha
     const double zl = td.z[kl], zr = td.z[kr];
     const double ma = sh.ma, mb = sh.mb, pdP = sh.pdP;
     const double pdet = sh.pdet, pdL = sh.pdL, pdR = sh.pdR, gs2eP = sh.gs2eP;
+    const double lgs2eP = sh.lgs2eP;
     const double c_prior = c.pr.c_prior, ln_u = c.pr.ln_u;
     double nR = move == kGrow ? seg_part(L) : 0.0, Rl = seg_part(kl), Rr = seg_part(kr);
     wave_totals3(nR, Rl, Rr);
@@ -644,17 +669,20 @@ __device__ __forceinline__ void decide_step(const SweepArgs *__restrict__ A, Sha
       // s2 I + v2 1 1^T), so LLR = 1/2 ln(s2 eP / (eL eR)) + v2 / (2 s2)
       // (tL^2/eL + tR^2/eR - tP^2/eP) with e = s2 + n v2 and t = S - n mu_mu,
       // the count-only parts from pre_decide -- plus the count-free terms
+      // (GROW: ln(s2 eP) from pre_decide minus a fast ln(eL eR), redone in
+      // full fp64 when ln u falls within kLogFastMargin of the result)
       auto log_r = [&]() {
-        double llr;
         if (grow) {
           const double eL = s2 + nl * v2, eR = s2 + nr * v2;
-          const double r = 1.0 / (eL * eR);
-          llr = 0.5 * log(gs2eP * r) +
-                v2 / (2.0 * s2) * (tL * tL * (eR * r) + tR * tR * (eL * r) - tP * tP * pdP);
-        } else {
-          llr = pdet + v2 / (2.0 * s2) * (tL * tL * pdL + tR * tR * pdR - tP * tP * pdP);
+          const double p = eL * eR, r = rcp_fast(p);
+          const double q = v2 / (2.0 * s2) * (tL * tL * (eR * r) + tR * tR * (eL * r) - tP * tP * pdP);
+          const double lp = log_fast(p);
+          const double fast = c_prior + (0.5 * (lgs2eP - lp) + q);
+          if (fabs(ln_u - fast) > kLogFastMargin * (1.0 + fabs(lp))) return fast;
+          return c_prior + (0.5 * log(gs2eP * r) + q);
         }
-        return c_prior + (grow ? llr : -llr);
+        const double llr = pdet + v2 / (2.0 * s2) * (tL * tL * pdL + tR * tR * pdR - tP * tP * pdP);
+        return c_prior - llr;
       };
       const float vm = (float)((Sl + Sr) * ma + mb);
       if (wave == 0) {
