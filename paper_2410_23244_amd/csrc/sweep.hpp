@@ -47,7 +47,7 @@ constexpr uint32_t kSpinLimit = 1u << 21;
 // kClockStart .. kClockStart + kClockSteps - 1 of a launch, and every
 // workgroup counts the mailbox loads its polls issue in each of them.  The
 // ordinary build compiles none of it.
-constexpr int kClockStart = 205, kClockSteps = 64, kClockPh = 10;
+constexpr int kClockStart = 205, kClockSteps = 64, kClockPh = 13;
 #ifdef BART_PHASE_CLOCKS
 __device__ uint64_t g_phase_clock[kMaxGrid][kClockSteps][kClockPh];
 __shared__ uint64_t clk_lds[kClockSteps][kClockPh];
@@ -896,6 +896,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     sh.ctx[q / (256 - kNullRank)].heap_of[kNullRank + q % (256 - kNullRank)] = 0;
   if (t < 6) sh.stats[t] = 0;
   int uncounted = -1;  // tree step whose move statistics workgroup 0 has yet to count
+  int clk = -1;        // phase-clock slot of the current step (diagnostic build)
 
   // ---- helpers over the pipeline ----
   // issue the index-row and predictor-row loads of tree `tree` (its proposal in ctx)
@@ -960,48 +961,72 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     if (lane == 0 && nr) atomicAdd(&sh.nr[tree & 1], nr);
   };
   // partial sums of tree `tree` from the current residuals: per-lane private
-  // LDS bins for up to kBinRanks ranks at a time (a plain read-modify-write:
-  // LDS float atomics are many times slower; ranks outside the pass, the
-  // null rank of padding points among them, add 0 to a bin of the pass, so
-  // there is no branch per point),
-  // then a fixed-order fp64 reduction; larger trees take several passes.
-  // The wave that forms the total of rank k posts it as word k of this
-  // workgroup's mailbox for the step that decides the tree (buffer par,
-  // step number seq), and after the first bin barrier thread kBlock-1 posts
-  // the GROW right-count that route(tree) gathered as word L: no barrier
-  // stands between the totals and the post (only between passes).
+  // LDS bins, two sets per lane (the points of chunk positions 0, 2 go to
+  // set 0, those of 1, 3 to set 1), so each lane runs two independent chains
+  // of read-modify-writes, for up to kRegRanks ranks at a time (a plain
+  // read-modify-write: LDS float atomics are many times slower; ranks outside
+  // the pass, the null rank of padding points among them, add 0 to a bin of
+  // the pass, so there is no branch per point); then a fixed-order fp64
+  // reduction of the 16 bins of each lane position and a DPP tree over the
+  // lanes; larger trees take several passes.  The wave that forms the total
+  // of rank k posts it as word k of this workgroup's mailbox for the step
+  // that decides the tree (buffer par, step number seq), and after the first
+  // bin barrier thread kBlock-1 posts the GROW right-count that route(tree)
+  // gathered as word L: no barrier stands between the totals and the post
+  // (only between passes).
+  constexpr int kSets = 2;
+  constexpr int kRegRanks = kBinFloats / (kSets * kBlock);  // 32
+  static_assert(kMaxLeaves % kRegRanks == 0 && kNullRank / kRegRanks >= kMaxLeaves / kRegRanks,
+                "the null rank must fall outside every bin pass");
   auto reduce = [&](int tree, const uint32_t (&rks)[V], int par, uint32_t seq) {
     const int L = sh.ctx[tree & (kRing - 1)].pr.L;
     const int wl = wave * 64 + lane;
-    for (int base = 0; base < L; base += kBinRanks) {
-      // the bin of rank k is k mod kBinRanks; a point outside the pass adds
-      // 0 to its bin there (exact: a bin never holds -0)
+    for (int base = 0; base < L; base += kRegRanks) {
+      // the bin of rank k is k mod kRegRanks; a point outside the pass adds
+      // 0 to its bin there (exact: a bin never holds -0).  Bins of different
+      // sets never share an address, so a pair (one point of each set) is
+      // read together and written together
 #pragma unroll
       for (int v = 0; v < V; ++v)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const uint32_t rb = (rks[v] >> (8 * b)) & 0xffu;
-          const bool in = rb / kBinRanks == (uint32_t)(base / kBinRanks);
-          sh.bins[(int)(rb % kBinRanks) * (kWaves * 64) + wl] += in ? r[v][b] : 0.f;
+        for (int b = 0; b < 4; b += 2) {
+          const uint32_t ra = (rks[v] >> (8 * b)) & 0xffu, rb = (rks[v] >> (8 * b + 8)) & 0xffu;
+          const uint32_t pass = (uint32_t)(base / kRegRanks);
+          const int qa = ((int)(ra % kRegRanks) * kSets + 0) * kBlock + wl;
+          const int qb = ((int)(rb % kRegRanks) * kSets + 1) * kBlock + wl;
+          const float xa = ra / kRegRanks == pass ? r[v][b] : 0.f;
+          const float xb = rb / kRegRanks == pass ? r[v][b + 1] : 0.f;
+          const float ca = sh.bins[qa], cb = sh.bins[qb];
+          sh.bins[qa] = ca + xa;
+          sh.bins[qb] = cb + xb;
         }
+      if (base == 0) BART_CLOCK(clk, 9);
       lds_barrier();
+      if (base == 0) BART_CLOCK(clk, 10);
       if (base == 0 && t == kBlock - 1) {
         // cleared for route(tree + 2), the next to count into this slot
         post(A, sh, par, L, mk_word(seq, (uint64_t)sh.nr[tree & 1]));
         sh.nr[tree & 1] = 0;
       }
-      for (int k = base + wave; k < min(L, base + kBinRanks); k += kWaves) {
-        double acc = 0.0;
+      for (int k = base + wave; k < min(L, base + kRegRanks); k += kWaves) {
+        // the 16 bins of this lane position (2 sets x 8 waves): all read,
+        // then cleared, then summed in a fixed tree
+        double x[kSets * kWaves];
 #pragma unroll
-        for (int u = 0; u < kWaves; ++u) {
-          const int q = (((k - base) * kWaves + u) << 6) | lane;
-          acc += (double)sh.bins[q];
-          sh.bins[q] = 0.f;
-        }
-        const double tot = wave_total63(acc);
+        for (int q = 0; q < kSets * kWaves; ++q)
+          x[q] = (double)sh.bins[(((k - base) * kSets + q / kWaves) * kWaves + q % kWaves) * 64 + lane];
+#pragma unroll
+        for (int q = 0; q < kSets * kWaves; ++q)
+          sh.bins[(((k - base) * kSets + q / kWaves) * kWaves + q % kWaves) * 64 + lane] = 0.f;
+#pragma unroll
+        for (int w2 = 1; w2 < kSets * kWaves; w2 *= 2)
+#pragma unroll
+          for (int q = 0; q < kSets * kWaves; q += 2 * w2) x[q] += x[q + w2];
+        const double tot = wave_total63(x[0]);
         if (lane == 63) post(A, sh, par, k, mk_word(seq, pack_f64(tot)));
+        if (k == 0) BART_CLOCK(clk, 11);
       }
-      if (base + kBinRanks < L) lds_barrier();
+      if (base + kRegRanks < L) lds_barrier();
     }
   };
   // proposals of trees j0.. j0+2 into the ring, rank tables, rows of j0,
@@ -1061,7 +1086,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       // 1. route tree j+1 (its rows were loaded a step ago); this
       //    workgroup's partial sums of tree j and its GROW right-count were
       //    posted by the reduce that formed them
-      const int clk = clock_slot(step);
+      clk = clock_slot(step);
       BART_CLOCK(clk, 0);
       if (more1) route(j + 1, rk2);
       BART_CLOCK(clk, 1);
@@ -1141,6 +1166,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       ++j;
     } else {
       // ================= sigma^2 step (sec. 3.3, "Sampling the error variance")
+      clk = -1;
       if (w == 0 && t == kBlock - 1 && uncounted >= 0)
         count_move(sh, sh.ctx[uncounted & (kRing - 1)]);
       uncounted = -1;

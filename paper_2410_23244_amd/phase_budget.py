@@ -12,7 +12,9 @@ counts the mailbox loads its polls issue.  Phases of a tree step j:
   barrier    until every wave has its part of the decision
   update     residual update and index-row rewrite
   finish     the owner's write of tree j
-  reduce     partial sums of tree j+1 and their post
+  reduce     partial sums of tree j+1 and their post (split into the bin
+             updates, the bin barrier, rank 0's cross-wave total and post,
+             and the rest)
 The script prints medians over workgroups and steps, the step period, the
 spread of the posts and the time from the last post to the first and last
 completed gathers, and the mailbox loads per step against G^2 (L + 1).
@@ -33,9 +35,11 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, os.path.dirname(HERE))
 
-K_GRID, K_STEPS, K_PH = 256, 64, 10  # kMaxGrid, kClockSteps, kClockPh
+K_GRID, K_STEPS, K_PH = 256, 64, 13  # kMaxGrid, kClockSteps, kClockPh
 K_START = 205                        # kClockStart
 PHASES = ["route", "prefetch", "gather", "decide", "barrier", "update", "finish", "reduce"]
+# stamps 9-11 (inside the reduce: bins done, bin barrier passed, rank 0 posted)
+SUB = ["bins", "bin barrier", "rank-0 total and post", "rest of reduce"]
 
 
 def run(config: int, warmup: int, seed: int, out: str | None) -> dict:
@@ -69,13 +73,16 @@ def run(config: int, warmup: int, seed: int, out: str | None) -> dict:
         np.save(out, ts)
     loads = ts[:, :, K_PH - 1]
     clk = ts[:, :, : K_PH - 1] * 10  # ns
+    sub = clk[:, :, [7, 9, 10, 11, 8]]  # finish, bins, barrier, rank-0 post, end
     ok = (clk[:, :, 0] > 0).all(0) & (clk[:, :, 8] > 0).all(0)  # tree steps (not sigma^2)
-    clk, loads = clk[:, ok], loads[:, ok]
-    d = np.diff(clk, axis=2)
+    clk, loads, sub = clk[:, ok], loads[:, ok], sub[:, ok]
+    d = np.diff(clk[:, :, :9], axis=2)
+    ds = np.diff(sub, axis=2)
     res = {"config": config, "workload": inp.workload, "grid": G, "tree_steps": int(ok.sum()),
            "first_step": K_START,
            "phase_median_ns": {p: float(np.median(d[:, :, k])) for k, p in enumerate(PHASES)},
-           "phase_p90_ns": {p: float(np.percentile(d[:, :, k], 90)) for k, p in enumerate(PHASES)}}
+           "phase_p90_ns": {p: float(np.percentile(d[:, :, k], 90)) for k, p in enumerate(PHASES)},
+           "reduce_parts_median_ns": {p: float(np.median(ds[:, :, k])) for k, p in enumerate(SUB)}}
     post, gd = clk[:, :, 8], clk[:, :, 3]
     res["step_period_median_ns"] = float(np.median(np.diff(clk[0, :, 0])))
     res["post_spread_median_ns"] = float(np.median(post.max(0) - post.min(0)))
