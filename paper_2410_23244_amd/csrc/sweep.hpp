@@ -254,8 +254,13 @@ __device__ __forceinline__ void build_ranks(const SweepArgs *__restrict__ A, Ctx
   if (threadIdx.x < 256) build_rank_slot(A, c, (int)threadIdx.x);
 }
 
+// Thread that loads and stages the decision data of the move's node eta: in
+// wave 3, which neither polls nor holds a rank (ranks are below kMaxLeaves).
+constexpr int kEtaThread = 255;
+static_assert(kEtaThread >= kMaxLeaves && kEtaThread < 256, "eta thread");
+
 // Per-thread registers of one tree's decision data in flight (thread t holds
-// rank t; thread kBlock-1 the node eta).
+// rank t; thread kEtaThread the node eta).
 struct TdRegs {
   int32_t cnt;
   float mu;
@@ -268,7 +273,7 @@ __device__ __forceinline__ TdRegs load_tree_data(const SweepArgs *__restrict__ A
   // every thread loads (slot 1 when it has no rank), see load_prop_word
   int h = 1;
   if (t < c.pr.L) h = c.heap_of[t];
-  if (t == kBlock - 1 && c.pr.move != kNone) h = c.pr.eta;
+  if (t == kEtaThread && c.pr.move != kNone) h = c.pr.eta;
   const int64_t o = (int64_t)j * 2 * H + h;
   TdRegs r;
   r.cnt = gbl((const int32_t *)A->count)[o];
@@ -284,7 +289,7 @@ __device__ __forceinline__ void store_tree_data(TreeData &td, const Ctx &c, cons
     td.mu[t] = r.mu;
     td.z[t] = r.z;
   }
-  if (t == kBlock - 1) {
+  if (t == kEtaThread) {
     td.eta_cnt = r.cnt;
     td.eta_mu = r.mu;
     td.eta_z = r.z;
@@ -391,15 +396,20 @@ __device__ __forceinline__ void post(const SweepArgs *__restrict__ A, SH &sh, in
 // order in fp64 into sh.part[seg * K + k] (words k < nsum are fp64 values,
 // the others counts), with all loads of a batch in flight at once.  The
 // partition depends only on G and K, so every workgroup sums in the same
-// order.  Returns nseg.  Ends with an LDS barrier.
+// order.  The polling threads are the last ceil(nseg K / 64) waves of the
+// workgroup (polling thread i is thread kBlock - 64 ceil(nseg K / 64) + i):
+// the waves that build no rank table and compute no constants before the
+// gather, so they start polling soonest.  Returns nseg.  Ends with an LDS
+// barrier.
 template <class SH>
 __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH &sh, int par,
                                             uint32_t seq, int K, int nsum, int clk = -1) {
-  const int t = threadIdx.x, G = A->G;
+  const int G = A->G;
 #ifdef BART_PHASE_CLOCKS
   uint32_t poll_loads = 0;
 #endif
   if (G == 1) {
+    const int t = threadIdx.x;
     lds_barrier();  // the words were staged by the waves that formed them
     if (t < K) {
       const uint64_t wv = sh.solo[t];
@@ -414,7 +424,9 @@ __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH 
   while (K * ((G + 8 * nb - 1) / (8 * nb)) > kBlock) ++nb;
   const int span = 8 * nb;
   const int nseg = (G + span - 1) / span;  // nseg * K <= kBlock
-  if (t < nseg * K) {
+  const int first = kBlock - (nseg * K + 63) / 64 * 64;  // first polling thread
+  const int t = (int)threadIdx.x - first;
+  if (t >= 0 && t < nseg * K) {
     const int k = t % K, seg = t / K;
     const int g0 = seg * span, g1 = min(G, g0 + span);
     const uint64_t *base = A->pub + (int64_t)par * A->G * kStride + k;
@@ -541,14 +553,18 @@ __device__ __forceinline__ void count_move(Shared &sh, const Ctx &c) {
 // 5, 9, 10): for every leaf of known count (all but the children of a GROW)
 // prec = n / s2 + 1 / v2 and the draw mean + z / sqrt(prec) written as
 // S la + lb; the merged leaf of eta; for a PRUNE, the determinant term and
-// the denominators of the likelihood ratio.  Waves 4..7, before the gather.
+// the denominators of the likelihood ratio.  Before the gather, on wave 1
+// when the tree is small (L + 5 <= 64 threads), else on waves 0-3: the
+// polls run on the last waves.  The previous tree step's move statistics
+// (its flags are still in sh.flags) are counted by thread 128 of workgroup 0.
 __device__ __forceinline__ void pre_decide(const SweepArgs *__restrict__ A, Shared &sh,
                                            const Ctx &c, const TreeData &td, int uncounted) {
-  const int u = (int)threadIdx.x - 4 * 64;
-  if (u < 0) return;
-  // the previous tree step's statistics (its flags are still in sh.flags)
-  if (uncounted >= 0 && threadIdx.x == kBlock - 1) count_move(sh, sh.ctx[uncounted & (kRing - 1)]);
-  const int move = c.pr.move, eta = c.pr.eta, L = c.pr.L;
+  const int L = c.pr.L;
+  const int u0 = L + 5 <= 64 ? 64 : 0, nthreads = L + 5 <= 64 ? 64 : 256;
+  if (uncounted >= 0 && threadIdx.x == 128) count_move(sh, sh.ctx[uncounted & (kRing - 1)]);
+  const int u = (int)threadIdx.x - u0;
+  if (u < 0 || u >= nthreads) return;
+  const int move = c.pr.move, eta = c.pr.eta;
   const int kl = c.pr.rank_l, kr = c.pr.rank_r;
   const double s2 = sh.sigma2, v2 = A->sigma_mu * A->sigma_mu;
   // prec = n / s2 + 1 / v2 = e / (s2 v2) with e = s2 + n v2, so the draw
@@ -1099,10 +1115,11 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       if (more2) issue_rows(j + 2);
       // 3. totals of tree j, in the same order in every workgroup: polls into
       //    per-segment partials, then one wave reduces a word over the
-      //    segments with the fixed-order DPP tree (nseg <= 32 lanes).  Before
-      //    that, wave 3 builds the rank table of tree j+2 (its proposal was
-      //    staged a step ago; 4 slots per lane, off the polling waves 0-2)
-      //    while waves 4-7 compute tree j's count-only constants
+      //    segments with the fixed-order DPP tree (nseg <= 32 lanes).  The
+      //    polls run on the last waves; before the gather, wave 3 builds the
+      //    rank table of tree j+2 (its proposal was staged a step ago; 4
+      //    slots per lane) and wave 1 (waves 0-3 for large trees) computes
+      //    tree j's count-only constants
       const int K = L + 1;
       if (more2 && wave == 3)
 #pragma unroll
