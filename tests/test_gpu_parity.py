@@ -312,6 +312,30 @@ def test_chains_lockstep(nchain, grid, residency, launch):
     assert not np.array_equal(states[0]["leaf"], states[1]["leaf"])
 
 
+@pytest.mark.parametrize("nchain,chunks", [(2, 4), (4, 8)])
+def test_chains_full_size_lockstep(nchain, chunks):
+    """Workload 3 at full size with 2 and 4 chains in the ordinary launch: the
+    4-chain shape is the one bench.py's batched leg times (62 workgroups per
+    chain, 8 chunks of 4 points per thread), the 2-chain one takes 4 chunks.
+    After untraced sweeps every chain's state meets the cache invariants, then
+    every chain runs a whole sweep in lockstep with its oracle stream."""
+    inp = _full(3)
+    g = _gpu(inp, launch=ORDINARY, nchain=nchain)
+    info = g.launch_info()
+    print(f"workload 3, {nchain} chains: grid {info.grid} x {nchain}, {info.chunks_per_thread} "
+          f"chunks per thread", flush=True)
+    assert info.nchain == nchain and info.chunks_per_thread == chunks
+    g.step(10, inp.seed)
+    assert g.status() == 0
+    for c in range(nchain):
+        inv = parity.check_invariants(inp, g.get_state(c), sweeps=10, n_sample=64, seed=c)
+        print(f"  chain {c} invariants: {inv}", flush=True)
+    reps = parity.lockstep_chains(inp, g, seed=inp.seed, warm_sweeps=0, n_steps=inp.m + 1)
+    for rep in reps:
+        print(f"  {rep}", flush=True)
+        assert rep.tree_steps == inp.m and rep.moves > 0
+
+
 def test_chains_of_one_workgroup_lockstep():
     """Small n: every chain is one workgroup, whose mailbox words stay in LDS;
     six chains in lockstep with their oracle streams (ragged n: a partial
