@@ -940,6 +940,14 @@ int bart_phase_clocks(uint64_t *host, size_t words) {
                               sizeof(uint64_t) * kMaxGrid * kClockSteps * kClockPh));
   return BART_OK;
 }
+// The stamps of the last sigma^2 step, u64 [kMaxGrid][kSigmaPh].
+int bart_sigma_clocks(uint64_t *host, size_t words) {
+  if (!host || words < (size_t)kMaxGrid * kSigmaPh)
+    return fail(BART_EINVAL, "need %zu words", (size_t)kMaxGrid * kSigmaPh);
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpyFromSymbol(host, HIP_SYMBOL(g_sigma_clock), sizeof(uint64_t) * kMaxGrid * kSigmaPh));
+  return BART_OK;
+}
 #endif
 
 }  // extern "C"

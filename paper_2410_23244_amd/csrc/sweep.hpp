@@ -45,9 +45,12 @@ constexpr uint32_t kSpinLimit = 1u << 21;
 // bart_phase_clocks): thread 0 of every workgroup of the register kernel
 // stamps the wall clock (100 MHz) at the phase boundaries of the tree steps
 // kClockStart .. kClockStart + kClockSteps - 1 of a launch, and every
-// workgroup counts the mailbox loads its polls issue in each of them.  The
-// ordinary build compiles none of it.
-constexpr int kClockStart = 205, kClockSteps = 64, kClockPh = 13;
+// workgroup counts the mailbox loads its polls issue in each of them; the
+// last thread of the workgroup (a polling thread) stamps the end of its
+// reduce, the start and end of its route, its loads, and the start and the
+// end of its polls.  The ordinary build
+// compiles none of it.
+constexpr int kClockStart = 205, kClockSteps = 48, kClockPh = 20;
 #ifdef BART_PHASE_CLOCKS
 __device__ uint64_t g_phase_clock[kMaxGrid][kClockSteps][kClockPh];
 __shared__ uint64_t clk_lds[kClockSteps][kClockPh];
@@ -58,13 +61,31 @@ __device__ __forceinline__ int clock_slot(int step) {
   do {                                                                                    \
     if (threadIdx.x == 0 && (slot) >= 0) clk_lds[slot][ph] = wall_clock64();              \
   } while (0)
+#define BART_CLOCK_LAST(slot, ph)                                                         \
+  do {                                                                                    \
+    if (threadIdx.x == kBlock - 1 && (slot) >= 0) clk_lds[slot][ph] = wall_clock64();     \
+  } while (0)
 #define BART_POLL_COUNT(n) (poll_loads += (n))
+// the sigma^2 step: stamps of the last one of a launch, thread 0 of every
+// workgroup, straight to device memory
+constexpr int kSigmaPh = 8;
+__device__ uint64_t g_sigma_clock[kMaxGrid][kSigmaPh];
+#define BART_SCLOCK(ph)                                                           \
+  do {                                                                            \
+    if (threadIdx.x == 0) g_sigma_clock[blockIdx.x][ph] = wall_clock64();         \
+  } while (0)
 #else
 __device__ __forceinline__ constexpr int clock_slot(int) { return -1; }
 #define BART_CLOCK(slot, ph) \
   do {                       \
   } while (0)
+#define BART_CLOCK_LAST(slot, ph) \
+  do {                            \
+  } while (0)
 #define BART_POLL_COUNT(n) ((void)0)
+#define BART_SCLOCK(ph) \
+  do {                  \
+  } while (0)
 #endif
 constexpr int kNullRank = kMaxLeaves;  // rank of a padding point (slot 0): no bin, zero delta
 constexpr int kBadRank = 255;          // rank of any other non-leaf slot: likewise, and flagged
@@ -426,6 +447,7 @@ __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH 
   const int nseg = (G + span - 1) / span;  // nseg * K <= kBlock
   const int first = kBlock - (nseg * K + 63) / 64 * 64;  // first polling thread
   const int t = (int)threadIdx.x - first;
+  BART_CLOCK_LAST(clk, 17);
   if (t >= 0 && t < nseg * K) {
     const int k = t % K, seg = t / K;
     const int g0 = seg * span, g1 = min(G, g0 + span);
@@ -460,6 +482,7 @@ __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH 
     }
     sh.part[t] = acc;
   }
+  BART_CLOCK_LAST(clk, 18);
 #ifdef BART_PHASE_CLOCKS
   if (clk >= 0 && poll_loads) atomicAdd((unsigned long long *)&clk_lds[clk][kClockPh - 1],
                                         (unsigned long long)poll_loads);
@@ -803,16 +826,21 @@ __device__ __forceinline__ void sigma2_tail(const SweepArgs *__restrict__ A, con
   if (!A->probit && t == kBlock - 64) sh.sig_gamma = sigma2_gamma(A, seed, s);
   // the next sweep's proposals (owners) and normals, published by the
   // release below together with this sweep's tree writes
+  BART_SCLOCK(1);
   gen_proposals(A, seed, s + 1, 0);
+  BART_SCLOCK(2);
   gen_normals(A, seed, s + 1, 0);
+  BART_SCLOCK(3);
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   __syncthreads();
+  BART_SCLOCK(4);
   if (t == 0) {
     double acc = 0.0;
     for (int u = 0; u < kWaves; ++u) acc += sh.wave_part[u];
     post(A, sh, par, 0, mk_word(seq, pack_f64(acc)));
   }
   gather_total(A, sh, par, seq, 1);
+  BART_SCLOCK(5);
   // acquire by the wave whose lanes polled (its cache invalidation serves
   // the whole workgroup: the other waves' reads follow the barrier at the
   // end of this step, so they happen after it)
@@ -1104,15 +1132,19 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
       //    posted by the reduce that formed them
       clk = clock_slot(step);
       BART_CLOCK(clk, 0);
+      BART_CLOCK_LAST(clk, 13);
       if (more1) route(j + 1, rk2);
       BART_CLOCK(clk, 1);
+      BART_CLOCK_LAST(clk, 14);
       // 2. while the mailboxes fill: load rows of j+2, the decision data of
       //    j+1 and the proposal of j+3
       // (the small loads first: nothing waits behind the row loads)
       const int j1 = more1 ? j + 1 : j, j3 = more3 ? j + 3 : j;
       const TdRegs tdn = load_tree_data(A, sh.ctx[j1 & (kRing - 1)], j1, s);
       const uint32_t pw3 = load_prop_word(A, j3);
+      BART_CLOCK_LAST(clk, 15);
       if (more2) issue_rows(j + 2);
+      BART_CLOCK_LAST(clk, 16);
       // 3. totals of tree j, in the same order in every workgroup: polls into
       //    per-segment partials, then one wave reduces a word over the
       //    segments with the fixed-order DPP tree (nseg <= 32 lanes).  The
@@ -1180,10 +1212,12 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
         lds_barrier();
       }
       BART_CLOCK(clk, 8);
+      BART_CLOCK_LAST(clk, 12);
       ++j;
     } else {
       // ================= sigma^2 step (sec. 3.3, "Sampling the error variance")
       clk = -1;
+      BART_SCLOCK(0);
       if (w == 0 && t == kBlock - 1 && uncounted >= 0)
         count_move(sh, sh.ctx[uncounted & (kRing - 1)]);
       uncounted = -1;
@@ -1205,7 +1239,9 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
           if (const uint32_t ok = ok4(v)) latent_chunk(A, seed, s, (w * V + v) * kBlock + t, ok, r[v]);
       j = 0;
       ++s;
+      BART_SCLOCK(6);
       if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s, step + 1);
+      BART_SCLOCK(7);
     }
   }
 

@@ -35,7 +35,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, os.path.dirname(HERE))
 
-K_GRID, K_STEPS, K_PH = 256, 64, 13  # kMaxGrid, kClockSteps, kClockPh
+K_GRID, K_STEPS, K_PH = 256, 48, 20  # kMaxGrid, kClockSteps, kClockPh
 K_START = 205                        # kClockStart
 PHASES = ["route", "prefetch", "gather", "decide", "barrier", "update", "finish", "reduce"]
 # stamps 9-11 (inside the reduce: bins done, bin barrier passed, rank 0 posted)
@@ -93,10 +93,37 @@ def run(config: int, warmup: int, seed: int, out: str | None) -> dict:
     res["gathered_to_posted_median_ns"] = float(np.median(post - gd))
     lw = post.argmax(0)
     res["last_poster_xcd_histogram (wg mod 8)"] = np.bincount(lw % 8, minlength=8).tolist()
+    # the last thread (a polling thread): its reduce ends (stamp 12) one step
+    # before the loop top (13), its route (14), decision-data and row loads
+    # (15, 16), poll start (17) and poll end (18)
+    pol = [clk[:, :-1, 12]] + [clk[:, 1:, q] for q in range(13, 19)]
+    names = ["reduce end to loop top", "route", "decision-data loads", "row loads",
+             "to polls start", "polls"]
+    lastpost = post[:, :-1].max(0)
+    res["poller_median_ns"] = {nm: float(np.median(pol[i + 1] - pol[i])) for i, nm in enumerate(names)}
+    res["poller_median_ns"]["polls start after last post"] = float(np.median(pol[5] - lastpost))
+    res["poller_median_ns"]["polls end after last post"] = float(np.median(pol[6] - lastpost))
+    late, cols = lw[:-1], np.arange(len(lw) - 1)
+    res["poller_last_poster_median_ns"] = {
+        nm: float(np.median((pol[i + 1] - pol[i])[late, cols])) for i, nm in enumerate(names)}
     # mailbox loads: words of every mailbox once, G^2 (L+1) per step, plus re-polls
     res["mailbox_loads_per_step_median"] = float(np.median(loads.sum(0)))
     res["mailbox_loads_per_wg_step_median"] = float(np.median(loads))
     res["mailbox_loads_per_wg_step_min"] = float(loads.min())
+    # the last sigma^2 step of the launch
+    lib.bart_sigma_clocks.argtypes = [C.c_void_p, C.c_size_t]
+    lib.bart_sigma_clocks.restype = C.c_int
+    sb = np.zeros(K_GRID * 8, np.uint64)
+    if lib.bart_sigma_clocks(sb.ctypes.data, sb.size) != 0:
+        raise RuntimeError(lib.bart_last_error().decode())
+    sc = sb.reshape(K_GRID, 8).astype(np.int64)[:G] * 10
+    ds = np.diff(sc, axis=1)
+    names = ["sums of squares", "proposals (owner wave 0)", "leaf normals", "release, barrier",
+             "gather of the sums", "draw", "refill of the next sweep"]
+    res["sigma2_step_median_ns"] = {nm: float(np.median(ds[:, k])) for k, nm in enumerate(names)}
+    res["sigma2_step_total_median_ns"] = float(np.median(sc[:, 7] - sc[:, 0]))
+    owners = min(G, inp.m)
+    res["proposal_owner_max_ns"] = float(ds[:owners, 1].max())
     g.close()
     return res
 
