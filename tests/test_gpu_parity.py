@@ -48,6 +48,13 @@ CASES = {
     "w1_stream_one_wg": (1, dict(n=997, p=8, m=12), 2, 13 * 2, 1, ORDINARY, STREAM),
     "w4_stream_u16": (4, dict(n=70001, p=20, m=50), 2, 51 + 10, 0, COOP, STREAM),
     "w5_stream_depth8": (5, dict(n=25003, p=1000, m=120), 2, 121 + 5, 3, COOP, STREAM),
+    # degenerate shapes: one observation, one chunk and a point, the shallowest
+    # trees (a root and its two children), a single tree, a single predictor
+    "w1_one_point": (1, dict(n=1, p=2, m=3), 2, 4 * 3, 0, COOP),
+    "w1_five_points_stream": (1, dict(n=5, p=3, m=4), 2, 5 * 3, 0, COOP, STREAM),
+    "w1_depth2": (1, dict(n=301, p=3, m=4, D=2), 2, 5 * 4, 0, COOP),
+    "w2_one_tree": (2, dict(n=5003, p=10, m=1), 3, 2 * 20, 0, COOP),
+    "w2_one_axis": (2, dict(n=2000, p=1, m=3), 2, 4 * 5, 0, ORDINARY),
 }
 
 
