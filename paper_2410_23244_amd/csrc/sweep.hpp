@@ -68,7 +68,7 @@ __device__ __forceinline__ int clock_slot(int step) {
 #define BART_POLL_COUNT(n) (poll_loads += (n))
 // the sigma^2 step: stamps of the last one of a launch, thread 0 of every
 // workgroup, straight to device memory
-constexpr int kSigmaPh = 8;
+constexpr int kSigmaPh = 9;
 __device__ uint64_t g_sigma_clock[kMaxGrid][kSigmaPh];
 #define BART_SCLOCK(ph)                                                           \
   do {                                                                            \
@@ -117,6 +117,18 @@ __device__ __forceinline__ uint64_t pack_f64(double x) {
 }
 __device__ __forceinline__ double unpack_f64(uint64_t w) {
   return __longlong_as_double((long long)((w & kPayloadMask) << (64 - kPayloadBits)));
+}
+
+// Make this workgroup's writes visible at agent scope before thread 0 posts
+// the word that announces them: the barrier orders every wave's writes
+// before wave 0 (they reach the XCD's L2 by the workgroup-scope release it
+// contains), then one agent-scope release by wave 0 writes the L2 back.  A
+// release by every wave queues eight write-backs per workgroup on the XCD's
+// L2 at once, and loads issued meanwhile (the proposals of the sigma^2 step)
+// wait behind them.
+__device__ __forceinline__ void publish_workgroup() {
+  __syncthreads();
+  if (threadIdx.x < 64) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
 }
 
 // Workgroup barrier that orders LDS accesses only: outstanding global loads
@@ -831,16 +843,17 @@ __device__ __forceinline__ void sigma2_tail(const SweepArgs *__restrict__ A, con
   BART_SCLOCK(2);
   gen_normals(A, seed, s + 1, 0);
   BART_SCLOCK(3);
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   __syncthreads();
   BART_SCLOCK(4);
+  if (t < 64) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // publish_workgroup, stamped
+  BART_SCLOCK(5);
   if (t == 0) {
     double acc = 0.0;
     for (int u = 0; u < kWaves; ++u) acc += sh.wave_part[u];
     post(A, sh, par, 0, mk_word(seq, pack_f64(acc)));
   }
   gather_total(A, sh, par, seq, 1);
-  BART_SCLOCK(5);
+  BART_SCLOCK(6);
   // acquire by the wave whose lanes polled (its cache invalidation serves
   // the whole workgroup: the other waves' reads follow the barrier at the
   // end of this step, so they happen after it)
@@ -1102,8 +1115,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     gen_proposals(A, seed, s, j);
     gen_normals(A, seed, s, j);
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
+  publish_workgroup();
   if (t == 0) post(A, sh, 1, 0, mk_word(1, 0));
   gather_total(A, sh, 1, 1, 0);
   // acquire by the polling wave; the barrier orders the other waves after it
@@ -1239,9 +1251,9 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
           if (const uint32_t ok = ok4(v)) latent_chunk(A, seed, s, (w * V + v) * kBlock + t, ok, r[v]);
       j = 0;
       ++s;
-      BART_SCLOCK(6);
-      if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s, step + 1);
       BART_SCLOCK(7);
+      if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s, step + 1);
+      BART_SCLOCK(8);
     }
   }
 
@@ -1599,8 +1611,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     gen_proposals(A, seed, s, j);
     gen_normals(A, seed, s, j);
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
+  publish_workgroup();
   if (t == 0) post(A, sh, 1, 0, mk_word(1, 0));
   gather_total(A, sh, 1, 1, 0);
   // acquire by the polling wave; the barrier orders the other waves after it

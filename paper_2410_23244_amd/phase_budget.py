@@ -37,6 +37,7 @@ sys.path.insert(0, os.path.dirname(HERE))
 
 K_GRID, K_STEPS, K_PH = 256, 48, 20  # kMaxGrid, kClockSteps, kClockPh
 K_START = 205                        # kClockStart
+K_SPH = 9                            # kSigmaPh
 PHASES = ["route", "prefetch", "gather", "decide", "barrier", "update", "finish", "reduce"]
 # stamps 9-11 (inside the reduce: bins done, bin barrier passed, rank 0 posted)
 SUB = ["bins", "bin barrier", "rank-0 total and post", "rest of reduce"]
@@ -113,15 +114,15 @@ def run(config: int, warmup: int, seed: int, out: str | None) -> dict:
     # the last sigma^2 step of the launch
     lib.bart_sigma_clocks.argtypes = [C.c_void_p, C.c_size_t]
     lib.bart_sigma_clocks.restype = C.c_int
-    sb = np.zeros(K_GRID * 8, np.uint64)
+    sb = np.zeros(K_GRID * K_SPH, np.uint64)
     if lib.bart_sigma_clocks(sb.ctypes.data, sb.size) != 0:
         raise RuntimeError(lib.bart_last_error().decode())
-    sc = sb.reshape(K_GRID, 8).astype(np.int64)[:G] * 10
+    sc = sb.reshape(K_GRID, K_SPH).astype(np.int64)[:G] * 10
     ds = np.diff(sc, axis=1)
-    names = ["sums of squares", "proposals (owner wave 0)", "leaf normals", "release, barrier",
-             "gather of the sums", "draw", "refill of the next sweep"]
+    names = ["sums of squares", "proposals (owner wave 0)", "leaf normals", "barrier",
+             "release (wave 0)", "gather of the sums", "draw", "refill of the next sweep"]
     res["sigma2_step_median_ns"] = {nm: float(np.median(ds[:, k])) for k, nm in enumerate(names)}
-    res["sigma2_step_total_median_ns"] = float(np.median(sc[:, 7] - sc[:, 0]))
+    res["sigma2_step_total_median_ns"] = float(np.median(sc[:, K_SPH - 1] - sc[:, 0]))
     owners = min(G, inp.m)
     res["proposal_owner_max_ns"] = float(ds[:owners, 1].max())
     g.close()
