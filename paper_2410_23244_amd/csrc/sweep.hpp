@@ -329,15 +329,24 @@ __device__ __forceinline__ void store_tree_data(TreeData &td, const Ctx &c, cons
   }
 }
 
-// Leaf normals of sweep s for trees >= j0, grid-stride over (tree, pair of
-// heap slots); each Philox block gives the normals of slots 2u and 2u+1.
+// Leaf normals of sweep s for trees >= j0, spread over every workgroup of
+// the chain: item q (tree q / H and pair u = q mod H of heap slots; one
+// Philox block gives the normals of slots 2u and 2u+1) goes to thread
+// first + q / G of workgroup q mod G.  The threads are those of the waves
+// that propose no tree (the first ceil(m / G) of a workgroup propose, see
+// gen_proposals) and draw no gamma variate (the last), so the normals run
+// beside the proposals on other SIMDs; with no such wave every thread takes
+// part.
 __device__ __noinline__ void gen_normals(const SweepArgs *__restrict__ A, uint64_t seed, int64_t s,
                                          int j0) {
   const Key key = chain_key(seed, A->chain);
-  const int H = A->H;
+  const int H = A->H, G = A->G, t = threadIdx.x;
+  int first = 64 * ((A->m + G - 1) / G), last = kBlock - 64;
+  if (first >= last) first = 0, last = kBlock;
+  if (t < first || t >= last) return;
   double *zb = A->z + (int64_t)(s & 1) * A->m * 2 * H;
-  const int64_t gsz = (int64_t)A->G * kBlock;
-  for (int64_t q = (int64_t)wg_id(A) * kBlock + threadIdx.x; q < (int64_t)A->m * H; q += gsz) {
+  const int64_t items = (int64_t)A->m * H;
+  for (int64_t q = (int64_t)(t - first) * G + wg_id(A); q < items; q += (int64_t)(last - first) * G) {
     const int tr = (int)(q / H), u = (int)(q % H);
     if (tr < j0) continue;
     const Block bl = draw(key, (uint64_t)s, (uint64_t)tr, 1, (uint64_t)u);
