@@ -863,10 +863,10 @@ __device__ __forceinline__ void sigma2_tail(const SweepArgs *__restrict__ A, con
   }
   gather_total(A, sh, par, seq, 1);
   BART_SCLOCK(6);
-  // acquire by the wave whose lanes polled (its cache invalidation serves
-  // the whole workgroup: the other waves' reads follow the barrier at the
-  // end of this step, so they happen after it)
-  if (t < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  // acquire by the wave that polled (a one-word gather polls on the last
+  // wave); the other waves read what it publishes after the barrier at the
+  // end of this step, and until then only LDS
+  if (t >= kBlock - 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   if (t == 0) {
     const double ssr_all = sh.tot[0];
     // the probit model holds sigma^2 at 1 and draws latents instead
@@ -1127,8 +1127,9 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   publish_workgroup();
   if (t == 0) post(A, sh, 1, 0, mk_word(1, 0));
   gather_total(A, sh, 1, 1, 0);
-  // acquire by the polling wave; the barrier orders the other waves after it
-  if (t < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  // acquire by the wave that polled (a one-word gather polls on the last
+  // wave); the barrier orders the other waves after it
+  if (t >= kBlock - 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __syncthreads();
   if (j < m && !sh.abort_flag) refill(j, s, 0);
 
@@ -1623,8 +1624,9 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   publish_workgroup();
   if (t == 0) post(A, sh, 1, 0, mk_word(1, 0));
   gather_total(A, sh, 1, 1, 0);
-  // acquire by the polling wave; the barrier orders the other waves after it
-  if (t < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  // acquire by the wave that polled (a one-word gather polls on the last
+  // wave); the barrier orders the other waves after it
+  if (t >= kBlock - 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __syncthreads();
   if (j < m && !sh.abort_flag) refill(j, s);
   bool have_ssr = false;
