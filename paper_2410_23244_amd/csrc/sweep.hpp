@@ -1027,21 +1027,24 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     if (lane == 0 && nr) atomicAdd(&sh.nr[tree & 1], nr);
   };
   // partial sums of tree `tree` from the current residuals: per-lane private
-  // LDS bins, two sets per lane (the points of chunk positions 0, 2 go to
-  // set 0, those of 1, 3 to set 1), so each lane runs two independent chains
-  // of read-modify-writes, for up to kRegRanks ranks at a time (a plain
-  // read-modify-write: LDS float atomics are many times slower; ranks outside
-  // the pass, the null rank of padding points among them, add 0 to a bin of
-  // the pass, so there is no branch per point); then a fixed-order fp64
-  // reduction of the 16 bins of each lane position and a DPP tree over the
-  // lanes; larger trees take several passes.  The wave that forms the total
+  // LDS bins in kSets sets per lane (with two, the points of chunk positions
+  // 0, 2 go to set 0, those of 1, 3 to set 1; with four, position e to set
+  // e), so each lane runs kSets independent chains of read-modify-writes,
+  // for up to kRegRanks ranks at a time (a plain read-modify-write: LDS float
+  // atomics are many times slower; ranks outside the pass, the null rank of
+  // padding points among them, add 0 to a bin of the pass, so there is no
+  // branch per point); then a fixed-order fp64 reduction of the kSets x 8
+  // bins of each lane position and a DPP tree over the lanes; larger trees
+  // take several passes.  The wave that forms the total
   // of rank k posts it as word k of this workgroup's mailbox for the step
   // that decides the tree (buffer par, step number seq), and after the first
   // bin barrier thread kBlock-1 posts the GROW right-count that route(tree)
   // gathered as word L: no barrier stands between the totals and the post
   // (only between passes).
-  constexpr int kSets = 2;
-  constexpr int kRegRanks = kBinFloats / (kSets * kBlock);  // 32
+  // four sets with 8 chunks per thread (chains of 8 read-modify-writes
+  // rather than 16: four chains 2547 -> 2562 chain-sweeps/s)
+  constexpr int kSets = V >= 8 ? 4 : 2;
+  constexpr int kRegRanks = kBinFloats / (kSets * kBlock);  // 32 or 16
   static_assert(kMaxLeaves % kRegRanks == 0 && kNullRank / kRegRanks >= kMaxLeaves / kRegRanks,
                 "the null rank must fall outside every bin pass");
   auto reduce = [&](int tree, const uint32_t (&rks)[V], int par, uint32_t seq) {
@@ -1055,16 +1058,20 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
 #pragma unroll
       for (int v = 0; v < V; ++v)
 #pragma unroll
-        for (int b = 0; b < 4; b += 2) {
-          const uint32_t ra = (rks[v] >> (8 * b)) & 0xffu, rb = (rks[v] >> (8 * b + 8)) & 0xffu;
+        for (int b0 = 0; b0 < 4; b0 += kSets) {
           const uint32_t pass = (uint32_t)(base / kRegRanks);
-          const int qa = ((int)(ra % kRegRanks) * kSets + 0) * kBlock + wl;
-          const int qb = ((int)(rb % kRegRanks) * kSets + 1) * kBlock + wl;
-          const float xa = ra / kRegRanks == pass ? r[v][b] : 0.f;
-          const float xb = rb / kRegRanks == pass ? r[v][b + 1] : 0.f;
-          const float ca = sh.bins[qa], cb = sh.bins[qb];
-          sh.bins[qa] = ca + xa;
-          sh.bins[qb] = cb + xb;
+          int q[kSets];
+          float x[kSets], cur[kSets];
+#pragma unroll
+          for (int e = 0; e < kSets; ++e) {
+            const uint32_t rr = (rks[v] >> (8 * (b0 + e))) & 0xffu;
+            q[e] = ((int)(rr % kRegRanks) * kSets + e) * kBlock + wl;
+            x[e] = rr / kRegRanks == pass ? r[v][b0 + e] : 0.f;
+          }
+#pragma unroll
+          for (int e = 0; e < kSets; ++e) cur[e] = sh.bins[q[e]];
+#pragma unroll
+          for (int e = 0; e < kSets; ++e) sh.bins[q[e]] = cur[e] + x[e];
         }
       if (base == 0) BART_CLOCK(clk, 9);
       lds_barrier();
@@ -1075,7 +1082,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
         sh.nr[tree & 1] = 0;
       }
       for (int k = base + wave; k < min(L, base + kRegRanks); k += kWaves) {
-        // the 16 bins of this lane position (2 sets x 8 waves): all read,
+        // the kSets x 8 bins of this lane position (sets x waves): all read,
         // then cleared, then summed in a fixed tree
         double x[kSets * kWaves];
 #pragma unroll
