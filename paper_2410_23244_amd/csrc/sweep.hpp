@@ -48,8 +48,7 @@ constexpr uint32_t kSpinLimit = 1u << 21;
 // workgroup counts the mailbox loads its polls issue in each of them; the
 // last thread of the workgroup (a polling thread) stamps the end of its
 // reduce, the start and end of its route, its loads, and the start and the
-// end of its polls.  The ordinary build
-// compiles none of it.
+// end of its polls.  The ordinary build compiles none of it.
 constexpr int kClockStart = 205, kClockSteps = 48, kClockPh = 20;
 #ifdef BART_PHASE_CLOCKS
 __device__ uint64_t g_phase_clock[kMaxGrid][kClockSteps][kClockPh];
@@ -346,7 +345,8 @@ __device__ __noinline__ void gen_normals(const SweepArgs *__restrict__ A, uint64
   if (t < first || t >= last) return;
   double *zb = A->z + (int64_t)(s & 1) * A->m * 2 * H;
   const int64_t items = (int64_t)A->m * H;
-  for (int64_t q = (int64_t)(t - first) * G + wg_id(A); q < items; q += (int64_t)(last - first) * G) {
+  const int64_t stride = (int64_t)(last - first) * G;
+  for (int64_t q = (int64_t)(t - first) * G + wg_id(A); q < items; q += stride) {
     const int tr = (int)(q / H), u = (int)(q % H);
     if (tr < j0) continue;
     const Block bl = draw(key, (uint64_t)s, (uint64_t)tr, 1, (uint64_t)u);
