@@ -263,6 +263,17 @@ int bart_set_state(bart_handle *h, const bart_state *src);
  * step and chain into trace (device bart_trace [nchain][n_steps]). */
 int bart_debug_steps(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace);
 
+/* Test hook for the bounded waits: one launch of n_steps steps (1 ..
+ * 2^20 - 8) in which workgroup wg of the launch grid (0 <= wg < grid x
+ * nchain) returns at once and every cross-workgroup wait gives up after
+ * spin_limit (>= 1) poll rounds.  Every other workgroup of wg's chain then
+ * ends the launch and bart_status reports BART_DEVERR_TIMEOUT.  The chains'
+ * state afterwards is unspecified (only bart_set_state or bart_destroy are
+ * meaningful); the position does not move.  With one workgroup per chain
+ * there is no cross-workgroup wait and nothing times out. */
+int bart_debug_stall(bart_handle *h, int32_t n_steps, uint64_t seed, int32_t wg,
+                     uint32_t spin_limit);
+
 /* Synchronise the stream and return BART_OK, or BART_EDEVICE with the device
  * error bits of all chains (or-ed) in *bits (may be NULL). */
 int bart_status(bart_handle *h, uint32_t *bits);

@@ -93,6 +93,7 @@ def lib():
         L.bart_get_state.argtypes = [vp, P(State)]
         L.bart_set_state.argtypes = [vp, P(State)]
         L.bart_debug_steps.argtypes = [vp, C.c_int32, C.c_uint64, vp]
+        L.bart_debug_stall.argtypes = [vp, C.c_int32, C.c_uint64, C.c_int32, C.c_uint32]
         L.bart_status.argtypes = [vp, P(C.c_uint32)]
         L.bart_launch_info.argtypes = [vp, P(LaunchInfo)]
         L.bart_move_stats.argtypes = [vp, C.c_int32, vp]
@@ -100,7 +101,7 @@ def lib():
         L.bart_destroy.restype = None
         L.bart_last_error.restype = C.c_char_p
         for f in ["bart_init", "bart_step", "bart_step_static", "bart_predict", "bart_get_state", "bart_set_state",
-                  "bart_debug_steps", "bart_status", "bart_launch_info",
+                  "bart_debug_steps", "bart_debug_stall", "bart_status", "bart_launch_info",
                   "bart_predict_accumulate", "bart_posterior_summary", "bart_cutpoints", "bart_bin", "bart_default_hyper",
                   "bart_move_stats"]:
             getattr(L, f).restype = C.c_int
@@ -199,6 +200,10 @@ def bart_debug_steps(h: int, n_steps: int, seed: int, trace_ptr: int) -> None:
     _check(lib().bart_debug_steps(h, int(n_steps), int(seed), trace_ptr))
 
 
+def bart_debug_stall(h: int, n_steps: int, seed: int, wg: int, spin_limit: int) -> None:
+    _check(lib().bart_debug_stall(h, int(n_steps), int(seed), int(wg), int(spin_limit)))
+
+
 def bart_status(h: int) -> int:
     bits = C.c_uint32(0)
     rc = lib().bart_status(h, C.byref(bits))
@@ -295,6 +300,12 @@ class Bart:
         self.stream.synchronize()
         tr = buf.cpu().numpy().view(TRACE_DTYPE)
         return tr if C_ == 1 else tr.reshape(C_, n_steps)
+
+    def debug_stall(self, n_steps: int, seed: int, wg: int, spin_limit: int) -> None:
+        """One launch with workgroup wg left out and every cross-workgroup wait
+        bounded by spin_limit poll rounds (the timeout path); see bart.h."""
+        bart_debug_stall(self.h, n_steps, seed, wg, spin_limit)
+        self.stream.synchronize()
 
     def predict(self, Xt, offset: float = 0.0):
         torch = self.torch

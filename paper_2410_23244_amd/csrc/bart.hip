@@ -505,7 +505,8 @@ SweepArgs make_args(bart_handle *h, int ch) {
 }
 
 int launch_sweep(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *trace,
-                 int64_t trace_stride, bool in_scratch) {
+                 int64_t trace_stride, bool in_scratch, uint32_t spin_limit = kSpinLimit,
+                 int32_t absent_wg = -1) {
   HIP_TRY(hipSetDevice(h->device));
   // mailbox words carry launch-relative step numbers: clear both buffers of
   // every chain (a fill kernel, so the call can be captured into a graph)
@@ -518,7 +519,7 @@ int launch_sweep(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace *tra
         h->ws, h->lay.pub, h->lay.chain_bytes, words);
   HIP_TRY(hipGetLastError());
   const SweepArgs *A = at<SweepArgs>(h, in_scratch ? h->lay.args_static : h->lay.args);
-  Launch Lc{h->sweep, h->next, n_steps, seed, trace, trace_stride};
+  Launch Lc{h->sweep, h->next, n_steps, seed, trace, trace_stride, spin_limit, absent_wg};
   void *args[] = {&A, &Lc};
   // the grid holds at most one workgroup per compute unit (checked at init)
   const dim3 grid(h->G * h->nchain);
@@ -732,6 +733,17 @@ int bart_debug_steps(bart_handle *h, int32_t n_steps, uint64_t seed, bart_trace 
   if (n_steps < 0) return fail(BART_EINVAL, "n_steps must be >= 0");
   if (n_steps > 0 && !trace) return fail(BART_EINVAL, "trace is NULL");
   return run_steps(h, n_steps, seed, trace);
+}
+
+int bart_debug_stall(bart_handle *h, int32_t n_steps, uint64_t seed, int32_t wg,
+                     uint32_t spin_limit) {
+  if (!h) return fail(BART_EINVAL, "handle is NULL");
+  if (n_steps < 1 || n_steps > kMaxLaunchSteps)
+    return fail(BART_EINVAL, "n_steps must be in [1, %d]", kMaxLaunchSteps);
+  if (wg < 0 || wg >= h->G * h->nchain)
+    return fail(BART_EINVAL, "wg %d is not in the launch grid of %d", wg, h->G * h->nchain);
+  if (spin_limit < 1) return fail(BART_EINVAL, "spin_limit must be >= 1");
+  return launch_sweep(h, n_steps, seed, nullptr, 0, false, spin_limit, wg);
 }
 
 int bart_predict(bart_handle *h, const uint8_t *Xt, int64_t xt_stride, int64_t n_t, double offset,

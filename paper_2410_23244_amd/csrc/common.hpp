@@ -88,6 +88,8 @@ struct Launch {
   uint64_t seed;
   bart_trace *trace;  // NULL: no trace; else [nchain][trace_stride] records
   int64_t trace_stride;
+  uint32_t spin_limit;  // poll rounds before a cross-workgroup wait gives up
+  int32_t absent_wg;    // -1; else a workgroup that returns at once (the timeout test)
 };
 
 // Index of the calling workgroup among the G workgroups of its chain.

@@ -39,6 +39,8 @@
 
 namespace bart {
 
+// Poll rounds a cross-workgroup wait may take before the launch gives up
+// (BART_DEVERR_TIMEOUT); launches pass it in Launch::spin_limit.
 constexpr uint32_t kSpinLimit = 1u << 21;
 
 // Phase clocks (diagnostic build, -DBART_PHASE_CLOCKS, read by
@@ -445,7 +447,8 @@ __device__ __forceinline__ void post(const SweepArgs *__restrict__ A, SH &sh, in
 // barrier.
 template <class SH>
 __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH &sh, int par,
-                                            uint32_t seq, int K, int nsum, int clk = -1) {
+                                            uint32_t seq, int K, int nsum, uint32_t limit,
+                                            int clk = -1) {
   const int G = A->G;
 #ifdef BART_PHASE_CLOCKS
   uint32_t poll_loads = 0;
@@ -490,7 +493,7 @@ __device__ __forceinline__ int gather_polls(const SweepArgs *__restrict__ A, SH 
           if (((pending >> u) & 1u) && seq_of(wv[u]) == seq) pending &= ~(1u << u);
         if (pending) {
           __builtin_amdgcn_s_sleep(1);
-          if (++spins > kSpinLimit) {
+          if (++spins > limit) {
             sh.abort_flag = 1;
             break;
           }
@@ -523,8 +526,8 @@ __device__ __forceinline__ double seg_total(const SH &sh, int nseg, int K, int k
 // Grid-wide sum of one fp64 word per workgroup (sigma^2 step), into sh.tot[0].
 template <class SH>
 __device__ __forceinline__ void gather_total(const SweepArgs *__restrict__ A, SH &sh, int par,
-                                             uint32_t seq, int nsum) {
-  const int nseg = gather_polls(A, sh, par, seq, 1, nsum);
+                                             uint32_t seq, int nsum, uint32_t limit) {
+  const int nseg = gather_polls(A, sh, par, seq, 1, nsum, limit);
   if (threadIdx.x == 0) sh.tot[0] = seg_total(sh, nseg, 1, 0);
   lds_barrier();
 }
@@ -861,7 +864,7 @@ __device__ __forceinline__ void sigma2_tail(const SweepArgs *__restrict__ A, con
     for (int u = 0; u < kWaves; ++u) acc += sh.wave_part[u];
     post(A, sh, par, 0, mk_word(seq, pack_f64(acc)));
   }
-  gather_total(A, sh, par, seq, 1);
+  gather_total(A, sh, par, seq, 1, Lc.spin_limit);
   BART_SCLOCK(6);
   // acquire by the wave that polled (a one-word gather polls on the last
   // wave); the other waves read what it publishes after the barrier at the
@@ -1133,7 +1136,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
   }
   publish_workgroup();
   if (t == 0) post(A, sh, 1, 0, mk_word(1, 0));
-  gather_total(A, sh, 1, 1, 0);
+  gather_total(A, sh, 1, 1, 0, Lc.spin_limit);
   // acquire by the wave that polled (a one-word gather polls on the last
   // wave); the barrier orders the other waves after it
   if (t >= kBlock - 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
@@ -1187,7 +1190,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
         for (int i = 0; i < 4; ++i) build_rank_slot(A, sh.ctx[(j + 2) & (kRing - 1)], 64 * i + lane);
       pre_decide(A, sh, c, sh.td[j & 1], w == 0 ? uncounted : -1);
       BART_CLOCK(clk, 2);
-      const int nseg = gather_polls(A, sh, par, seq, K, L, clk);
+      const int nseg = gather_polls(A, sh, par, seq, K, L, Lc.spin_limit, clk);
       BART_CLOCK(clk, 3);
       decide_step(A, sh, c, sh.td[j & 1], nseg);
       BART_CLOCK(clk, 4);
@@ -1297,6 +1300,8 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
 template <int V, int IB>
 __global__ void __launch_bounds__(kBlock) sweep_kernel(const SweepArgs *__restrict__ A, Launch Lc) {
   __shared__ Shared sh;
+  // a workgroup left out (bart_debug_stall): every wait on it times out
+  if ((int)blockIdx.x == Lc.absent_wg) return;
 #ifdef BART_PHASE_CLOCKS
   for (int q = threadIdx.x; q < kClockSteps * kClockPh; q += kBlock)
     clk_lds[q / kClockPh][q % kClockPh] = 0;
@@ -1634,7 +1639,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   }
   publish_workgroup();
   if (t == 0) post(A, sh, 1, 0, mk_word(1, 0));
-  gather_total(A, sh, 1, 1, 0);
+  gather_total(A, sh, 1, 1, 0, Lc.spin_limit);
   // acquire by the wave that polled (a one-word gather polls on the last
   // wave); the barrier orders the other waves after it
   if (t >= kBlock - 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
@@ -1663,7 +1668,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       // the poster of the count word clears it (see the register kernel)
       if (t == L) sh.nr[j & 1] = 0;
       pre_decide(A, sh, c, sh.td[j & 1], w == 0 ? uncounted : -1);
-      const int nseg = gather_polls(A, sh, par, seq, L + 1, L);
+      const int nseg = gather_polls(A, sh, par, seq, L + 1, L, Lc.spin_limit);
       decide_step(A, sh, c, sh.td[j & 1], nseg);
       if (more3 && t < kPropWords) ((uint32_t *)&sh.ctx[(j + 3) & (kRing - 1)].pr)[t] = pw3;
       if (CF && more3) store_struct(sh.ctx[(j + 3) & (kRing - 1)], sw3);
@@ -1714,6 +1719,7 @@ template <int IB, bool CF>
 __global__ void __launch_bounds__(kBlock) sweep_kernel_stream(const SweepArgs *__restrict__ A,
                                                               Launch Lc) {
   __shared__ Shared sh;
+  if ((int)blockIdx.x == Lc.absent_wg) return;
   const int c = (int)blockIdx.x / A->G;
   if (Lc.trace) Lc.trace += c * Lc.trace_stride;
   sweep_body_stream<IB, CF>(A + c, Lc, sh);

@@ -140,6 +140,25 @@ def test_set_state_flags_an_inconsistent_index_cache():
     assert c.status() == 0
 
 
+@pytest.mark.parametrize("residency", [REGS, STREAM])
+def test_an_absent_workgroup_ends_the_launch_with_a_timeout(residency):
+    """Every cross-workgroup wait is bounded: with one workgroup of the grid
+    left out and a small spin limit, the launch returns and reports
+    BART_DEVERR_TIMEOUT (1) instead of waiting for it; the workgroups that
+    ran exit normally, and a new chain on the same inputs then runs clean."""
+    inp = make_inputs(2, n=20011, p=10, m=12)
+    g = _gpu(inp, launch=ORDINARY, residency=residency)
+    info = g.launch_info()
+    print(f"grid={info.grid} residency={info.residency}", flush=True)
+    assert info.grid >= 2
+    g.debug_stall(2 * (inp.m + 1), 5, 1, 2000)
+    assert g.status() & 1
+    g.close()
+    h = _gpu(inp, launch=ORDINARY, residency=residency)
+    h.step(2, 5)
+    assert h.status() == 0
+
+
 def test_launch_modes_agree():
     inp = make_inputs(2, n=30011, p=16, m=20)
     a, b = _gpu(inp, launch=COOP), _gpu(inp, launch=ORDINARY)
