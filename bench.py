@@ -271,7 +271,8 @@ def main() -> int:
     g = from_inputs(inp, launch=mode, nchain=C, grid=args.grid)
     info = g.launch_info()
     kernel = (f"bart::sweep_kernel_stream<{max(1, inp.idx_bytes)}, "
-              f"{'true' if inp.idx_bytes == 0 else 'false'}>" if info.residency == 2 else
+              f"{'true' if inp.idx_bytes == 0 else 'false'}, "
+              f"{'true' if info.rank_stash else 'false'}>" if info.residency == 2 else
               f"bart::sweep_kernel<{info.chunks_per_thread}, {inp.idx_bytes}>")
     stream = g.stream
     for k in warm_plan:

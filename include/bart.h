@@ -166,11 +166,14 @@ typedef struct {
 } bart_trace;
 
 /* Launch shape chosen by bart_init (grid: workgroups per chain; the launch
- * has grid x nchain workgroups). */
+ * has grid x nchain workgroups).  rank_stash: 1 if streamed residuals keep
+ * each tree's leaf ranks in LDS from the pass that accumulates the tree to
+ * the pass that applies its decision (a thread's chunks fit the stash), 0
+ * otherwise. */
 typedef struct {
   int32_t grid, block, chunks_per_thread, lds_bytes;
   int32_t obs_per_thread, max_leaves, launch, residency;
-  int32_t nchain, reserved;
+  int32_t nchain, rank_stash;
 } bart_launch;
 
 /* Bytes of device workspace bart_init needs for cfg (0 if cfg is invalid). */

@@ -139,10 +139,15 @@ SweepFn regs_fn(int V) {
 
 SweepFn sweep_fn(int V, int IB) { return IB == 1 ? regs_fn<1>(V) : regs_fn<2>(V); }
 
-// IB = 0: no index cache (rolling u8 rows and Algorithm 1 per tree step)
-SweepFn stream_fn(int IB) {
-  return IB == 0 ? sweep_kernel_stream<1, true>
-                 : (IB == 1 ? sweep_kernel_stream<1, false> : sweep_kernel_stream<2, false>);
+// IB = 0: no index cache (Algorithm 1 per tree step); the rank stash when a
+// thread's chunks fit it
+template <bool ST>
+SweepFn stream_fn_st(int IB) {
+  return IB == 0 ? sweep_kernel_stream<1, true, ST>
+                 : (IB == 1 ? sweep_kernel_stream<1, false, ST> : sweep_kernel_stream<2, false, ST>);
+}
+SweepFn stream_fn(int IB, int cpt) {
+  return cpt <= kStashCpt ? stream_fn_st<true>(IB) : stream_fn_st<false>(IB);
 }
 
 // ------------------------------------------------------- static scratch
@@ -624,7 +629,7 @@ int bart_init(const bart_config *cfg, const uint8_t *X_b, const float *y_c, cons
     G = cfg->grid > 0 ? cfg->grid : gmax;
     cpt = (int)((chunks + (int64_t)G * kBlock - 1) / ((int64_t)G * kBlock));
   }
-  SweepFn fn = streamed ? stream_fn(cfg->idx_bytes) : sweep_fn(V, cfg->idx_bytes);
+  SweepFn fn = streamed ? stream_fn(cfg->idx_bytes, cpt) : sweep_fn(V, cfg->idx_bytes);
   int per_cu = 0;
   HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)fn, kBlock, 0));
   if (per_cu < 1) return fail(BART_ENOTSUP, "sweep kernel does not fit on a compute unit");
@@ -935,6 +940,7 @@ int bart_launch_info(const bart_handle *h, bart_launch *o) {
   o->max_leaves = std::min(h->H, kMaxLeaves);
   o->launch = h->cfg.launch;
   o->nchain = h->nchain;
+  o->rank_stash = h->streamed && h->V <= kStashCpt ? 1 : 0;
   return BART_OK;
 }
 

@@ -93,7 +93,14 @@ constexpr int kBadRank = 255;          // rank of any other non-leaf slot: likew
 constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
 constexpr int kBinRanks = kBinFloats / (kWaves * 64);  // ranks per pass of the LDS bins (64)
 constexpr int kSlotRanks = kBinRanks / 4;  // the same with a bin per chunk position (16)
-static_assert(kMaxLeaves % kBinRanks == 0 && kMaxLeaves % kSlotRanks == 0,
+// The streamed kernel with a rank stash: bins for half as many ranks per pass,
+// and the other half of the bin array holds one 32-bit word (the ranks of a
+// chunk's 4 points) per chunk of every thread.
+constexpr int kStashRanks = kSlotRanks / 2;                       // 8
+constexpr int kStashOffset = kStashRanks * 4 * kBlock;            // floats of bins before it
+constexpr int kStashCpt = (kBinFloats - kStashOffset) / kBlock;  // chunks per thread it holds (32)
+static_assert(kMaxLeaves % kBinRanks == 0 && kMaxLeaves % kSlotRanks == 0 &&
+                  kMaxLeaves % kStashRanks == 0,
               "the null rank must fall outside every bin pass");
 
 __device__ __forceinline__ uint64_t ld_dev(const uint64_t *p) {
@@ -1326,18 +1333,29 @@ __global__ void __launch_bounds__(kBlock) sweep_kernel(const SweepArgs *__restri
 // row and predictor row), writes it back, rewrites the index row where the
 // tree changed, and accumulates tree j+1's partial sums from the updated
 // value (route of j+1 from its rows).  Partial sums are fp64 per lane.
+// With ST (the chunks of a thread fit the stash, kStashCpt), the ranks of tree
+// j+1 that this pass computes stay in LDS, one byte per point, for the pass
+// of step j+1 that applies the tree: that pass then reads neither the index
+// row nor the predictor row again (nor, without an index cache, a rolling
+// row of leaves), and trees with more leaves than one bin pass holds take
+// their extra passes from the stash too.
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-template <int IB, bool CF>
+template <int IB, bool CF, bool ST>
 __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ A, const Launch &Lc,
                                                   Shared &sh) {
   using IC = IdxChunk<IB>;
   using ChunkT = typename IC::T;
-  // chunks of 4 points per batch (three batches in flight); without an index
+  // chunks of 4 points per batch (three batches in flight): without an index
   // cache two, so that the level-by-level predictor gathers of Algorithm 1
   // have twice the points in flight (one chunk: 374, two: 409 sweeps/s at
-  // n = 1e6; four spill)
-  constexpr int U = CF ? 2 : 1;
+  // n = 1e6; four spill); with the rank stash also two, as its batches load
+  // no rows of the tree they apply and would otherwise keep fewer bytes in
+  // flight (n = 1e7: one chunk 183, two 194, three 180 sweeps/s)
+  constexpr int U = (CF || ST) ? 2 : 1;
+  constexpr int kPassRanks = ST ? kStashRanks : kSlotRanks;
+  constexpr uint32_t kNull4 = kNullRank * 0x01010101u;  // a chunk of padding points
+  uint32_t *const stash = (uint32_t *)(sh.bins + kStashOffset);  // [kStashCpt][kBlock]
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6, w = wg_id(A);
   const int m = A->m, cpt = A->cpt;
   const uint64_t seed = Lc.seed;
@@ -1380,7 +1398,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   };
 
   // one pass: apply tree ja (-1: none), accumulate the ranks [lo, lo +
-  // kSlotRanks) of tree jn (-1: none) into sh.red (private fp32 bins per lane
+  // kPassRanks) of tree jn (-1: none) into sh.red (private fp32 bins per lane
   // and chunk position, then a fixed-order fp64 reduction), sum of squares
   // into sh.wave_part if want_ssr.  Ends with an LDS barrier.
   auto pass = [&](int ja, int jn, bool want_ssr, int lo) {
@@ -1390,7 +1408,13 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     const int flags = sh.flags, acc = flags & 1, merged = (flags >> 1) & 1;
     const int kl = ca.pr.rank_l, kr = ca.pr.rank_r, eta_a = ca.pr.eta;
     const bool changed = do_a && acc && ca.pr.move != kNone;
-    const bool xa = do_a && ca.pr.move == kGrow, xn = do_n && cn.pr.move == kGrow;
+    // a rejected GROW gives both children the merged value of eta (equal
+    // deltas), so the predictor row that tells them apart is read only when
+    // the GROW is accepted
+    const bool xa = do_a && ca.pr.move == kGrow && acc, xn = do_n && cn.pr.move == kGrow;
+    // ranks of tree jn: computed from its rows by the first bin pass, read
+    // back from the stash by the others
+    const bool fresh = do_n && (!ST || lo == 0);
     const int Ln = do_n ? cn.pr.L : 0;
     // index rows of trees ja and jn: rows of the cache, or without one the
     // two rolling rows (by tree parity) that carry a tree's leaves from the
@@ -1415,7 +1439,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     // a batch of U chunks per thread: its loads, then its arithmetic; the
     // loop keeps the next two batches' loads in flight while one is computed
     struct Batch {
-      int32_t ch[U];
+      int32_t ch[U], sl[U];  // chunk, and its stash word (-1: none)
       uint32_t ok[U];
       f32x4 rv[U];
       ChunkT ra[U], rn[U];
@@ -1434,20 +1458,24 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         B.ch[u] = (w * cpt + i0 + u) * kBlock + t;
+        B.sl[u] = i0 + u < cpt ? (i0 + u) * kBlock + t : -1;
         const bool valid = i0 + u < cpt && B.ch[u] < A->chunks;
         const int32_t rem = A->n - 4 * B.ch[u];
         B.ok[u] = !valid ? 0u : (rem >= 4 ? 15u : ((1u << rem) - 1u));
         cu[u] = valid ? B.ch[u] : 0;
         B.rv[u] = res[cu[u]];
       }
+      // with the stash, tree ja's ranks come from LDS: no loads of its rows
+      if (!ST) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) B.ra[u] = rowa[do_a ? cu[u] : 0];
+        for (int u = 0; u < U; ++u) B.ra[u] = rowa[do_a ? cu[u] : 0];
 #pragma unroll
-      for (int u = 0; u < U; ++u) B.xa4[u] = xra[xa ? cu[u] : 0];
+        for (int u = 0; u < U; ++u) B.xa4[u] = xra[xa ? cu[u] : 0];
+      }
 #pragma unroll
-      for (int u = 0; u < U; ++u) B.rn[u] = rown[do_n && !trav ? cu[u] : 0];
+      for (int u = 0; u < U; ++u) B.rn[u] = rown[fresh && !trav ? cu[u] : 0];
 #pragma unroll
-      for (int u = 0; u < U; ++u) B.xn4[u] = xrn[xn ? cu[u] : 0];
+      for (int u = 0; u < U; ++u) B.xn4[u] = xrn[xn && fresh ? cu[u] : 0];
     };
     auto compute_batch = [&](Batch &B) {
       int32_t (&ch)[U] = B.ch;
@@ -1460,7 +1488,8 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
 #pragma unroll
       for (int u = 0; u < U; ++u)
         if (!ok[u]) {
-          ra[u] = rn[u] = (ChunkT)0;
+          if (!ST) ra[u] = (ChunkT)0;
+          rn[u] = (ChunkT)0;
           rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
       if (trav) {
@@ -1499,14 +1528,18 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
 #pragma unroll
           for (int b = 0; b < 4; ++b) pk = IC::put(pk, b, ((ok[u] >> b) & 1u) ? hh[u][b] : 0);
           rn[u] = pk;
-          if (ok[u]) rown[ch[u]] = pk;
+          if (!ST && ok[u]) rown[ch[u]] = pk;
         }
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         int nra = 0;
         if (do_a) {
-          const uint32_t rk = ranks4(ca, ra[u], xa4[u], nra, bad);
+          uint32_t rk;
+          if (ST)
+            rk = ok[u] ? stash[B.sl[u]] : kNull4;
+          else
+            rk = ranks4(ca, ra[u], xa4[u], nra, bad);
           float dl[4];
 #pragma unroll
           for (int b = 0; b < 4; ++b) dl[b] = sh.dlt[(rk >> (8 * b)) & 0xff];
@@ -1535,13 +1568,19 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           // chunk never share one, so the chunk is one batch of independent
           // read-modify-writes (chunks follow in LDS order); points of the
           // null rank or outside the pass add 0 to a bin of the pass
-          const uint32_t rk = ranks4(cn, rn[u], xn4[u], nr, bad);
+          uint32_t rk;
+          if (ST && lo > 0) {
+            rk = ok[u] ? stash[B.sl[u]] : kNull4;
+          } else {
+            rk = ranks4(cn, rn[u], xn4[u], nr, bad);
+            if (ST && B.sl[u] >= 0) stash[B.sl[u]] = rk;  // after the read above
+          }
           int q[4];
           float add[4], cur[4];
 #pragma unroll
           for (int b = 0; b < 4; ++b) {
             const int rl = (int)((rk >> (8 * b)) & 0xff) - lo;
-            const bool in = rl >= 0 && rl < kSlotRanks;
+            const bool in = rl >= 0 && rl < kPassRanks;
             q[b] = ((((in ? rl : 0) * 4 + b) * kWaves + wave) << 6) | lane;
             add[b] = in ? rv[u][b] : 0.f;
           }
@@ -1576,7 +1615,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     }
     lds_barrier();
     if (do_n) {
-      for (int k = lo + wave; k < min(Ln, lo + kSlotRanks); k += kWaves) {
+      for (int k = lo + wave; k < min(Ln, lo + kPassRanks); k += kWaves) {
         double a = 0.0;
 #pragma unroll
         for (int u = 0; u < kWaves; ++u)
@@ -1597,7 +1636,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   auto pass_all = [&](int ja, int jn, bool want_ssr) {
     pass(ja, jn, want_ssr, 0);
     const int Ln = jn >= 0 ? sh.ctx[jn & (kRing - 1)].pr.L : 0;
-    for (int lo = kSlotRanks; lo < Ln; lo += kSlotRanks) pass(-1, jn, false, lo);
+    for (int lo = kPassRanks; lo < Ln; lo += kPassRanks) pass(-1, jn, false, lo);
   };
   auto partial = [&](int, int k) { return sh.red[k]; };
   // axis and cut of one heap slot of tree j (thread t < H), packed
@@ -1715,14 +1754,14 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
                                  (sh.dev_err ? BART_DEVERR_CACHE : 0u));
 }
 
-template <int IB, bool CF>
+template <int IB, bool CF, bool ST>
 __global__ void __launch_bounds__(kBlock) sweep_kernel_stream(const SweepArgs *__restrict__ A,
                                                               Launch Lc) {
   __shared__ Shared sh;
   if ((int)blockIdx.x == Lc.absent_wg) return;
   const int c = (int)blockIdx.x / A->G;
   if (Lc.trace) Lc.trace += c * Lc.trace_stride;
-  sweep_body_stream<IB, CF>(A + c, Lc, sh);
+  sweep_body_stream<IB, CF, ST>(A + c, Lc, sh);
 }
 
 }  // namespace bart

@@ -69,7 +69,7 @@ def test_lockstep_small(name):
     print(f"  grid={info.grid} chunks/thread={info.chunks_per_thread} "
           f"residency={info.residency}", flush=True)
     if residency == STREAM:
-        assert info.residency == STREAM
+        assert info.residency == STREAM and info.rank_stash == 1
     rep = parity.lockstep(inp, g, seed=inp.seed + 100, warm_sweeps=warm, n_steps=steps)
     print(f"  {rep}", flush=True)
     assert rep.tree_steps > 0 and rep.moves > 0
@@ -284,6 +284,32 @@ def test_lockstep_big_trees(shape, residency):
           flush=True)
     g.set_state(_full_trees(inp, depth, np.random.default_rng(7)))
     rep = parity.lockstep(inp, g, seed=5, warm_sweeps=0, n_steps=2 * (inp.m + 1))
+    print(f"  {rep}", flush=True)
+    assert rep.moves > 0
+
+
+@pytest.mark.parametrize("shape", ["u8", "u16", "d6_32_leaves", "no_index_cache"])
+def test_streamed_without_the_rank_stash(shape):
+    """More chunks per thread than the LDS rank stash holds (one workgroup,
+    n = 70001: 35 chunks of 4 points per thread): the streamed kernel reads
+    each tree's rows again in the pass that applies it.  Small trees, u8 and
+    u16 caches, 32-leaf trees (two bin passes) and no index cache."""
+    if shape == "u16":
+        inp = make_inputs(4, n=70001, p=12, m=16)
+    elif shape == "no_index_cache":
+        inp = make_inputs(2, n=70001, p=12, m=16, idx_bytes=0)
+    else:
+        inp = make_inputs(2, n=70001, p=12, m=12 if shape == "d6_32_leaves" else 16)
+    g = _gpu(inp, grid=1, launch=ORDINARY, residency=STREAM)
+    info = g.launch_info()
+    print(f"{shape}: grid={info.grid} chunks/thread={info.chunks_per_thread} "
+          f"rank_stash={info.rank_stash}", flush=True)
+    assert info.residency == STREAM and info.rank_stash == 0 and info.chunks_per_thread > 32
+    if shape == "d6_32_leaves":
+        g.set_state(_full_trees(inp, 5, np.random.default_rng(7)))
+        rep = parity.lockstep(inp, g, seed=5, warm_sweeps=0, n_steps=2 * (inp.m + 1))
+    else:
+        rep = parity.lockstep(inp, g, seed=inp.seed + 3, warm_sweeps=2, n_steps=inp.m + 1 + 9)
     print(f"  {rep}", flush=True)
     assert rep.moves > 0
 
