@@ -204,7 +204,11 @@ struct Ctx {
   uint16_t heap_of[256];  // rank -> heap slot; 0 from kNullRank on
   uint16_t ax[kMaxLeaves];       // without an index cache: the tree's axis and cut per
   uint8_t ct[kMaxLeaves];        // internal heap slot, for Algorithm 1
+  uint8_t nidx[kMaxLeaves];      // heap slot -> index among the internal nodes (kNoNode: none)
+  uint8_t nh[kMaxLeaves];        // heap slot of the k-th internal node, in heap order
+  int32_t ni;                    // internal nodes
 };
+constexpr int kNoNode = 255;
 
 // What the decision of one tree needs besides the sums: per rank of the
 // larger tree its stored count, current value and leaf normal, and the same
@@ -293,6 +297,28 @@ __device__ __forceinline__ void build_rank_slot(const SweepArgs *__restrict__ A,
 // Rank table of the larger tree: threads 0..255, one slot each.
 __device__ __forceinline__ void build_ranks(const SweepArgs *__restrict__ A, Ctx &c) {
   if (threadIdx.x < 256) build_rank_slot(A, c, (int)threadIdx.x);
+}
+
+// Without an index cache: the internal nodes of the tree snapshot in c (cut
+// nonzero; a slot outside the tree has cut 0), numbered in heap order by a
+// ballot per 64 slots.  Wave 4 (it holds no rank slot), after the snapshot
+// is in LDS.
+__device__ __forceinline__ void build_inodes(const SweepArgs *__restrict__ A, Ctx &c) {
+  const int t = (int)threadIdx.x, lane = t & 63;
+  if ((t >> 6) != 4) return;
+  const int H = A->H;
+  int base = 0;
+  for (int h0 = 0; h0 < H; h0 += 64) {
+    const int h = h0 + lane;
+    const bool in = h >= 1 && h < H && c.ct[h] != 0;
+    const uint64_t bal = __ballot(in);
+    const int k = base + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+    if (h < H) c.nidx[h] = in ? (uint8_t)k : (uint8_t)kNoNode;
+    if (in) c.nh[k] = (uint8_t)h;
+    base += __popcll(bal);
+  }
+  if (lane == 0) c.ni = base;
 }
 
 // Thread that loads and stages the decision data of the move's node eta: in
@@ -1492,9 +1518,69 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           rn[u] = (ChunkT)0;
           rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-      if (trav) {
-        // leaves of tree jn by Algorithm 1 on its structure snapshot, level
-        // by level with the predictor bytes of all 4 U points in flight
+      if (trav && cn.ni <= 32) {
+        // leaves of tree jn by Algorithm 1 on its structure snapshot: the
+        // decision of every internal node for the chunk's 4 points, from one
+        // coalesced word of the node's predictor row (8 nodes' words in
+        // flight at a time, so a small tree costs one round trip, not one
+        // per level), as bit k of a mask per point; then the descent in
+        // registers
+        uint32_t bits[U][4];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) bits[u][b] = 0u;
+        const int ni = cn.ni;
+        int32_t cu[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) cu[u] = ok[u] ? ch[u] : 0;
+        for (int k0 = 0; k0 < ni; k0 += 8) {
+          uint32_t wd[8][U];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int k = k0 + e < ni ? k0 + e : 0;
+            const gptr<const uint32_t> xr =
+                gbl((const uint32_t *)(A->X + (int64_t)cn.ax[cn.nh[k]] * A->ldx));
+#pragma unroll
+            for (int u = 0; u < U; ++u) wd[e][u] = xr[cu[u]];
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int k = k0 + e;
+            const int cv = k < ni ? (int)cn.ct[cn.nh[k]] : 256;  // no bit past the last node
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+              for (int b = 0; b < 4; ++b)
+                bits[u][b] |= (uint32_t)((int)((wd[e][u] >> (8 * b)) & 0xffu) >= cv) << (k & 31);
+          }
+        }
+        const int H = A->H;
+        int hh[U][4];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) hh[u][b] = 1;
+        for (int lvl = 1; lvl < A->D; ++lvl)
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              const int h = hh[u][b];
+              const int q = h < H ? (int)cn.nidx[h] : kNoNode;
+              if (q != kNoNode) hh[u][b] = 2 * h + (int)((bits[u][b] >> q) & 1u);
+            }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          ChunkT pk = 0;
+#pragma unroll
+          for (int b = 0; b < 4; ++b) pk = IC::put(pk, b, ((ok[u] >> b) & 1u) ? hh[u][b] : 0);
+          rn[u] = pk;
+          if (!ST && ok[u]) rown[ch[u]] = pk;
+        }
+      } else if (trav) {
+        // a tree with more internal nodes than a mask holds (depth 8 only):
+        // level by level, with the predictor bytes of all 4 U points in flight
         int hh[U][4];
 #pragma unroll
         for (int u = 0; u < U; ++u)
@@ -1662,7 +1748,10 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       }
     lds_barrier();
     for (int q = 0; q < 3; ++q)
-      if (j0 + q < m) build_ranks(A, sh.ctx[(j0 + q) & (kRing - 1)]);
+      if (j0 + q < m) {
+        build_ranks(A, sh.ctx[(j0 + q) & (kRing - 1)]);
+        if (CF) build_inodes(A, sh.ctx[(j0 + q) & (kRing - 1)]);
+      }
     lds_barrier();
     const TdRegs tr0 = load_tree_data(A, sh.ctx[j0 & (kRing - 1)], j0, s);
     store_tree_data(sh.td[j0 & 1], sh.ctx[j0 & (kRing - 1)], tr0);
@@ -1745,6 +1834,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       finish_tree(A, Lc, sh, c, j, s, step);
       uncounted = j;
       if (more3) build_ranks(A, sh.ctx[(j + 3) & (kRing - 1)]);
+      if (CF && more3) build_inodes(A, sh.ctx[(j + 3) & (kRing - 1)]);
       have_ssr = j == m - 1;
       pass_all(j, more1 ? j + 1 : -1, have_ssr);
       ++j;

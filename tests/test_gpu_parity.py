@@ -270,16 +270,22 @@ def _full_trees(inp, depth, rng):
                 sigma2=inp.hyper.sigma2_init, sweep=0, next=0)
 
 
-@pytest.mark.parametrize("residency", [REGS, STREAM])
+NO_CACHE = -1  # streamed residuals without an index cache
+
+
+@pytest.mark.parametrize("residency", [REGS, STREAM, NO_CACHE])
 @pytest.mark.parametrize("shape", ["d6_32_leaves", "d8_128_leaves"])
 def test_lockstep_big_trees(shape, residency):
     """Trees far larger than the sampler grows by itself: 32 and 128 leaves
-    take the LDS-bin reductions and mailboxes of up to 129 words."""
+    take the LDS-bin reductions and mailboxes of up to 129 words; without an
+    index cache, 31 internal nodes fill the 32-bit decision masks of the
+    descent and 127 take the level-by-level descent."""
+    kw = dict(idx_bytes=0) if residency == NO_CACHE else {}
     if shape == "d6_32_leaves":
-        inp, depth = make_inputs(2, n=20011, p=12, m=12), 5
+        inp, depth = make_inputs(2, n=20011, p=12, m=12, **kw), 5
     else:
-        inp, depth = make_inputs(5, n=30011, p=40, m=6), 7
-    g = _gpu(inp, residency=residency)
+        inp, depth = make_inputs(5, n=30011, p=40, m=6, **kw), 7
+    g = _gpu(inp, residency=STREAM if residency == NO_CACHE else residency)
     print(f"{shape}: grid={g.launch_info().grid} residency={g.launch_info().residency}",
           flush=True)
     g.set_state(_full_trees(inp, depth, np.random.default_rng(7)))
