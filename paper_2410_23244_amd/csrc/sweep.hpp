@@ -204,9 +204,13 @@ struct Ctx {
   uint16_t heap_of[256];  // rank -> heap slot; 0 from kNullRank on
   uint16_t ax[kMaxLeaves];       // without an index cache: the tree's axis and cut per
   uint8_t ct[kMaxLeaves];        // internal heap slot, for Algorithm 1
-  uint8_t nidx[kMaxLeaves];      // heap slot -> index among the internal nodes (kNoNode: none)
-  uint8_t nh[kMaxLeaves];        // heap slot of the k-th internal node, in heap order
-  int32_t ni;                    // internal nodes
+};
+
+// Without an index cache: the internal nodes of a tree snapshot, by ring slot.
+struct NodeList {
+  uint8_t nidx[kMaxLeaves];  // heap slot -> index among the internal nodes (kNoNode: none)
+  uint8_t nh[kMaxLeaves];    // heap slot of the k-th internal node, in heap order
+  int32_t ni;                // internal nodes
 };
 constexpr int kNoNode = 255;
 
@@ -250,6 +254,7 @@ struct Shared {
   int flags;  // bit0 accept, bit1 merged
   int abort_flag;
   int dev_err;
+  NodeList nl[kRing];  // last, so the other members keep their offsets
 };
 
 template <int IB>
@@ -303,7 +308,8 @@ __device__ __forceinline__ void build_ranks(const SweepArgs *__restrict__ A, Ctx
 // nonzero; a slot outside the tree has cut 0), numbered in heap order by a
 // ballot per 64 slots.  Wave 4 (it holds no rank slot), after the snapshot
 // is in LDS.
-__device__ __forceinline__ void build_inodes(const SweepArgs *__restrict__ A, Ctx &c) {
+__device__ __forceinline__ void build_inodes(const SweepArgs *__restrict__ A, const Ctx &c,
+                                             NodeList &nl) {
   const int t = (int)threadIdx.x, lane = t & 63;
   if ((t >> 6) != 4) return;
   const int H = A->H;
@@ -314,11 +320,11 @@ __device__ __forceinline__ void build_inodes(const SweepArgs *__restrict__ A, Ct
     const uint64_t bal = __ballot(in);
     const int k = base + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-    if (h < H) c.nidx[h] = in ? (uint8_t)k : (uint8_t)kNoNode;
-    if (in) c.nh[k] = (uint8_t)h;
+    if (h < H) nl.nidx[h] = in ? (uint8_t)k : (uint8_t)kNoNode;
+    if (in) nl.nh[k] = (uint8_t)h;
     base += __popcll(bal);
   }
-  if (lane == 0) c.ni = base;
+  if (lane == 0) nl.ni = base;
 }
 
 // Thread that loads and stages the decision data of the move's node eta: in
@@ -1518,7 +1524,8 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           rn[u] = (ChunkT)0;
           rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-      if (trav && cn.ni <= 32) {
+      const NodeList &nn = sh.nl[(jn < 0 ? 0 : jn) & (kRing - 1)];
+      if (trav && nn.ni <= 32) {
         // leaves of tree jn by Algorithm 1 on its structure snapshot: the
         // decision of every internal node for the chunk's 4 points, from one
         // coalesced word of the node's predictor row (8 nodes' words in
@@ -1530,7 +1537,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
         for (int u = 0; u < U; ++u)
 #pragma unroll
           for (int b = 0; b < 4; ++b) bits[u][b] = 0u;
-        const int ni = cn.ni;
+        const int ni = nn.ni;
         int32_t cu[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) cu[u] = ok[u] ? ch[u] : 0;
@@ -1540,14 +1547,14 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           for (int e = 0; e < 8; ++e) {
             const int k = k0 + e < ni ? k0 + e : 0;
             const gptr<const uint32_t> xr =
-                gbl((const uint32_t *)(A->X + (int64_t)cn.ax[cn.nh[k]] * A->ldx));
+                gbl((const uint32_t *)(A->X + (int64_t)cn.ax[nn.nh[k]] * A->ldx));
 #pragma unroll
             for (int u = 0; u < U; ++u) wd[e][u] = xr[cu[u]];
           }
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const int k = k0 + e;
-            const int cv = k < ni ? (int)cn.ct[cn.nh[k]] : 256;  // no bit past the last node
+            const int cv = k < ni ? (int)cn.ct[nn.nh[k]] : 256;  // no bit past the last node
 #pragma unroll
             for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -1567,7 +1574,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
               const int h = hh[u][b];
-              const int q = h < H ? (int)cn.nidx[h] : kNoNode;
+              const int q = h < H ? (int)nn.nidx[h] : kNoNode;
               if (q != kNoNode) hh[u][b] = 2 * h + (int)((bits[u][b] >> q) & 1u);
             }
 #pragma unroll
@@ -1750,7 +1757,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     for (int q = 0; q < 3; ++q)
       if (j0 + q < m) {
         build_ranks(A, sh.ctx[(j0 + q) & (kRing - 1)]);
-        if (CF) build_inodes(A, sh.ctx[(j0 + q) & (kRing - 1)]);
+        if (CF) build_inodes(A, sh.ctx[(j0 + q) & (kRing - 1)], sh.nl[(j0 + q) & (kRing - 1)]);
       }
     lds_barrier();
     const TdRegs tr0 = load_tree_data(A, sh.ctx[j0 & (kRing - 1)], j0, s);
@@ -1834,7 +1841,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       finish_tree(A, Lc, sh, c, j, s, step);
       uncounted = j;
       if (more3) build_ranks(A, sh.ctx[(j + 3) & (kRing - 1)]);
-      if (CF && more3) build_inodes(A, sh.ctx[(j + 3) & (kRing - 1)]);
+      if (CF && more3) build_inodes(A, sh.ctx[(j + 3) & (kRing - 1)], sh.nl[(j + 3) & (kRing - 1)]);
       have_ssr = j == m - 1;
       pass_all(j, more1 ? j + 1 : -1, have_ssr);
       ++j;
