@@ -340,7 +340,7 @@ __global__ void k_recount(const uint8_t *idx, int64_t ldi, int ib, int32_t *coun
 // of writing fp32(f) to out.
 constexpr int kPredBlock = 256;
 constexpr int kPredNodes = 2048;  // heap slots per LDS tile (axis u16 + cut u8 + 2 leaves f32: 22 KB)
-constexpr int kPredIlp = 4;
+constexpr int kPredIlp = 8;
 
 template <bool ACC>
 __global__ void __launch_bounds__(kPredBlock)
