@@ -91,16 +91,16 @@ __device__ __forceinline__ constexpr int clock_slot(int) { return -1; }
 constexpr int kNullRank = kMaxLeaves;  // rank of a padding point (slot 0): no bin, zero delta
 constexpr int kBadRank = 255;          // rank of any other non-leaf slot: likewise, and flagged
 constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, rows j+2, load j+3
-constexpr int kBinRanks = kBinFloats / (kWaves * 64);  // ranks per pass of the LDS bins (64)
-constexpr int kSlotRanks = kBinRanks / 4;  // the same with a bin per chunk position (16)
+// Ranks per pass of the streamed kernel's LDS bins, one bin per lane and chunk
+// position (16).
+constexpr int kSlotRanks = kBinFloats / (4 * kBlock);
 // The streamed kernel with a rank stash: bins for half as many ranks per pass,
 // and the other half of the bin array holds one 32-bit word (the ranks of a
 // chunk's 4 points) per chunk of every thread.
 constexpr int kStashRanks = kSlotRanks / 2;                       // 8
 constexpr int kStashOffset = kStashRanks * 4 * kBlock;            // floats of bins before it
 constexpr int kStashCpt = (kBinFloats - kStashOffset) / kBlock;  // chunks per thread it holds (32)
-static_assert(kMaxLeaves % kBinRanks == 0 && kMaxLeaves % kSlotRanks == 0 &&
-                  kMaxLeaves % kStashRanks == 0,
+static_assert(kMaxLeaves % kSlotRanks == 0 && kMaxLeaves % kStashRanks == 0,
               "the null rank must fall outside every bin pass");
 
 __device__ __forceinline__ uint64_t ld_dev(const uint64_t *p) {
