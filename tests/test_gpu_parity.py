@@ -517,10 +517,14 @@ def test_probit_recovers_class_probabilities():
 # ---------------------------------------------------------------- no index cache
 
 @pytest.mark.parametrize("cfg,over", [(2, dict(n=40003, p=30, m=40)),
-                                      (5, dict(n=25003, p=1000, m=120))])
+                                      (5, dict(n=25003, p=1000, m=120)),
+                                      (1, dict(n=301, p=3, m=4, D=2)),
+                                      (5, dict(n=20011, p=50, m=40, D=7))])
 def test_no_index_cache_lockstep(cfg, over):
     """idx_bytes = 0: the trees route the observations by Algorithm 1 every
-    step; lockstep against the oracle, whose cache the device exports."""
+    step; lockstep against the oracle, whose cache the device exports.  Depth
+    2 and 6 take the decision bits by heap slot, depth 7 and 8 by the node's
+    place in the list of internal nodes."""
     inp = make_inputs(cfg, **over, idx_bytes=0)
     g = _gpu(inp, grid=4, launch=ORDINARY)
     assert g.launch_info().residency == STREAM
