@@ -294,6 +294,21 @@ def test_lockstep_big_trees(shape, residency):
     assert rep.moves > 0
 
 
+@pytest.mark.parametrize("n,stash", [(65536, 1), (65537, 0)])
+def test_streamed_at_the_stash_capacity(n, stash):
+    """One workgroup with exactly 32 chunks of 4 points per thread (every
+    word of the LDS rank stash in use) and with 33 (the first size past it,
+    a ragged last chunk): the kernel switches between its two passes there."""
+    inp = make_inputs(4, n=n, p=12, m=16)
+    g = _gpu(inp, grid=1, launch=ORDINARY, residency=STREAM)
+    info = g.launch_info()
+    print(f"n={n}: chunks/thread={info.chunks_per_thread} rank_stash={info.rank_stash}", flush=True)
+    assert info.rank_stash == stash and info.chunks_per_thread == 32 + (1 - stash)
+    rep = parity.lockstep(inp, g, seed=inp.seed + 11, warm_sweeps=2, n_steps=inp.m + 1 + 9)
+    print(f"  {rep}", flush=True)
+    assert rep.moves > 0
+
+
 @pytest.mark.parametrize("shape", ["u8", "u16", "d6_32_leaves", "no_index_cache"])
 def test_streamed_without_the_rank_stash(shape):
     """More chunks per thread than the LDS rank stash holds (one workgroup,
