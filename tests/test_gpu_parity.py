@@ -294,6 +294,28 @@ def test_lockstep_big_trees(shape, residency):
     assert rep.moves > 0
 
 
+@pytest.mark.parametrize("extra", [0, 1])
+def test_register_residency_at_its_maximum(extra):
+    """n = 256 workgroups x 512 threads x 8 chunks x 4 points fills every
+    residual register of the grid (automatic residency keeps them on chip);
+    one observation more streams them from HBM."""
+    n = 256 * 512 * 8 * 4 + extra
+    inp = make_inputs(2, n=n, p=10, m=6)
+    g = _gpu(inp, launch=ORDINARY)
+    info = g.launch_info()
+    print(f"n={n}: grid={info.grid} chunks/thread={info.chunks_per_thread} "
+          f"residency={info.residency}", flush=True)
+    if info.grid < 256:
+        pytest.skip("fewer than 256 compute units")
+    if extra == 0:
+        assert info.residency == REGS and info.chunks_per_thread == 8
+    else:
+        assert info.residency == STREAM and info.rank_stash == 1
+    rep = parity.lockstep(inp, g, seed=inp.seed + 13, warm_sweeps=1, n_steps=inp.m + 1 + 3)
+    print(f"  {rep}", flush=True)
+    assert rep.moves > 0
+
+
 @pytest.mark.parametrize("n,stash", [(65536, 1), (65537, 0)])
 def test_streamed_at_the_stash_capacity(n, stash):
     """One workgroup with exactly 32 chunks of 4 points per thread (every
