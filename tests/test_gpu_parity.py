@@ -54,6 +54,10 @@ CASES = {
     "w1_five_points_stream": (1, dict(n=5, p=3, m=4), 2, 5 * 3, 0, COOP, STREAM),
     "w1_depth2": (1, dict(n=301, p=3, m=4, D=2), 2, 5 * 4, 0, COOP),
     "w2_one_tree": (2, dict(n=5003, p=10, m=1), 3, 2 * 20, 0, COOP),
+    "w2_one_tree_stream": (2, dict(n=5003, p=10, m=1), 3, 2 * 20, 0, COOP, STREAM),
+    "w2_one_tree_no_cache": (2, dict(n=5003, p=10, m=1, idx_bytes=0), 3, 2 * 20, 0, COOP, STREAM),
+    "w2_two_trees_no_cache": (2, dict(n=5003, p=10, m=2, idx_bytes=0), 3, 3 * 12, 0, ORDINARY,
+                              STREAM),
     "w2_one_axis": (2, dict(n=2000, p=1, m=3), 2, 4 * 5, 0, ORDINARY),
 }
 
