@@ -28,19 +28,21 @@ def _same(a, b, nchain):
         assert sa["sigma2"] == sb["sigma2"] and sa["sweep"] == sb["sweep"]
 
 
-@pytest.mark.parametrize("launch", [0, 1])
-def test_step_static_equals_step_on_two_calls(launch):
-    # first call: 2 chains of 10 workgroups, 40003 observations
+@pytest.mark.parametrize("launch,residency", [(0, 0), (1, 0), (1, 2)])
+def test_step_static_equals_step_on_two_calls(launch, residency):
+    # first call: 2 chains of 10 workgroups, 40003 observations (residency 0:
+    # automatic, registers at these sizes; 2: streamed)
     inp = make_inputs(2, n=40003, p=30, m=40)
-    a, b = _pair(inp, grid=10, nchain=2, launch=launch)
-    print(f"call 1: n={inp.n} grid={a.launch_info().grid} nchain=2", flush=True)
+    a, b = _pair(inp, grid=10, nchain=2, launch=launch, residency=residency)
+    print(f"call 1: n={inp.n} grid={a.launch_info().grid} nchain=2 "
+          f"residency={a.launch_info().residency}", flush=True)
     a.step(3, 17)
     b.step_static(3, 17)
     assert a.status() == 0 and b.status() == 0
     _same(a, b, 2)
     # second call, smaller: one chain of 3 workgroups, 5003 observations
     inp2 = make_inputs(1, n=5003, p=8, m=12)
-    a2, b2 = _pair(inp2, grid=3, launch=launch)
+    a2, b2 = _pair(inp2, grid=3, launch=launch, residency=residency)
     print(f"call 2: n={inp2.n} grid={a2.launch_info().grid} nchain=1", flush=True)
     a2.step(4, 5)
     b2.step_static(4, 5)
