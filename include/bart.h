@@ -169,11 +169,14 @@ typedef struct {
  * has grid x nchain workgroups).  rank_stash: 1 if streamed residuals keep
  * each tree's leaf ranks in LDS from the pass that accumulates the tree to
  * the pass that applies its decision (a thread's chunks fit the stash), 0
- * otherwise. */
+ * otherwise.  stash_chunks: the most chunks of 4 observations per thread the
+ * stash holds.  lds_resid_chunks: with the stash, how many of a thread's
+ * chunks keep their residuals in LDS for the whole launch (the others stream
+ * from HBM every tree step); 0 otherwise. */
 typedef struct {
   int32_t grid, block, chunks_per_thread, lds_bytes;
   int32_t obs_per_thread, max_leaves, launch, residency;
-  int32_t nchain, rank_stash;
+  int32_t nchain, rank_stash, stash_chunks, lds_resid_chunks;
 } bart_launch;
 
 /* Bytes of device workspace bart_init needs for cfg (0 if cfg is invalid). */

@@ -54,7 +54,8 @@ class LaunchInfo(C.Structure):
     _fields_ = [("grid", C.c_int32), ("block", C.c_int32), ("chunks_per_thread", C.c_int32),
                 ("lds_bytes", C.c_int32), ("obs_per_thread", C.c_int32),
                 ("max_leaves", C.c_int32), ("launch", C.c_int32), ("residency", C.c_int32),
-                ("nchain", C.c_int32), ("rank_stash", C.c_int32)]
+                ("nchain", C.c_int32), ("rank_stash", C.c_int32),
+                ("stash_chunks", C.c_int32), ("lds_resid_chunks", C.c_int32)]
 
 
 # bart_trace, 4224 bytes (include/bart.h)

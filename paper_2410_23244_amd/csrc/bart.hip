@@ -941,6 +941,8 @@ int bart_launch_info(const bart_handle *h, bart_launch *o) {
   o->launch = h->cfg.launch;
   o->nchain = h->nchain;
   o->rank_stash = h->streamed && h->V <= kStashCpt ? 1 : 0;
+  o->stash_chunks = kStashCpt;
+  o->lds_resid_chunks = o->rank_stash ? resid_lds_chunks(h->V) : 0;
   return BART_OK;
 }
 

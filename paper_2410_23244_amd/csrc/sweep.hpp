@@ -94,12 +94,21 @@ constexpr int kRing = 4;  // proposal contexts in flight: decide j, route j+1, r
 // Ranks per pass of the streamed kernel's LDS bins, one bin per lane and chunk
 // position (16).
 constexpr int kSlotRanks = kBinFloats / (4 * kBlock);
-// The streamed kernel with a rank stash: bins for half as many ranks per pass,
-// and the other half of the bin array holds one 32-bit word (the ranks of a
-// chunk's 4 points) per chunk of every thread.
+// The streamed kernel with a rank stash: bins for 8 ranks per pass, one per
+// lane and kStashPos chunk positions; after them one 32-bit word per chunk of
+// every thread (the ranks of the chunk's 4 points), and in what remains of
+// the bin array the residuals of a thread's first chunks for the launch.
 constexpr int kStashRanks = kSlotRanks / 2;                       // 8
-constexpr int kStashOffset = kStashRanks * 4 * kBlock;            // floats of bins before it
-constexpr int kStashCpt = (kBinFloats - kStashOffset) / kBlock;  // chunks per thread it holds (32)
+constexpr int kStashPos = 2;  // n = 1e7: 1 position 211, 2 214.5, 4 207 sweeps/s
+constexpr int kStashOffset = kStashRanks * kStashPos * kBlock;    // floats of bins before it
+constexpr int kStashCpt = (kBinFloats - kStashOffset) / kBlock;  // chunks per thread it holds (48)
+// chunks per thread (of cpt) whose residuals stay in LDS with the stash
+__host__ __device__ constexpr int resid_lds_chunks(int cpt) {
+  return cpt > kStashCpt ? 0
+                         : (kBinFloats - kStashOffset - cpt * kBlock) / (4 * kBlock) < cpt
+                               ? (kBinFloats - kStashOffset - cpt * kBlock) / (4 * kBlock)
+                               : cpt;
+}
 static_assert(kMaxLeaves % kSlotRanks == 0 && kMaxLeaves % kStashRanks == 0,
               "the null rank must fall outside every bin pass");
 
@@ -227,7 +236,7 @@ struct TreeData {
 };
 
 struct Shared {
-  float bins[kBinFloats];
+  alignas(16) float bins[kBinFloats];
   Ctx ctx[kRing];
   TreeData td[2];
   double red[kMaxLeaves + 1];  // this workgroup's partial sums of the tree to post next
@@ -1386,12 +1395,23 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   // flight (n = 1e7: one chunk 183, two 194, three 180 sweeps/s)
   constexpr int U = (CF || ST) ? 2 : 1;
   constexpr int kPassRanks = ST ? kStashRanks : kSlotRanks;
+  constexpr int kPos = ST ? kStashPos : 4;  // bins per lane and rank: chunk positions
   constexpr uint32_t kNull4 = kNullRank * 0x01010101u;  // a chunk of padding points
-  uint32_t *const stash = (uint32_t *)(sh.bins + kStashOffset);  // [kStashCpt][kBlock]
+  uint32_t *const stash = (uint32_t *)(sh.bins + kStashOffset);  // [cpt][kBlock]
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6, w = wg_id(A);
   const int m = A->m, cpt = A->cpt;
   const uint64_t seed = Lc.seed;
-  for (int k = t; k < kBinFloats; k += kBlock) sh.bins[k] = 0.f;
+  // with the stash, the residuals of this thread's chunks 0..rc-1 stay in
+  // LDS for the launch ([rc][kBlock] chunks after the stash; only this thread
+  // touches its own), read from HBM here and written back at the end
+  const int rc = ST ? resid_lds_chunks(cpt) : 0;
+  f32x4 *const rcache = (f32x4 *)(sh.bins + kStashOffset + cpt * kBlock);
+  for (int k = t; k < (ST ? kStashOffset + cpt * kBlock : kBinFloats); k += kBlock) sh.bins[k] = 0.f;
+  for (int i = 0; i < rc; ++i) {
+    const int32_t ch = (w * cpt + i) * kBlock + t;
+    rcache[i * kBlock + t] =
+        ch < A->chunks ? gbl((const f32x4 *)A->resid)[ch] : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
   if (t == 0) {
     sh.abort_flag = 0;
     sh.dev_err = 0;
@@ -1472,6 +1492,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     // loop keeps the next two batches' loads in flight while one is computed
     struct Batch {
       int32_t ch[U], sl[U];  // chunk, and its stash word (-1: none)
+      bool inl[U];           // the chunk's residuals are in LDS
       uint32_t ok[U];
       f32x4 rv[U];
       ChunkT ra[U], rn[U];
@@ -1491,11 +1512,12 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       for (int u = 0; u < U; ++u) {
         B.ch[u] = (w * cpt + i0 + u) * kBlock + t;
         B.sl[u] = i0 + u < cpt ? (i0 + u) * kBlock + t : -1;
+        B.inl[u] = i0 + u < rc;
         const bool valid = i0 + u < cpt && B.ch[u] < A->chunks;
         const int32_t rem = A->n - 4 * B.ch[u];
         B.ok[u] = !valid ? 0u : (rem >= 4 ? 15u : ((1u << rem) - 1u));
         cu[u] = valid ? B.ch[u] : 0;
-        B.rv[u] = res[cu[u]];
+        B.rv[u] = res[B.inl[u] ? 0 : cu[u]];  // in LDS: chunk 0 stands in
       }
       // with the stash, tree ja's ranks come from LDS: no loads of its rows
       if (!ST) {
@@ -1517,6 +1539,9 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       ChunkT (&rn)[U] = B.rn;
       uint32_t (&xa4)[U] = B.xa4;
       uint32_t (&xn4)[U] = B.xn4;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (B.inl[u]) rv[u] = rcache[B.sl[u]];
 #pragma unroll
       for (int u = 0; u < U; ++u)
         if (!ok[u]) {
@@ -1670,7 +1695,10 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
             touch |= pair;
             if (changed) out = IC::put(out, b, (merged && pair) ? eta_a : (int)ca.heap_of[rnk]);
           }
-          if (ok[u]) res[ch[u]] = rv[u];
+          if (B.inl[u])
+            rcache[B.sl[u]] = rv[u];
+          else if (ok[u])
+            res[ch[u]] = rv[u];
           if (!CF && changed && touch && ok[u]) rowa[ch[u]] = out;
         }
         if (want_ssr) {
@@ -1692,19 +1720,24 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
             rk = ranks4(cn, rn[u], xn4[u], nr, bad);
             if (ST && B.sl[u] >= 0) stash[B.sl[u]] = rk;  // after the read above
           }
-          int q[4];
-          float add[4], cur[4];
+          // points b0..b0+kPos-1 go to kPos different bins, read together
+          // and written together
 #pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            const int rl = (int)((rk >> (8 * b)) & 0xff) - lo;
-            const bool in = rl >= 0 && rl < kPassRanks;
-            q[b] = ((((in ? rl : 0) * 4 + b) * kWaves + wave) << 6) | lane;
-            add[b] = in ? rv[u][b] : 0.f;
+          for (int b0 = 0; b0 < 4; b0 += kPos) {
+            int q[kPos];
+            float add[kPos], cur[kPos];
+#pragma unroll
+            for (int e = 0; e < kPos; ++e) {
+              const int rl = (int)((rk >> (8 * (b0 + e))) & 0xff) - lo;
+              const bool in = rl >= 0 && rl < kPassRanks;
+              q[e] = ((((in ? rl : 0) * kPos + e) * kWaves + wave) << 6) | lane;
+              add[e] = in ? rv[u][b0 + e] : 0.f;
+            }
+#pragma unroll
+            for (int e = 0; e < kPos; ++e) cur[e] = sh.bins[q[e]];
+#pragma unroll
+            for (int e = 0; e < kPos; ++e) sh.bins[q[e]] = cur[e] + add[e];
           }
-#pragma unroll
-          for (int b = 0; b < 4; ++b) cur[b] = sh.bins[q[b]];
-#pragma unroll
-          for (int b = 0; b < 4; ++b) sh.bins[q[b]] = cur[b] + add[b];
         }
       }
     };
@@ -1737,8 +1770,8 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
 #pragma unroll
         for (int u = 0; u < kWaves; ++u)
 #pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            const int q = ((((k - lo) * 4 + b) * kWaves + u) << 6) | lane;
+          for (int b = 0; b < kPos; ++b) {
+            const int q = ((((k - lo) * kPos + b) * kWaves + u) << 6) | lane;
             a += (double)sh.bins[q];
             sh.bins[q] = 0.f;
           }
@@ -1843,7 +1876,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
         for (int u = 0; u < kTouch; ++u) {
           const int32_t ch = (w * cpt + u) * kBlock + t;
           const int32_t cu = (u < cpt && ch < A->chunks) ? ch : 0;
-          touch[u][0] = rw[4 * (int64_t)cu];
+          touch[u][0] = rw[4 * (int64_t)(u < rc ? 0 : cu)];
           touch[u][1] = nw[IB * (int64_t)cu];
           touch[u][2] = xw[xg ? cu : 0];
         }
@@ -1884,16 +1917,23 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           if (ch >= A->chunks) break;
           const int32_t rem = A->n - 4 * ch;
           const uint32_t ok = rem >= 4 ? 15u : ((1u << rem) - 1u);
-          const f32x4 rv = res[ch];
+          const f32x4 rv = i0 < rc ? rcache[i0 * kBlock + t] : res[ch];
           float r4[4] = {rv[0], rv[1], rv[2], rv[3]};
           latent_chunk(A, seed, s, ch, ok, r4);
-          res[ch] = f32x4{r4[0], r4[1], r4[2], r4[3]};
+          if (i0 < rc)
+            rcache[i0 * kBlock + t] = f32x4{r4[0], r4[1], r4[2], r4[3]};
+          else
+            res[ch] = f32x4{r4[0], r4[1], r4[2], r4[3]};
         }
       }
       j = 0;
       ++s;
       if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s);
     }
+  }
+  for (int i = 0; i < rc; ++i) {
+    const int32_t ch = (w * cpt + i) * kBlock + t;
+    if (ch < A->chunks) gbl((f32x4 *)A->resid)[ch] = rcache[i * kBlock + t];
   }
   if (w == 0 && t == kBlock - 1 && uncounted >= 0)
     count_move(sh, sh.ctx[uncounted & (kRing - 1)]);

@@ -320,16 +320,34 @@ def test_register_residency_at_its_maximum(extra):
     assert rep.moves > 0
 
 
-@pytest.mark.parametrize("n,stash", [(65536, 1), (65537, 0)])
-def test_streamed_at_the_stash_capacity(n, stash):
-    """One workgroup with exactly 32 chunks of 4 points per thread (every
-    word of the LDS rank stash in use) and with 33 (the first size past it,
-    a ragged last chunk): the kernel switches between its two passes there."""
+@functools.lru_cache(maxsize=None)
+def _stash_chunks():
+    """Chunks of 4 points per thread the streamed kernel's LDS stash holds."""
+    g = _gpu(make_inputs(2, n=1000, p=5, m=2), launch=ORDINARY, residency=STREAM)
+    return g.launch_info().stash_chunks
+
+
+@pytest.mark.parametrize("where", ["mixed", "full", "past"])
+def test_streamed_at_the_stash_capacity(where):
+    """One workgroup with 30 chunks of 4 points per thread (the stash in use,
+    the residuals of the first few chunks in LDS and of the rest in HBM),
+    with exactly as many chunks as the stash holds (every stash word in use)
+    and with one more (the first size past it, a ragged last chunk): the
+    kernel switches between its two passes there."""
+    cap = _stash_chunks()
+    cpt = {"mixed": 30, "full": cap, "past": cap + 1}[where]
+    n = 2048 * cpt - (0 if where == "full" else 3)
     inp = make_inputs(4, n=n, p=12, m=16)
     g = _gpu(inp, grid=1, launch=ORDINARY, residency=STREAM)
     info = g.launch_info()
-    print(f"n={n}: chunks/thread={info.chunks_per_thread} rank_stash={info.rank_stash}", flush=True)
-    assert info.rank_stash == stash and info.chunks_per_thread == 32 + (1 - stash)
+    print(f"{where}: n={n} chunks/thread={info.chunks_per_thread} rank_stash={info.rank_stash} "
+          f"lds_resid_chunks={info.lds_resid_chunks}", flush=True)
+    assert info.chunks_per_thread == cpt
+    assert info.rank_stash == (0 if where == "past" else 1)
+    if where == "mixed":
+        assert 0 < info.lds_resid_chunks < cpt
+    if where == "past":
+        assert info.lds_resid_chunks == 0
     rep = parity.lockstep(inp, g, seed=inp.seed + 11, warm_sweeps=2, n_steps=inp.m + 1 + 9)
     print(f"  {rep}", flush=True)
     assert rep.moves > 0
@@ -338,20 +356,23 @@ def test_streamed_at_the_stash_capacity(n, stash):
 @pytest.mark.parametrize("shape", ["u8", "u16", "d6_32_leaves", "no_index_cache"])
 def test_streamed_without_the_rank_stash(shape):
     """More chunks per thread than the LDS rank stash holds (one workgroup,
-    n = 70001: 35 chunks of 4 points per thread): the streamed kernel reads
-    each tree's rows again in the pass that applies it.  Small trees, u8 and
-    u16 caches, 32-leaf trees (two bin passes) and no index cache."""
+    three chunks of 4 points per thread more than the stash, ragged): the
+    streamed kernel reads each tree's rows again in the pass that applies it.
+    Small trees, u8 and u16 caches, 32-leaf trees (two bin passes) and no
+    index cache."""
+    n = 2048 * (_stash_chunks() + 3) - 5
     if shape == "u16":
-        inp = make_inputs(4, n=70001, p=12, m=16)
+        inp = make_inputs(4, n=n, p=12, m=16)
     elif shape == "no_index_cache":
-        inp = make_inputs(2, n=70001, p=12, m=16, idx_bytes=0)
+        inp = make_inputs(2, n=n, p=12, m=16, idx_bytes=0)
     else:
-        inp = make_inputs(2, n=70001, p=12, m=12 if shape == "d6_32_leaves" else 16)
+        inp = make_inputs(2, n=n, p=12, m=12 if shape == "d6_32_leaves" else 16)
     g = _gpu(inp, grid=1, launch=ORDINARY, residency=STREAM)
     info = g.launch_info()
     print(f"{shape}: grid={info.grid} chunks/thread={info.chunks_per_thread} "
           f"rank_stash={info.rank_stash}", flush=True)
-    assert info.residency == STREAM and info.rank_stash == 0 and info.chunks_per_thread > 32
+    assert info.residency == STREAM and info.rank_stash == 0
+    assert info.chunks_per_thread > info.stash_chunks
     if shape == "d6_32_leaves":
         g.set_state(_full_trees(inp, 5, np.random.default_rng(7)))
         rep = parity.lockstep(inp, g, seed=5, warm_sweeps=0, n_steps=2 * (inp.m + 1))
