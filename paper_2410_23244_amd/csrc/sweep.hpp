@@ -1379,7 +1379,10 @@ __global__ void __launch_bounds__(kBlock) sweep_kernel(const SweepArgs *__restri
 // of step j+1 that applies the tree: that pass then reads neither the index
 // row nor the predictor row again (nor, without an index cache, a rolling
 // row of leaves), and trees with more leaves than one bin pass holds take
-// their extra passes from the stash too.
+// their extra passes from the stash too.  The LDS left after the bins and the
+// stash holds the residuals of each thread's first chunks for the launch
+// (resid_lds_chunks), so only the other chunks' residuals cross HBM every
+// step.
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <int IB, bool CF, bool ST>
