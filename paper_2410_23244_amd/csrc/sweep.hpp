@@ -1434,9 +1434,10 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   // rank, whose delta is 0 and which falls in no bin; any other non-leaf
   // slot is an inconsistent cache, rank kBadRank (likewise inert), and bad
   // keeps the largest rank seen so the pass can flag it.
-  auto ranks4 = [&](const Ctx &c, ChunkT rc, uint32_t rx, int &nr, uint32_t &bad) -> uint32_t {
-    const int move = c.pr.move, eta = c.pr.eta, cutv = c.pr.cut;
-    const int grow_eta = move == kGrow ? eta : -1;
+  // (grow_eta: eta of a GROW, -1 otherwise; eta and cut of the proposal,
+  // read once per pass by the caller)
+  auto ranks4 = [&](const Ctx &c, int grow_eta, int eta, int cutv, ChunkT rc, uint32_t rx, int &nr,
+                    uint32_t &bad) -> uint32_t {
     uint32_t pk = 0;
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
@@ -1467,6 +1468,14 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     // deltas), so the predictor row that tells them apart is read only when
     // the GROW is accepted
     const bool xa = do_a && ca.pr.move == kGrow && acc, xn = do_n && cn.pr.move == kGrow;
+    // the proposals' fields the per-chunk routes use, out of LDS once per pass
+    // (read per chunk, each was a dependent LDS round trip, and its wait also
+    // waited for the chunk's outstanding bin writes: n = 1e7, 215 -> 248
+    // sweeps/s)
+    const int eta_n = cn.pr.eta, cut_n = cn.pr.cut, grow_n = xn ? eta_n : -1;
+    const int cut_a = ca.pr.cut, grow_a = do_a && ca.pr.move == kGrow ? eta_a : -1;
+    const int n_obs = A->n;
+    const uint32_t n_chunks = (uint32_t)A->chunks;
     // ranks of tree jn: computed from its rows by the first bin pass, read
     // back from the stash by the others
     const bool fresh = do_n && (!ST || lo == 0);
@@ -1494,7 +1503,8 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     // a batch of U chunks per thread: its loads, then its arithmetic; the
     // loop keeps the next two batches' loads in flight while one is computed
     struct Batch {
-      int32_t ch[U], sl[U];  // chunk, and its stash word (-1: none)
+      uint32_t ch[U];        // chunk (unsigned: a 32-bit offset from a uniform base)
+      int32_t sl[U];         // its stash word (-1: none)
       bool inl[U];           // the chunk's residuals are in LDS
       uint32_t ok[U];
       f32x4 rv[U];
@@ -1510,16 +1520,16 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     // its points are padding like those of a partial chunk (index entry 0,
     // residual 0)
     auto load_batch = [&](int i0, Batch &B) {
-      int32_t cu[U];
+      uint32_t cu[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        B.ch[u] = (w * cpt + i0 + u) * kBlock + t;
+        B.ch[u] = (uint32_t)((w * cpt + i0 + u) * kBlock + t);
         B.sl[u] = i0 + u < cpt ? (i0 + u) * kBlock + t : -1;
         B.inl[u] = i0 + u < rc;
-        const bool valid = i0 + u < cpt && B.ch[u] < A->chunks;
-        const int32_t rem = A->n - 4 * B.ch[u];
+        const bool valid = i0 + u < cpt && B.ch[u] < n_chunks;
+        const int32_t rem = n_obs - 4 * (int32_t)B.ch[u];
         B.ok[u] = !valid ? 0u : (rem >= 4 ? 15u : ((1u << rem) - 1u));
-        cu[u] = valid ? B.ch[u] : 0;
+        cu[u] = valid ? B.ch[u] : 0u;
         B.rv[u] = res[B.inl[u] ? 0 : cu[u]];  // in LDS: chunk 0 stands in
       }
       // with the stash, tree ja's ranks come from LDS: no loads of its rows
@@ -1535,7 +1545,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       for (int u = 0; u < U; ++u) B.xn4[u] = xrn[xn && fresh ? cu[u] : 0];
     };
     auto compute_batch = [&](Batch &B) {
-      int32_t (&ch)[U] = B.ch;
+      uint32_t (&ch)[U] = B.ch;
       uint32_t (&ok)[U] = B.ok;
       f32x4 (&rv)[U] = B.rv;
       ChunkT (&ra)[U] = B.ra;
@@ -1573,9 +1583,9 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
         // descent needs no LDS; deeper, it is the node's index in the list
         const bool by_slot = H <= 32;
         uint64_t imask = 0;  // internal heap slots (by_slot)
-        int32_t cu[U];
+        uint32_t cu[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) cu[u] = ok[u] ? ch[u] : 0;
+        for (int u = 0; u < U; ++u) cu[u] = ok[u] ? ch[u] : 0u;
         for (int k0 = 0; k0 < ni; k0 += 8) {
           uint32_t wd[8][U];
 #pragma unroll
@@ -1684,20 +1694,23 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           if (ST)
             rk = ok[u] ? stash[B.sl[u]] : kNull4;
           else
-            rk = ranks4(ca, ra[u], xa4[u], nra, bad);
+            rk = ranks4(ca, grow_a, eta_a, cut_a, ra[u], xa4[u], nra, bad);
           float dl[4];
 #pragma unroll
           for (int b = 0; b < 4; ++b) dl[b] = sh.dlt[(rk >> (8 * b)) & 0xff];
+#pragma unroll
+          for (int b = 0; b < 4; ++b) rv[u][b] += dl[b];  // final delta of the rank
+          // the index row changes only under an accepted move
           bool touch = false;
           ChunkT out = 0;
+          if (changed)
 #pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            const int rnk = (rk >> (8 * b)) & 0xff;
-            const bool pair = (rnk == kl) || (rnk == kr);
-            rv[u][b] += dl[b];  // final delta of the rank
-            touch |= pair;
-            if (changed) out = IC::put(out, b, (merged && pair) ? eta_a : (int)ca.heap_of[rnk]);
-          }
+            for (int b = 0; b < 4; ++b) {
+              const int rnk = (rk >> (8 * b)) & 0xff;
+              const bool pair = (rnk == kl) || (rnk == kr);
+              touch |= pair;
+              out = IC::put(out, b, (merged && pair) ? eta_a : (int)ca.heap_of[rnk]);
+            }
           if (B.inl[u])
             rcache[B.sl[u]] = rv[u];
           else if (ok[u])
@@ -1720,7 +1733,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           if (ST && lo > 0) {
             rk = ok[u] ? stash[B.sl[u]] : kNull4;
           } else {
-            rk = ranks4(cn, rn[u], xn4[u], nr, bad);
+            rk = ranks4(cn, grow_n, eta_n, cut_n, rn[u], xn4[u], nr, bad);
             if (ST && B.sl[u] >= 0) stash[B.sl[u]] = rk;  // after the read above
           }
           // points b0..b0+kPos-1 go to kPos different bins, read together
