@@ -217,6 +217,9 @@ struct Ctx {
 
 // Without an index cache: the internal nodes of a tree snapshot, by ring slot.
 struct NodeList {
+  uint64_t imask;            // internal heap slots below 64
+  uint16_t axis8[8];         // axis and cut of the first 8 internal nodes
+  uint8_t cut8[8];
   uint8_t nidx[kMaxLeaves];  // heap slot -> index among the internal nodes (kNoNode: none)
   uint8_t nh[kMaxLeaves];    // heap slot of the k-th internal node, in heap order
   int32_t ni;                // internal nodes
@@ -331,6 +334,11 @@ __device__ __forceinline__ void build_inodes(const SweepArgs *__restrict__ A, co
                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
     if (h < H) nl.nidx[h] = in ? (uint8_t)k : (uint8_t)kNoNode;
     if (in) nl.nh[k] = (uint8_t)h;
+    if (in && k < 8) {
+      nl.axis8[k] = c.ax[h];
+      nl.cut8[k] = c.ct[h];
+    }
+    if (h0 == 0 && lane == 0) nl.imask = bal;
     base += __popcll(bal);
   }
   if (lane == 0) nl.ni = base;
@@ -1490,6 +1498,26 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     const gptr<ChunkT> rowa = row_of(do_a ? ja : 0);
     const gptr<ChunkT> rown = row_of(do_n ? jn : 0);
     const bool trav = CF && do_n && lo == 0;  // Algorithm 1 for tree jn
+    const NodeList &nn = sh.nl[(jn < 0 ? 0 : jn) & (kRing - 1)];
+    // without an index cache: tree jn's internal-node count, its mask of
+    // internal heap slots and its first 8 nodes (predictor-row offset, cut,
+    // heap slot), out of LDS once per pass rather than per batch
+    const int ni_p = trav ? nn.ni : 0;
+    uint64_t imask_p = 0;
+    int64_t xoff8[8];
+    int cut8[8], slot8[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) xoff8[k] = 0, cut8[k] = 256, slot8[k] = 0;
+    if (CF && trav && ni_p <= 32) {
+      imask_p = nn.imask;
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (k < ni_p) {
+          slot8[k] = nn.nh[k];
+          cut8[k] = nn.cut8[k];
+          xoff8[k] = (int64_t)nn.axis8[k] * A->ldx;
+        }
+    }
     // a tree's axis is read only when it takes part (a ring slot may not
     // hold a proposal yet); every proposal's axis is a valid row
     const gptr<const uint32_t> xra =
@@ -1562,8 +1590,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           rn[u] = (ChunkT)0;
           rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-      const NodeList &nn = sh.nl[(jn < 0 ? 0 : jn) & (kRing - 1)];
-      if (trav && nn.ni <= 32) {
+      if (trav && ni_p <= 32) {
         // leaves of tree jn by Algorithm 1 on its structure snapshot: the
         // decision of every internal node for the chunk's 4 points, from one
         // coalesced word of the node's predictor row (the words of up to 8
@@ -1577,12 +1604,12 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
         for (int u = 0; u < U; ++u)
 #pragma unroll
           for (int b = 0; b < 4; ++b) bits[u][b] = 0u;
-        const int ni = nn.ni;
+        const int ni = ni_p;
         const int H = A->H;
         // up to depth 6 the bit of a decision is its heap slot, and the
         // descent needs no LDS; deeper, it is the node's index in the list
         const bool by_slot = H <= 32;
-        uint64_t imask = 0;  // internal heap slots (by_slot)
+        const uint64_t imask = imask_p;  // internal heap slots (by_slot)
         uint32_t cu[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) cu[u] = ok[u] ? ch[u] : 0u;
@@ -1593,8 +1620,8 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
 #pragma unroll
             for (int u = 0; u < U; ++u) wd[e][u] = 0u;
             if (k0 + e < ni) {
-              const gptr<const uint32_t> xr =
-                  gbl((const uint32_t *)(A->X + (int64_t)cn.ax[nn.nh[k0 + e]] * A->ldx));
+              const int64_t off = k0 == 0 ? xoff8[e] : (int64_t)cn.ax[nn.nh[k0 + e]] * A->ldx;
+              const gptr<const uint32_t> xr = gbl((const uint32_t *)(A->X + off));
 #pragma unroll
               for (int u = 0; u < U; ++u) wd[e][u] = xr[cu[u]];
             }
@@ -1602,10 +1629,10 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const int k = k0 + e;
-            const int hk = k < ni ? (int)nn.nh[k] : 0;
-            const int cv = k < ni ? (int)cn.ct[hk] : 256;  // no bit past the last node
+            const int hk = k0 == 0 ? slot8[e] : (k < ni ? (int)nn.nh[k] : 0);
+            // no bit past the last node
+            const int cv = k0 == 0 ? cut8[e] : (k < ni ? (int)cn.ct[hk] : 256);
             const int pos = by_slot ? hk : (k & 31);
-            if (k < ni) imask |= 1ull << hk;
 #pragma unroll
             for (int u = 0; u < U; ++u)
 #pragma unroll
