@@ -12,7 +12,7 @@ synchronisations.  Prints one JSON line.
 --chains C runs C independent chains in the same launches (multi-chain
 batching); value is then the chain-sweeps per second summed over the chains
 and the roofline counts every chain's bytes.  The single-chain headline run
-also times 4 chains batched on the same workload after its own measurement
+also times 16 chains batched on the same workload after its own measurement
 and reports them in a separate 'batched' object (--batched sets the count,
 0 turns it off); value stays the single chain's.
 
@@ -217,7 +217,7 @@ def make_parser() -> argparse.ArgumentParser:
     ap.add_argument("--batched", type=int, default=-1, metavar="C",
                     help="after the main line's measurement, also time C chains batched in the "
                          "same launches on the same workload and report them under 'batched' "
-                         "(-1: 4 for the single-chain headline workload, else off; 0: off)")
+                         "(-1: 16 for the single-chain headline workload, else off; 0: off)")
     ap.add_argument("--grid", type=int, default=0, help="workgroups per chain (0 = automatic)")
     ap.add_argument("--no-index-cache", action="store_true",
                     help="run without the [ntree][n] index cache (Algorithm 1 every tree step)")
@@ -316,7 +316,7 @@ def main() -> int:
 
     batched = None
     nb = args.batched if args.batched >= 0 else (
-        4 if args.config == 3 and C == 1 and args.grid == 0 and not args.no_index_cache else 0)
+        16 if args.config == 3 and C == 1 and args.grid == 0 and not args.no_index_cache else 0)
     if nb > 1:
         # the same workload with nb chains in the same launches: chain-sweeps
         # per second summed over the chains, timed like the main line
@@ -341,6 +341,8 @@ def main() -> int:
         batched = {"chains": nb, "value": nb * sweeps_b / (msb / 1e3), "unit": "chain-sweeps/s",
                    "steps": sweeps_b, "ms_per_step": msb / sweeps_b, "grid_per_chain": ib.grid,
                    "chunks_per_thread": ib.chunks_per_thread,
+                   "residency": "streamed" if ib.residency == 2 else "registers",
+                   "lds_resid_chunks": ib.lds_resid_chunks,
                    "roofline_achieved_gbs": achb, "roofline_frac": achb / HBM_PEAK_GBS}
         print(f"[bench] {nb} chains batched: {batched['value']:.1f} chain-sweeps/s",
               file=sys.stderr, flush=True)

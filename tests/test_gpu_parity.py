@@ -432,19 +432,21 @@ def test_chains_lockstep(nchain, grid, residency, launch):
     assert not np.array_equal(states[0]["leaf"], states[1]["leaf"])
 
 
-@pytest.mark.parametrize("nchain,chunks", [(2, 4), (4, 8)])
-def test_chains_full_size_lockstep(nchain, chunks):
-    """Workload 3 at full size with 2 and 4 chains in the ordinary launch: the
-    4-chain shape is the one bench.py's batched leg times (62 workgroups per
-    chain, 8 chunks of 4 points per thread), the 2-chain one takes 4 chunks.
+@pytest.mark.parametrize("nchain,chunks,residency", [(2, 4, REGS), (4, 8, REGS), (16, 31, STREAM)])
+def test_chains_full_size_lockstep(nchain, chunks, residency):
+    """Workload 3 at full size with 2, 4 and 16 chains in the ordinary launch:
+    2 and 4 chains keep their residuals in registers (4 and 8 chunks of 4
+    points per thread); 16 chains of 16 workgroups stream them (31 chunks per
+    thread, the first 4 in LDS): the shape bench.py's batched leg times.
     After untraced sweeps every chain's state meets the cache invariants, then
     every chain runs a whole sweep in lockstep with its oracle stream."""
     inp = _full(3)
     g = _gpu(inp, launch=ORDINARY, nchain=nchain)
     info = g.launch_info()
     print(f"workload 3, {nchain} chains: grid {info.grid} x {nchain}, {info.chunks_per_thread} "
-          f"chunks per thread", flush=True)
+          f"chunks per thread, residency {info.residency}", flush=True)
     assert info.nchain == nchain and info.chunks_per_thread == chunks
+    assert info.residency == residency
     g.step(10, inp.seed)
     assert g.status() == 0
     for c in range(nchain):
