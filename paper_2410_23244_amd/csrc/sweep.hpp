@@ -1462,10 +1462,13 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   };
 
   // one pass: apply tree ja (-1: none), accumulate the ranks [lo, lo +
-  // kPassRanks) of tree jn (-1: none) into sh.red (private fp32 bins per lane
-  // and chunk position, then a fixed-order fp64 reduction), sum of squares
-  // into sh.wave_part if want_ssr.  Ends with an LDS barrier.
-  auto pass = [&](int ja, int jn, bool want_ssr, int lo) {
+  // kPassRanks) of tree jn (-1: none) in private fp32 bins per lane and chunk
+  // position, then reduce each in a fixed order in fp64, the wave that forms
+  // a total posting it as word k of this workgroup's mailbox (buffer ppar,
+  // step number pseq: the step that decides jn), and the sum of squares into
+  // sh.wave_part if want_ssr.  The bins are cleared as they are read; an LDS
+  // barrier separates the bin updates from the reduction.
+  auto pass = [&](int ja, int jn, bool want_ssr, int lo, int ppar, uint32_t pseq) {
     const Ctx &ca = sh.ctx[(ja < 0 ? 0 : ja) & (kRing - 1)];
     const Ctx &cn = sh.ctx[(jn < 0 ? 0 : jn) & (kRing - 1)];
     const bool do_a = ja >= 0, do_n = jn >= 0;
@@ -1807,6 +1810,12 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       if (lane == 63) sh.wave_part[wave] = tot;
     }
     lds_barrier();
+    if (do_n && lo == 0 && t == kBlock - 1) {
+      // the GROW right-count of tree jn, complete after the barrier, as the
+      // last word of this workgroup's mailbox for the step that decides jn
+      post(A, sh, ppar, Ln, mk_word(pseq, (uint64_t)sh.nr[jn & 1]));
+      sh.nr[jn & 1] = 0;
+    }
     if (do_n) {
       for (int k = lo + wave; k < min(Ln, lo + kPassRanks); k += kWaves) {
         double a = 0.0;
@@ -1819,19 +1828,23 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
             sh.bins[q] = 0.f;
           }
         const double tot = wave_total63(a);
-        if (lane == 63) sh.red[k] = tot;
+        // the wave that forms a total posts it
+        if (lane == 63) post(A, sh, ppar, k, mk_word(pseq, pack_f64(tot)));
       }
-      lds_barrier();
     }
   };
   // all partial sums of tree jn: trees with more leaves than one bin pass
   // holds take extra accumulate-only passes over the data
-  auto pass_all = [&](int ja, int jn, bool want_ssr) {
-    pass(ja, jn, want_ssr, 0);
+  // (ppar, pseq: mailbox buffer and step number of the step that decides jn;
+  // a pass that follows another waits for its bins to be cleared)
+  auto pass_all = [&](int ja, int jn, bool want_ssr, int ppar, uint32_t pseq) {
+    pass(ja, jn, want_ssr, 0, ppar, pseq);
     const int Ln = jn >= 0 ? sh.ctx[jn & (kRing - 1)].pr.L : 0;
-    for (int lo = kPassRanks; lo < Ln; lo += kPassRanks) pass(-1, jn, false, lo);
+    for (int lo = kPassRanks; lo < Ln; lo += kPassRanks) {
+      lds_barrier();
+      pass(-1, jn, false, lo, ppar, pseq);
+    }
   };
-  auto partial = [&](int, int k) { return sh.red[k]; };
   // axis and cut of one heap slot of tree j (thread t < H), packed
   auto struct_word = [&](int tree) -> uint32_t {
     const int H = A->H, h = t < H ? t : 0;
@@ -1846,7 +1859,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   };
   // proposals of trees j0..j0+2, their rank tables (and structures, without
   // an index cache), the decision data of j0 and tree j0's partial sums
-  auto refill = [&](int j0, int64_t s) {
+  auto refill = [&](int j0, int64_t s, int ppar, uint32_t pseq) {
     for (int q = 0; q < 3; ++q)
       if (j0 + q < m) {
         const uint32_t wd = load_prop_word(A, j0 + q);
@@ -1862,7 +1875,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     lds_barrier();
     const TdRegs tr0 = load_tree_data(A, sh.ctx[j0 & (kRing - 1)], j0, s);
     store_tree_data(sh.td[j0 & 1], sh.ctx[j0 & (kRing - 1)], tr0);
-    pass_all(-1, j0, false);
+    pass_all(-1, j0, false, ppar, pseq);
   };
 
   // ---- prologue
@@ -1879,7 +1892,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   // wave); the barrier orders the other waves after it
   if (t >= kBlock - 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __syncthreads();
-  if (j < m && !sh.abort_flag) refill(j, s);
+  if (j < m && !sh.abort_flag) refill(j, s, 0, 2u);
   bool have_ssr = false;
 
 #pragma unroll 1
@@ -1892,10 +1905,6 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       const int L = c.pr.L;
       const bool more1 = (j + 1 < m) && (step + 1 < Lc.n_steps);
       const bool more3 = more1 && (j + 3 < m);
-      if (t <= L) {
-        const uint64_t pay = t < L ? pack_f64(partial(L, t)) : (uint64_t)sh.nr[j & 1];
-        post(A, sh, par, t, mk_word(seq, pay));
-      }
       const int j1 = more1 ? j + 1 : j, j3 = more3 ? j + 3 : j;
       const TdRegs tdn = load_tree_data(A, sh.ctx[j1 & (kRing - 1)], j1, s);
       const uint32_t pw3 = load_prop_word(A, j3);
@@ -1924,8 +1933,6 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           touch[u][2] = xw[xg ? cu : 0];
         }
       }
-      // the poster of the count word clears it (see the register kernel)
-      if (t == L) sh.nr[j & 1] = 0;
       pre_decide(A, sh, c, sh.td[j & 1], w == 0 ? uncounted : -1);
       const int nseg = gather_polls(A, sh, par, seq, L + 1, L, Lc.spin_limit);
       // the touched words are discarded; issued before the polls, they have
@@ -1943,14 +1950,14 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       if (more3) build_ranks(A, sh.ctx[(j + 3) & (kRing - 1)]);
       if (CF && more3) build_inodes(A, sh.ctx[(j + 3) & (kRing - 1)], sh.nl[(j + 3) & (kRing - 1)]);
       have_ssr = j == m - 1;
-      pass_all(j, more1 ? j + 1 : -1, have_ssr);
+      pass_all(j, more1 ? j + 1 : -1, have_ssr, (step + 1) & 1, (uint32_t)step + 3);
       ++j;
     } else {
       if (w == 0 && t == kBlock - 1 && uncounted >= 0)
         count_move(sh, sh.ctx[uncounted & (kRing - 1)]);
       uncounted = -1;
       __syncthreads();
-      if (!have_ssr) pass(-1, -1, true, 0);
+      if (!have_ssr) pass(-1, -1, true, 0, 0, 0u);
       have_ssr = false;
       sigma2_tail(A, Lc, sh, s, step, seq, par);
       if (A->probit) {
@@ -1971,7 +1978,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       }
       j = 0;
       ++s;
-      if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s);
+      if (step + 1 < Lc.n_steps && !sh.abort_flag) refill(0, s, (step + 1) & 1, (uint32_t)step + 3);
     }
   }
   for (int i = 0; i < rc; ++i) {
