@@ -242,7 +242,6 @@ struct Shared {
   alignas(16) float bins[kBinFloats];
   Ctx ctx[kRing];
   TreeData td[2];
-  double red[kMaxLeaves + 1];  // this workgroup's partial sums of the tree to post next
   double part[kBlock];
   double tot[kMaxLeaves + 1];
   double S[kMaxLeaves];
