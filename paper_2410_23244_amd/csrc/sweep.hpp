@@ -1435,15 +1435,15 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   if (t < 6) sh.stats[t] = 0;
   int uncounted = -1;  // tree step whose move statistics workgroup 0 has yet to count
 
-  // leaf ranks in tree c's larger tree of the 4 points of a chunk; GROW
-  // right-count into nr.  Index 0 marks a padding point (its entry in the
-  // row, or a chunk past the end whose loaded values were zeroed): the null
-  // rank, whose delta is 0 and which falls in no bin; any other non-leaf
-  // slot is an inconsistent cache, rank kBadRank (likewise inert), and bad
-  // keeps the largest rank seen so the pass can flag it.
+  // leaf ranks in tree c's larger tree of the 4 points of a chunk.  Index 0
+  // marks a padding point (its entry in the row, or a chunk past the end
+  // whose loaded values were zeroed): the null rank, whose delta is 0 and
+  // which falls in no bin; any other non-leaf slot is an inconsistent cache,
+  // rank kBadRank (likewise inert), and bad keeps the largest rank seen so
+  // the pass can flag it.
   // (grow_eta: eta of a GROW, -1 otherwise; eta and cut of the proposal,
   // read once per pass by the caller)
-  auto ranks4 = [&](const Ctx &c, int grow_eta, int eta, int cutv, ChunkT rc, uint32_t rx, int &nr,
+  auto ranks4 = [&](const Ctx &c, int grow_eta, int eta, int cutv, ChunkT rc, uint32_t rx,
                     uint32_t &bad) -> uint32_t {
     uint32_t pk = 0;
 #pragma unroll
@@ -1453,11 +1453,15 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       const bool in = ci == grow_eta;
       const int right = xi >= cutv;
       const int r0 = c.rank_of[in ? 2 * eta + right : ci];  // slot below 256: eta < 128
-      nr += __popcll(__ballot(in && right));
       bad = max(bad, (uint32_t)r0);
       pk |= (uint32_t)r0 << (8 * b);
     }
     return pk;
+  };
+  // the number of bytes of x that are zero (no carry crosses a byte)
+  auto zero_bytes = [](uint32_t x) -> int {
+    const uint32_t y = (x & 0x7f7f7f7fu) + 0x7f7f7f7fu;
+    return __popc(~(y | x) & 0x80808080u);
   };
 
   // one pass: apply tree ja (-1: none), accumulate the ranks [lo, lo +
@@ -1483,6 +1487,13 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     // waited for the chunk's outstanding bin writes: n = 1e7, 215 -> 248
     // sweeps/s)
     const int eta_n = cn.pr.eta, cut_n = cn.pr.cut, grow_n = xn ? eta_n : -1;
+    // a point of a GROW's eta goes right exactly when its rank is that of
+    // the right child (every other slot has another rank), so the GROW
+    // right-count is the number of bytes of the packed ranks equal to it;
+    // without a GROW, a byte no rank takes (ranks: below kNullRank, or
+    // kBadRank)
+    static_assert(kNullRank < 254 && kBadRank != 254, "254 must be no rank");
+    const uint32_t right4 = (uint32_t)(xn ? cn.rank_of[2 * eta_n + 1] : 254) * 0x01010101u;
     const int cut_a = ca.pr.cut, grow_a = do_a && ca.pr.move == kGrow ? eta_a : -1;
     const int n_obs = A->n;
     const uint32_t n_chunks = (uint32_t)A->chunks;
@@ -1490,6 +1501,11 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     // back from the stash by the others
     const bool fresh = do_n && (!ST || lo == 0);
     const int Ln = do_n ? cn.pr.L : 0;
+    // when tree jn's ranks all fit this pass but its last slot (lo == 0,
+    // fewer leaves than the pass holds), every other rank (padding, an
+    // inconsistent cache) goes to that spare slot, which no total reads and
+    // the pass clears: no range test per point
+    const bool spare = lo == 0 && Ln < kPassRanks;
     // index rows of trees ja and jn: rows of the cache, or without one the
     // two rolling rows (by tree parity) that carry a tree's leaves from the
     // step that accumulates it to the step that applies it
@@ -1717,13 +1733,12 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        int nra = 0;
         if (do_a) {
           uint32_t rk;
           if (ST)
             rk = ok[u] ? stash[B.sl[u]] : kNull4;
           else
-            rk = ranks4(ca, grow_a, eta_a, cut_a, ra[u], xa4[u], nra, bad);
+            rk = ranks4(ca, grow_a, eta_a, cut_a, ra[u], xa4[u], bad);
           float dl[4];
 #pragma unroll
           for (int b = 0; b < 4; ++b) dl[b] = sh.dlt[(rk >> (8 * b)) & 0xff];
@@ -1762,26 +1777,44 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           if (ST && lo > 0) {
             rk = ok[u] ? stash[B.sl[u]] : kNull4;
           } else {
-            rk = ranks4(cn, grow_n, eta_n, cut_n, rn[u], xn4[u], nr, bad);
+            rk = ranks4(cn, grow_n, eta_n, cut_n, rn[u], xn4[u], bad);
             if (ST && B.sl[u] >= 0) stash[B.sl[u]] = rk;  // after the read above
+            nr += zero_bytes(rk ^ right4);
           }
           // points b0..b0+kPos-1 go to kPos different bins, read together
           // and written together
+          if (spare) {
 #pragma unroll
-          for (int b0 = 0; b0 < 4; b0 += kPos) {
-            int q[kPos];
-            float add[kPos], cur[kPos];
+            for (int b0 = 0; b0 < 4; b0 += kPos) {
+              int q[kPos];
+              float cur[kPos];
 #pragma unroll
-            for (int e = 0; e < kPos; ++e) {
-              const int rl = (int)((rk >> (8 * (b0 + e))) & 0xff) - lo;
-              const bool in = rl >= 0 && rl < kPassRanks;
-              q[e] = ((((in ? rl : 0) * kPos + e) * kWaves + wave) << 6) | lane;
-              add[e] = in ? rv[u][b0 + e] : 0.f;
+              for (int e = 0; e < kPos; ++e) {
+                const uint32_t rl = min((rk >> (8 * (b0 + e))) & 0xffu, (uint32_t)(kPassRanks - 1));
+                q[e] = ((((int)rl * kPos + e) * kWaves + wave) << 6) | lane;
+              }
+#pragma unroll
+              for (int e = 0; e < kPos; ++e) cur[e] = sh.bins[q[e]];
+#pragma unroll
+              for (int e = 0; e < kPos; ++e) sh.bins[q[e]] = cur[e] + rv[u][b0 + e];
             }
+          } else {
 #pragma unroll
-            for (int e = 0; e < kPos; ++e) cur[e] = sh.bins[q[e]];
+            for (int b0 = 0; b0 < 4; b0 += kPos) {
+              int q[kPos];
+              float add[kPos], cur[kPos];
 #pragma unroll
-            for (int e = 0; e < kPos; ++e) sh.bins[q[e]] = cur[e] + add[e];
+              for (int e = 0; e < kPos; ++e) {
+                const int rl = (int)((rk >> (8 * (b0 + e))) & 0xff) - lo;
+                const bool in = rl >= 0 && rl < kPassRanks;
+                q[e] = ((((in ? rl : 0) * kPos + e) * kWaves + wave) << 6) | lane;
+                add[e] = in ? rv[u][b0 + e] : 0.f;
+              }
+#pragma unroll
+              for (int e = 0; e < kPos; ++e) cur[e] = sh.bins[q[e]];
+#pragma unroll
+              for (int e = 0; e < kPos; ++e) sh.bins[q[e]] = cur[e] + add[e];
+            }
           }
         }
       }
@@ -1803,7 +1836,11 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       compute_batch(B2);
     }
     if (bad == kBadRank) sh.dev_err = 1;  // bad: the largest rank seen
-    if (do_n && lo == 0 && lane == 0 && nr) atomicAdd(&sh.nr[jn & 1], nr);
+    if (do_n && lo == 0) {
+      // per-lane counts (below 2^24) summed exactly over the wave
+      const double tot = wave_total63((double)nr);
+      if (lane == 63 && tot != 0.0) atomicAdd(&sh.nr[jn & 1], (int)tot);
+    }
     if (want_ssr) {
       const double tot = wave_total63(ssr);
       if (lane == 63) sh.wave_part[wave] = tot;
@@ -1816,6 +1853,11 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       sh.nr[jn & 1] = 0;
     }
     if (do_n) {
+      if (spare && wave == (kPassRanks - 1) % kWaves)
+#pragma unroll
+        for (int u = 0; u < kWaves; ++u)
+#pragma unroll
+          for (int b = 0; b < kPos; ++b) sh.bins[((((kPassRanks - 1) * kPos + b) * kWaves + u) << 6) | lane] = 0.f;
       for (int k = lo + wave; k < min(Ln, lo + kPassRanks); k += kWaves) {
         double a = 0.0;
 #pragma unroll

@@ -278,14 +278,19 @@ NO_CACHE = -1  # streamed residuals without an index cache
 
 
 @pytest.mark.parametrize("residency", [REGS, STREAM, NO_CACHE])
-@pytest.mark.parametrize("shape", ["d6_32_leaves", "d8_128_leaves"])
+@pytest.mark.parametrize("shape", ["d3_8_leaves", "d6_32_leaves", "d8_128_leaves"])
 def test_lockstep_big_trees(shape, residency):
     """Trees far larger than the sampler grows by itself: 32 and 128 leaves
     take the LDS-bin reductions and mailboxes of up to 129 words; without an
     index cache, 31 internal nodes fill the 32-bit decision masks of the
-    descent and 127 take the level-by-level descent."""
+    descent and 127 take the level-by-level descent.  8 leaves sit at the
+    streamed pass's rank capacity (8 ranks a pass with the rank stash): a
+    PRUNE's larger tree fills one pass with no spare slot, a GROW's 9 ranks
+    take two passes, and a pruned tree's 7 leave the spare slot free."""
     kw = dict(idx_bytes=0) if residency == NO_CACHE else {}
-    if shape == "d6_32_leaves":
+    if shape == "d3_8_leaves":
+        inp, depth = make_inputs(2, n=20011, p=12, m=12, **kw), 3
+    elif shape == "d6_32_leaves":
         inp, depth = make_inputs(2, n=20011, p=12, m=12, **kw), 5
     else:
         inp, depth = make_inputs(5, n=30011, p=40, m=6, **kw), 7
