@@ -1458,6 +1458,17 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     }
     return pk;
   };
+  // the same when the move is not a GROW: every point keeps its leaf
+  auto ranks4_plain = [&](const Ctx &c, ChunkT rc, uint32_t &bad) -> uint32_t {
+    uint32_t pk = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int r0 = c.rank_of[IC::get(rc, b)];
+      bad = max(bad, (uint32_t)r0);
+      pk |= (uint32_t)r0 << (8 * b);
+    }
+    return pk;
+  };
   // the number of bytes of x that are zero (no carry crosses a byte)
   auto zero_bytes = [](uint32_t x) -> int {
     const uint32_t y = (x & 0x7f7f7f7fu) + 0x7f7f7f7fu;
@@ -1777,7 +1788,12 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           if (ST && lo > 0) {
             rk = ok[u] ? stash[B.sl[u]] : kNull4;
           } else {
-            rk = ranks4(cn, grow_n, eta_n, cut_n, rn[u], xn4[u], bad);
+            // (a uniform branch: a GROW's points of eta take a child; without
+            // an index cache, the route of every pass measured faster)
+            if (CF || xn)
+              rk = ranks4(cn, grow_n, eta_n, cut_n, rn[u], xn4[u], bad);
+            else
+              rk = ranks4_plain(cn, rn[u], bad);
             if (ST && B.sl[u] >= 0) stash[B.sl[u]] = rk;  // after the read above
             nr += zero_bytes(rk ^ right4);
           }
