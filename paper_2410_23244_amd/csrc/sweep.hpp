@@ -1047,18 +1047,29 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
     // leaf of every point in the larger tree, then all rank lookups at once
     int cp[V][4];
     int nr = 0;
+    if (grow_eta >= 0) {
 #pragma unroll
-    for (int v = 0; v < V; ++v) {
-      // a chunk past the end: index 0, the null rank, for all its points
-      const ChunkT rc = chunk_ok(v) ? rawc[v] : (ChunkT)0;
+      for (int v = 0; v < V; ++v) {
+        // a chunk past the end: index 0, the null rank, for all its points
+        const ChunkT rc = chunk_ok(v) ? rawc[v] : (ChunkT)0;
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int ci = IC::get(rc, b);
-        const int xi = (rawx[v] >> (8 * b)) & 0xff;
-        const bool in = ci == grow_eta;
-        const int right = xi >= cutv;
-        cp[v][b] = in ? 2 * eta + right : ci;  // below 256: eta < 128
-        nr += __popcll(__ballot(in && right));  // wave-uniform
+        for (int b = 0; b < 4; ++b) {
+          const int ci = IC::get(rc, b);
+          const int xi = (rawx[v] >> (8 * b)) & 0xff;
+          const bool in = ci == grow_eta;
+          const int right = xi >= cutv;
+          cp[v][b] = in ? 2 * eta + right : ci;  // below 256: eta < 128
+          nr += __popcll(__ballot(in && right));  // wave-uniform
+        }
+      }
+    } else {
+      // not a GROW (a uniform branch): every point keeps its leaf, and the
+      // predictor bytes, loaded all the same, go unused
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        const ChunkT rc = chunk_ok(v) ? rawc[v] : (ChunkT)0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) cp[v][b] = IC::get(rc, b);
       }
     }
     int r0[V][4];
