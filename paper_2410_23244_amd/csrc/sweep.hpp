@@ -1453,9 +1453,11 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
   // rank kBadRank (likewise inert), and bad keeps the largest rank seen so
   // the pass can flag it.
   // (grow_eta: eta of a GROW, -1 otherwise; eta and cut of the proposal,
-  // read once per pass by the caller)
+  // read once per pass by the caller.  Without the rank stash, the GROW
+  // right-count into *nrb when given: a ballot per point, which there keeps
+  // fewer registers live than the packed-byte count of the stash kernels)
   auto ranks4 = [&](const Ctx &c, int grow_eta, int eta, int cutv, ChunkT rc, uint32_t rx,
-                    uint32_t &bad) -> uint32_t {
+                    uint32_t &bad, int *nrb) -> uint32_t {
     uint32_t pk = 0;
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
@@ -1464,6 +1466,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       const bool in = ci == grow_eta;
       const int right = xi >= cutv;
       const int r0 = c.rank_of[in ? 2 * eta + right : ci];  // slot below 256: eta < 128
+      if (!ST && nrb) *nrb += __popcll(__ballot(in && right));  // wave-uniform
       bad = max(bad, (uint32_t)r0);
       pk |= (uint32_t)r0 << (8 * b);
     }
@@ -1527,7 +1530,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
     // fewer leaves than the pass holds), every other rank (padding, an
     // inconsistent cache) goes to that spare slot, which no total reads and
     // the pass clears: no range test per point
-    const bool spare = lo == 0 && Ln < kPassRanks;
+    const bool spare = ST && lo == 0 && Ln < kPassRanks;
     // index rows of trees ja and jn: rows of the cache, or without one the
     // two rolling rows (by tree parity) that carry a tree's leaves from the
     // step that accumulates it to the step that applies it
@@ -1760,7 +1763,7 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           if (ST)
             rk = ok[u] ? stash[B.sl[u]] : kNull4;
           else
-            rk = ranks4(ca, grow_a, eta_a, cut_a, ra[u], xa4[u], bad);
+            rk = ranks4(ca, grow_a, eta_a, cut_a, ra[u], xa4[u], bad, nullptr);
           float dl[4];
 #pragma unroll
           for (int b = 0; b < 4; ++b) dl[b] = sh.dlt[(rk >> (8 * b)) & 0xff];
@@ -1801,12 +1804,12 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           } else {
             // (a uniform branch: a GROW's points of eta take a child; without
             // an index cache, the route of every pass measured faster)
-            if (CF || xn)
-              rk = ranks4(cn, grow_n, eta_n, cut_n, rn[u], xn4[u], bad);
+            if (CF || !ST || xn)
+              rk = ranks4(cn, grow_n, eta_n, cut_n, rn[u], xn4[u], bad, &nr);
             else
               rk = ranks4_plain(cn, rn[u], bad);
             if (ST && B.sl[u] >= 0) stash[B.sl[u]] = rk;  // after the read above
-            nr += zero_bytes(rk ^ right4);
+            if (ST) nr += zero_bytes(rk ^ right4);
           }
           // points b0..b0+kPos-1 go to kPos different bins, read together
           // and written together
@@ -1863,10 +1866,12 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
       compute_batch(B2);
     }
     if (bad == kBadRank) sh.dev_err = 1;  // bad: the largest rank seen
-    if (do_n && lo == 0) {
+    if (ST && do_n && lo == 0) {
       // per-lane counts (below 2^24) summed exactly over the wave
       const double tot = wave_total63((double)nr);
       if (lane == 63 && tot != 0.0) atomicAdd(&sh.nr[jn & 1], (int)tot);
+    } else if (!ST && do_n && lo == 0 && lane == 0 && nr) {
+      atomicAdd(&sh.nr[jn & 1], nr);  // wave-uniform
     }
     if (want_ssr) {
       const double tot = wave_total63(ssr);
