@@ -1286,12 +1286,17 @@ __device__ __forceinline__ void sweep_body(const SweepArgs *__restrict__ A, cons
         for (int v = 0; v < V; ++v) {
           bool touch = false;
           ChunkT out = 0;
+          // every rank's heap slot read unconditionally (no exec mask per
+          // point; ranks from kNullRank on have slot 0), then selected
+          int hs[4];
+#pragma unroll
+          for (int b = 0; b < 4; ++b) hs[b] = c.heap_of[(rk[v] >> (8 * b)) & 0xff];
 #pragma unroll
           for (int b = 0; b < 4; ++b) {
             const int rnk = (rk[v] >> (8 * b)) & 0xff;
             const bool pair = (rnk == kl) || (rnk == kr);
             touch |= pair;
-            out = IC::put(out, b, (merged && pair) ? eta : (int)c.heap_of[rnk]);
+            out = IC::put(out, b, (merged && pair) ? eta : hs[b]);
           }
           // only an existing chunk has a point of the move's pair
           if (touch) row[(w * V + v) * kBlock + t] = out;
@@ -1772,14 +1777,20 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           // the index row changes only under an accepted move
           bool touch = false;
           ChunkT out = 0;
-          if (changed)
+          if (changed) {
+            // every rank's heap slot read unconditionally (no exec mask per
+            // point; ranks from kNullRank on have slot 0), then selected
+            int hs[4];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) hs[b] = ca.heap_of[(rk >> (8 * b)) & 0xff];
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
               const int rnk = (rk >> (8 * b)) & 0xff;
               const bool pair = (rnk == kl) || (rnk == kr);
               touch |= pair;
-              out = IC::put(out, b, (merged && pair) ? eta_a : (int)ca.heap_of[rnk]);
+              out = IC::put(out, b, (merged && pair) ? eta_a : hs[b]);
             }
+          }
           if (B.inl[u])
             rcache[B.sl[u]] = rv[u];
           else if (ok[u])
