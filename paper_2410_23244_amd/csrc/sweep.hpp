@@ -1808,7 +1808,8 @@ __device__ __forceinline__ void sweep_body_stream(const SweepArgs *__restrict__ 
           // a private bin per lane and chunk position: the 4 points of a
           // chunk never share one, so the chunk is one batch of independent
           // read-modify-writes (chunks follow in LDS order); points of the
-          // null rank or outside the pass add 0 to a bin of the pass
+          // null rank or outside the pass go to the spare slot (spare) or add
+          // 0 to a bin of the pass
           uint32_t rk;
           if (ST && lo > 0) {
             rk = ok[u] ? stash[B.sl[u]] : kNull4;
